@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""Benchmark of the provenance-bound key path on one MI355X.
+
+One step = one pass of the whole hot path over one synthetic request batch, inputs resident in
+HBM: key offsets -> descriptor digests -> chained block keys -> longest-prefix lookup -> store of
+the misses (then the step's new entries are rolled back so that every step meets the same
+index).  The default workload is 1024 requests x 2048 tokens, block 16, against a 4M-slot index
+at load 0.5.
+
+Prints one JSON line: Gkeys/s (keys derived and probed per second), the derive kernel's share of
+the int32 VALU roofline, and the CPU oracle timed on the host cores.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X: 256 CUs x 4 SIMD16 = 64 int32 lanes per clock per CU, 2.4 GHz peak engine clock.
+CUS, LANES_PER_CU, CLOCK_HZ = 256, 64, 2.4e9
+INT_PEAK = CUS * LANES_PER_CU * CLOCK_HZ                  # 39.3 T int32 lane-ops/s
+OPS_PER_COMPRESSION = 1384                                # minimal gfx950 VALU lane-ops per SHA-256 block
+HBM_PEAK_GBS = 8000.0
+
+WORKLOAD_TEXT = {
+    "tiny": "8 req x 256 tok, block 16, 1K-slot index",
+    "c2": "1024 req x 2048 tok (64 shared prefixes), vocab 128256, block 16, 32 provenance classes, "
+          "4M-slot index at load 0.5",
+    "c3": "4096 req x 8192 tok, chunk 256, Zipf(1.1) over 512 prefixes, 16 descriptors, 512K-slot index",
+    "c4": "16384 req x 4096 tok, block 16, 20 dimensions, 64M-slot index with 2^25 entries",
+    "c5": "256 req x 131072 tok, block 16, groups of 4 with uniform fork points, 4M-slot index",
+}
+
+
+def compressions_per_key(block: int) -> int:
+    return (block + 11 + 15) // 16
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_TEXT))
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (0 = host cores, at most 16)")
+    p.add_argument("--calib-copy", action="store_true", help="run only a plain 1 GiB device copy (counter calibration)")
+    p.add_argument("--quiet", action="store_true")
+    return p.parse_args()
+
+
+def log(args, *a):
+    if not args.quiet:
+        print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def calib_copy():
+    import torch
+    n = 1 << 30
+    src = torch.ones(n // 4, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calib_copy_bytes": n}))
+
+
+def setup_gpu(args, w):
+    import paper_2609_38706_amd as pkv
+    from paper_2609_38706_amd.pipeline import DeviceBatch
+    from workloads import locations
+
+    table = pkv.Table(w.capacity)
+    for pre in (w.fill, w.warmup):
+        if pre is None:
+            continue
+        db = DeviceBatch.from_batch(pre)
+        db.set_locations(locations(db.key_off.cpu().numpy(), pre.tag))
+        db.digest()
+        db.derive()
+        if pre is w.warmup:
+            db.lookup(table)
+        else:
+            db.hits.zero_()
+        db.store(table)
+        if db.host_status() != 0:
+            raise RuntimeError(f"index preparation failed: status {db.host_status()}")
+        del db
+    run = DeviceBatch.from_batch(w.batch)
+    run.set_locations(locations(run.key_off.cpu().numpy(), w.batch.tag))
+    return pkv, table, run
+
+
+def gpu_leg(args, w):
+    import torch
+    pkv, table, run = setup_gpu(args, w)
+    stream = torch.cuda.current_stream()
+    n_keys = run.n_keys
+
+    def step(ev=None):
+        run.n_new.zero_()
+        run.key_offsets()
+        run.digest()
+        if ev is not None:
+            ev[0].record(stream)
+        run.derive()
+        if ev is not None:
+            ev[1].record(stream)
+        run.lookup(table)
+        if ev is not None:
+            ev[2].record(stream)
+        run.store(table)
+        if ev is not None:
+            ev[3].record(stream)
+        run.rollback(table)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if run.host_status() != 0:
+        raise RuntimeError(f"step failed: status {run.host_status()}")
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    if run.host_status() != 0:
+        raise RuntimeError(f"step failed: status {run.host_status()}")
+    ms = (t1 - t0) * 1e3 / args.steps
+    derive_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    lookup_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    store_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    hits = run.host_hits()
+    return {"ms": ms, "derive_ms": derive_ms, "lookup_ms": lookup_ms, "store_ms": store_ms, "n_keys": n_keys,
+            "n_req": run.n_req, "hit_blocks": int(hits.sum()), "new_entries": int(run.n_new.item())}
+
+
+def cpu_leg(args, w):
+    """The oracle as it stands, on the host cores: one full step of the same workload."""
+    import oracle
+    from workloads import locations
+
+    threads = args.cpu_threads or max(1, min(16, len(os.sched_getaffinity(0))))
+    idx = oracle.Index(w.capacity)
+    for pre in (w.fill, w.warmup):
+        if pre is None:
+            continue
+        ko = oracle.key_offsets(pre.tok_off, pre.block)
+        keys = oracle.derive(pre.tokens, pre.tok_off, oracle.batch_digests(pre), pre.block, threads)
+        hits = idx.lookup(keys, ko) if pre is w.warmup else np.zeros(pre.n_req, np.int32)
+        assert idx.store(keys, ko, hits, locations(ko, pre.tag)) == 0
+    b = w.batch
+    t0 = time.perf_counter()
+    digs = oracle.batch_digests(b)
+    ko = oracle.key_offsets(b.tok_off, b.block)
+    keys = oracle.derive(b.tokens, b.tok_off, digs, b.block, threads)
+    hits = idx.lookup(keys, ko)
+    rc = idx.store(keys, ko, hits, locations(ko, b.tag))
+    t1 = time.perf_counter()
+    assert rc == 0
+    n_keys = int(ko[-1])
+    return {"value": round(n_keys / (t1 - t0) / 1e9, 6), "unit": "Gkeys/s", "cores": threads, "kind": "oracle",
+            "sample": f"one full step of the same workload ({b.n_req} requests, {n_keys} keys): digests, "
+                      f"derive on {threads} threads, lookup and store single-threaded; {t1 - t0:.2f} s",
+            "seconds": round(t1 - t0, 3)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the path is measured at its "
+              f"one-GPU shape", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    if args.calib_copy:
+        calib_copy()
+        return
+    from workloads import make_workload
+    log(args, "generating workload", args.workload)
+    w = make_workload(args.workload)
+    log(args, "gpu leg")
+    g = gpu_leg(args, w)
+    log(args, "gpu leg done", g)
+    block = w.batch.block
+    ops = g["n_keys"] * compressions_per_key(block) * OPS_PER_COMPRESSION
+    achieved = ops / (g["derive_ms"] * 1e-3)
+    n_chains = w.batch.n_req
+    roofline = {"bound": "alu", "achieved": round(achieved / 1e12, 4), "peak": round(INT_PEAK / 1e12, 4),
+                "unit": "Tops/s", "frac": round(achieved / INT_PEAK, 5), "traffic": None,
+                "kernel": "derive", "ops_per_key": compressions_per_key(block) * OPS_PER_COMPRESSION,
+                "chain_ceiling_frac": round(min(1.0, n_chains / (CUS * 4 * 64)), 5)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(args, "cpu leg")
+        cpu = cpu_leg(args, w)
+    value = g["n_keys"] / (g["ms"] * 1e-3) / 1e9
+    out = {
+        "metric": "provenance-bound block keys derived+probed per second (Gkeys/s); % of roofline",
+        "value": round(value, 6), "unit": "Gkeys/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(g["ms"], 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u32", "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload, "requests": g["n_req"],
+                   "keys": g["n_keys"], "block": block, "capacity": w.capacity, "parallelism": "1 GPU"},
+        "kernels_ms": {"derive": round(g["derive_ms"], 4), "lookup": round(g["lookup_ms"], 4),
+                       "store": round(g["store_ms"], 4)},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,171 @@
+/* pkv.h -- provenance-bound shared-tier KV-cache keys on MI355X (gfx950).
+ *
+ * C ABI of the hot path of the KV provenance contract (paper section 5): a request's canonical
+ * provenance descriptor is encoded and digested (section 5.2, Eq. 3), the digest is folded into
+ * chained per-block keys, and the keys probe and then extend a shared-tier index held in HBM.
+ *
+ *   H(m)       = leftmost 16 bytes of SHA-256(m)                      (FIPS 180-4)
+ *   enc(c)     = "PKV1" | u32le(m) | per present field, in canonical order:
+ *                u32le(|name|) | name | u32le(|value|) | value         (section 5.2, Eq. 3)
+ *   d          = H(enc(c))                                            (the descriptor digest)
+ *   key_0      = 16 zero bytes
+ *   key_i      = H(key_{i-1} | d | LE32 token ids of block i),  i = 1 .. floor(L / B)
+ *   hit_r      = largest h such that key_{r,1..h} are all in the index (a longest-prefix hit)
+ *   store      : key_{r,j}, j > hit_r, is inserted if absent; among equal keys of one batch the
+ *                smallest location wins; entries already present are never modified
+ *                (section 3.4: a hit returns the first entry written).
+ *
+ * Canonical order (section 5.1 registry; Prop. 1 appends further dimensions): the six core
+ * dimensions model_id, adapter_id, weight_dtype, weight_version, kv_format, salt in that order,
+ * then any further registered dimension by unsigned byte order of its name (a proper prefix
+ * first).  An absent dimension is simply not passed, so a request that carries no adapter and
+ * no salt keys independently of those two registry entries (section 5.3, request-level tags).
+ * Lookup and store take the same key array, so both access sites bind the same descriptor
+ * (section 5.3, cross-site consistency).
+ *
+ * Conventions
+ *   - "d_" pointers are device memory owned by the caller; nothing here allocates or frees.
+ *   - Device calls are asynchronous on the given stream and never synchronize.  Argument errors
+ *     that the host can see are returned synchronously as negative codes (and described by
+ *     pkv_last_error()).  Errors found by a kernel (inconsistent offsets, a reserved location, a
+ *     full index) are written to the caller's int32 device status word: a kernel only ever
+ *     replaces 0 by the first error code it meets, so one zeroed word can serve a whole batch.
+ *   - Keys are 16 bytes, stored exactly as the leftmost 16 SHA-256 output bytes.
+ *   - Request boundaries are int64 offsets: tokens of request r are tok[tok_off[r] ..
+ *     tok_off[r+1]); its keys are keys[key_off[r] .. key_off[r+1]) with key_off[r+1]-key_off[r]
+ *     = floor((tok_off[r+1]-tok_off[r]) / B).  A request shorter than one block has no key.
+ *   - Locations are caller-defined 64-bit values below PKV_LOC_LIMIT (the top two bits are
+ *     reserved for the insert protocol).
+ *   - Device errors leave the index contents unspecified.
+ */
+#ifndef PKV_H
+#define PKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    PKV_OK = 0,
+    PKV_EINVAL = -1,     /* a malformed argument */
+    PKV_EDUPDIM = -2,    /* two descriptor fields share a name */
+    PKV_ERESERVED = -3,  /* a location >= PKV_LOC_LIMIT */
+    PKV_EFULL = -4,      /* the index has no free slot for a new key */
+    PKV_EHIP = -5,       /* a HIP runtime call failed */
+    PKV_ELAYOUT = -6,    /* device offsets inconsistent with each other or with buffer sizes */
+    PKV_ESTALL = -7,     /* an insert waited too long on a slot another lane had claimed */
+};
+
+#define PKV_LOC_LIMIT (1ULL << 62)
+#define PKV_KEY_BYTES 16
+
+/* One provenance dimension: its registered name and its identity value, both raw bytes
+ * (section 5.1: id_i maps a runtime value to a stable, cross-worker identity). */
+typedef struct {
+    const uint8_t* name;
+    uint32_t name_len;
+    const uint8_t* value;
+    uint32_t value_len;
+} pkv_field;
+
+/* The shared-tier index (section 2.1 shared KV-cache tier): open addressing over 4-slot
+ * buckets of 64 bytes, struct-of-arrays in HBM.
+ *   keys     : capacity x 16 bytes, 64-byte aligned.
+ *   locs     : capacity + 1 words (the extra word serves the one key that equals the
+ *              all-0xFF empty marker).
+ *   capacity : a power of two, >= 4.
+ * The struct itself is host memory; the arrays are device memory owned by the caller. */
+typedef struct {
+    uint8_t* keys;
+    uint64_t* locs;
+    uint64_t capacity;
+} pkv_table;
+
+/* ---- host, pure, thread-safe ------------------------------------------------------------- */
+
+/* Canonical encoding enc(c) of the n fields (section 5.2, Eq. 3), in any input order.  Writes
+ * at most cap bytes to out (out may be NULL when cap is 0); *out_len always receives the full
+ * length.  Returns PKV_EDUPDIM if two fields share a name, PKV_EINVAL if out is too small. */
+int pkv_descriptor_encode(const pkv_field* fields, size_t n, uint8_t* out, size_t cap, size_t* out_len);
+
+/* d = H(enc(c)) for one descriptor, on the host (the per-request digest of section 6.5). */
+int pkv_descriptor_digest(const pkv_field* fields, size_t n, uint8_t out[16]);
+
+/* ---- device, asynchronous on stream ------------------------------------------------------ */
+
+/* Batched descriptor digests on the GPU: d_digests[i] = H(bytes[msg_off[i] .. msg_off[i] +
+ * msg_len[i])) for i < n_msg, where each message is a canonical encoding (pkv_descriptor_encode).
+ * Messages may overlap, so requests sharing a descriptor can point at one copy.
+ * d_bytes: n_bytes bytes.  d_msg_off: n_msg int64.  d_msg_len: n_msg uint32.
+ * d_digests: n_msg x 16 bytes, 16-byte aligned.  A message outside [0, n_bytes) sets
+ * PKV_ELAYOUT in *d_status and yields no digest. */
+int pkv_digest_batch(const uint8_t* d_bytes, uint64_t n_bytes, const int64_t* d_msg_off,
+                     const uint32_t* d_msg_len, uint32_t n_msg, uint8_t* d_digests,
+                     int32_t* d_status, hipStream_t stream);
+
+/* d_key_off[r] = sum over q < r of floor((tok_off[q+1] - tok_off[q]) / block), r = 0..n_req
+ * (section 4.4: only complete chunks are keyed).  d_tok_off and d_key_off: n_req + 1 int64.
+ * block >= 1.  Offsets must be non-decreasing. */
+int pkv_key_offsets(const int64_t* d_tok_off, uint32_t n_req, uint32_t block, int64_t* d_key_off,
+                    hipStream_t stream);
+
+/* Chained block keys of n_req requests (section 5.2, Eq. 3 with f = the chained block key).
+ * d_tokens: n_tokens int32 token ids.  d_tok_off: n_req + 1 int64.  d_digests: n_req x 16
+ * bytes (16-byte aligned), one descriptor digest per request.  d_key_off: n_req + 1 int64 as
+ * produced by pkv_key_offsets.  d_keys: n_keys x 16 bytes (16-byte aligned).  A request whose
+ * offsets fall outside the buffers or disagree with floor(len / block) sets PKV_ELAYOUT and
+ * writes no key. */
+int pkv_derive_keys(const int32_t* d_tokens, uint64_t n_tokens, const int64_t* d_tok_off,
+                    uint32_t n_req, const uint8_t* d_digests, uint32_t block,
+                    const int64_t* d_key_off, uint64_t n_keys, uint8_t* d_keys,
+                    int32_t* d_status, hipStream_t stream);
+
+/* Marks every slot of the index empty. */
+int pkv_table_init(const pkv_table* table, hipStream_t stream);
+
+/* Longest-prefix hit per request (section 3.4 / 4.1: the prefix a shared tier can serve):
+ * d_hit_blocks[r] = largest h with keys key_off[r] .. key_off[r] + h - 1 all present.
+ * d_keys: n_keys x 16 bytes; d_key_off: n_req + 1 int64; d_hit_blocks: n_req int32. */
+int pkv_lookup_prefix(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off,
+                      uint32_t n_req, uint64_t n_keys, int32_t* d_hit_blocks, int32_t* d_status,
+                      hipStream_t stream);
+
+/* Store path: inserts key j (0-based) of request r with location d_locs[key_off[r] + j] for
+ * every j >= d_hit_blocks[r], unless the key is already present.  Duplicates inside the batch
+ * keep the smallest location; entries present before the call are never changed.
+ * d_locs: n_keys uint64 (< PKV_LOC_LIMIT, else PKV_ERESERVED).
+ * d_n_new: one uint64 counter that the call increments by the number of new entries; the
+ * caller zeroes it.  d_new_slots: NULL, or room for n_keys uint64: the slot index of each new
+ * entry is appended at d_new_slots[old *d_n_new ...] (the all-0xFF key's slot is `capacity`).
+ * No free slot for a new key sets PKV_EFULL. */
+int pkv_store(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off,
+              uint32_t n_req, uint64_t n_keys, const int32_t* d_hit_blocks, const uint64_t* d_locs,
+              uint64_t* d_new_slots, uint64_t* d_n_new, int32_t* d_status, hipStream_t stream);
+
+/* Undoes the stores whose new slots were logged in d_new_slots[0 .. *d_n_new) (at most
+ * max_slots), provided nothing else was inserted since: the index returns to its earlier
+ * contents exactly.  *d_n_new is left as is. */
+int pkv_table_rollback(const pkv_table* table, const uint64_t* d_new_slots, const uint64_t* d_n_new,
+                       uint64_t max_slots, hipStream_t stream);
+
+/* Copies every occupied (key, location) pair out, in no particular order.  d_keys_out: room for
+ * capacity + 1 keys; d_locs_out: capacity + 1 words; *d_count receives the number of pairs (the
+ * call zeroes it first). */
+int pkv_table_export(const pkv_table* table, uint8_t* d_keys_out, uint64_t* d_locs_out,
+                     uint64_t* d_count, hipStream_t stream);
+
+/* Text describing the last non-OK return on this thread. */
+const char* pkv_last_error(void);
+
+/* Library version string. */
+const char* pkv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -328,6 +328,12 @@ int orc_lookup(const orc_index* t, const uint8_t* keys, const int64_t* key_off, 
 
 #define ORC_LOC_LIMIT ((uint64_t)1 << 62)
 
+static int all_ff(const uint8_t key[16]) {
+    for (int i = 0; i < 16; ++i)
+        if (key[i] != 0xFF) return 0;
+    return 1;
+}
+
 int orc_store(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
               const int32_t* hits, const uint64_t* locs) {
     /* S = every (k_{r,j}, loc_{r,j}) with j >= h_r */
@@ -358,7 +364,12 @@ int orc_store(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_
         if (contains(t, s[i].key)) continue;
         s[n_new++] = s[i];                       /* compact the new keys in place, still sorted */
     }
-    if (t->size + n_new > t->capacity) { free(s); return ORC_EFULL; }
+    /* Capacity counts ordinary keys; the one key whose 16 bytes are all 0xFF has a reserved
+     * place of its own (that byte pattern marks an empty slot of the index). */
+    uint64_t ordinary = 0;
+    for (uint64_t i = 0; i < t->size; ++i) ordinary += !all_ff(t->e[i].key);
+    for (uint64_t i = 0; i < n_new; ++i) ordinary += !all_ff(s[i].key);
+    if (ordinary > t->capacity) { free(s); return ORC_EFULL; }
     /* merge the two sorted runs */
     entry* m = (entry*)malloc(sizeof(entry) * ((t->size + n_new) ? (t->size + n_new) : 1));
     if (!m) { free(s); return ORC_EINVAL; }

@@ -15,6 +15,8 @@
  *   lookup: h_r = largest h with k_{r,1..h} all in the index
  *   store:  every k_{r,j}, j > h_r, absent from the index is inserted once; among duplicates in
  *           one batch the smallest location wins; entries already present are never changed.
+ *   capacity: an index of capacity C holds at most C keys other than the all-0xFF key, which has
+ *           a reserved place of its own.
  *
  * Canonical order: the six core dimensions first, in the fixed registry order
  *   model_id, adapter_id, weight_dtype, weight_version, kv_format, salt,

@@ -1,0 +1,206 @@
+"""Python binding of the pkv C ABI (include/pkv.h): provenance-bound shared-tier KV-cache keys on
+MI355X.  Argument marshalling only -- every step runs in the HIP library ``lib/libpkv.so``.
+
+Device buffers are torch tensors on the current HIP device; uint64 buffers are int64 tensors with
+the same bits.  Every device call is asynchronous on ``stream`` (default: torch's current stream).
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+from ._build import LIB_PATH, build  # noqa: F401
+
+PKV_OK, PKV_EINVAL, PKV_EDUPDIM, PKV_ERESERVED, PKV_EFULL, PKV_EHIP, PKV_ELAYOUT, PKV_ESTALL = 0, -1, -2, -3, -4, -5, -6, -7
+PKV_LOC_LIMIT = 1 << 62
+ERROR_NAMES = {0: "PKV_OK", -1: "PKV_EINVAL", -2: "PKV_EDUPDIM", -3: "PKV_ERESERVED", -4: "PKV_EFULL",
+               -5: "PKV_EHIP", -6: "PKV_ELAYOUT", -7: "PKV_ESTALL"}
+
+EXPORTED = ["pkv_descriptor_encode", "pkv_descriptor_digest", "pkv_digest_batch", "pkv_key_offsets",
+            "pkv_derive_keys", "pkv_table_init", "pkv_lookup_prefix", "pkv_store", "pkv_table_rollback",
+            "pkv_table_export", "pkv_last_error", "pkv_version"]
+
+
+class PkvError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERROR_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+class pkv_field(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char_p), ("name_len", ctypes.c_uint32),
+                ("value", ctypes.c_char_p), ("value_len", ctypes.c_uint32)]
+
+
+class pkv_table(ctypes.Structure):
+    _fields_ = [("keys", ctypes.c_void_p), ("locs", ctypes.c_void_p), ("capacity", ctypes.c_uint64)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library.  Raises if it has not been built: there is no fallback."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"the pkv HIP library is not built ({LIB_PATH}); run __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        P, U32, U64, I32 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int
+        sig = {
+            "pkv_descriptor_encode": [P, ctypes.c_size_t, P, ctypes.c_size_t, P],
+            "pkv_descriptor_digest": [P, ctypes.c_size_t, P],
+            "pkv_digest_batch": [P, U64, P, P, U32, P, P, P],
+            "pkv_key_offsets": [P, U32, U32, P, P],
+            "pkv_derive_keys": [P, U64, P, U32, P, U32, P, U64, P, P, P],
+            "pkv_table_init": [P, P],
+            "pkv_lookup_prefix": [P, P, P, U32, U64, P, P, P],
+            "pkv_store": [P, P, P, U32, U64, P, P, P, P, P, P],
+            "pkv_table_rollback": [P, P, P, U64, P],
+            "pkv_table_export": [P, P, P, P, P],
+        }
+        for name, args in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = I32
+        L.pkv_last_error.restype = ctypes.c_char_p
+        L.pkv_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != PKV_OK:
+        raise PkvError(rc, lib().pkv_last_error().decode(errors="replace"))
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t, dtype=None, device=True):
+    if t is None:
+        return None
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"expected {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    if device and not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _fields(desc):
+    arr = (pkv_field * max(1, len(desc)))()
+    keep = []
+    for i, (n, v) in enumerate(desc):
+        n, v = bytes(n), bytes(v)
+        keep += [n, v]
+        arr[i] = pkv_field(n, len(n), v, len(v))
+    return arr, keep
+
+
+# ---- host -------------------------------------------------------------------------------------
+
+def pkv_descriptor_encode(desc) -> bytes:
+    arr, _keep = _fields(desc)
+    n = ctypes.c_size_t(0)
+    _check(lib().pkv_descriptor_encode(arr, len(desc), None, 0, ctypes.byref(n)))
+    out = (ctypes.c_uint8 * n.value)()
+    _check(lib().pkv_descriptor_encode(arr, len(desc), out, n.value, ctypes.byref(n)))
+    return bytes(out)
+
+
+def pkv_descriptor_digest(desc) -> bytes:
+    arr, _keep = _fields(desc)
+    out = (ctypes.c_uint8 * 16)()
+    _check(lib().pkv_descriptor_digest(arr, len(desc), out))
+    return bytes(out)
+
+
+# ---- device -----------------------------------------------------------------------------------
+
+def pkv_digest_batch(pool, msg_off, msg_len, digests, status, stream=None):
+    import torch
+    _check(lib().pkv_digest_batch(_ptr(pool, torch.uint8), pool.numel(), _ptr(msg_off, torch.int64),
+                                  _ptr(msg_len, torch.int32), msg_off.numel(), _ptr(digests, torch.uint8),
+                                  _ptr(status, torch.int32), _stream(stream)))
+
+
+def pkv_key_offsets(tok_off, block, key_off, stream=None):
+    import torch
+    _check(lib().pkv_key_offsets(_ptr(tok_off, torch.int64), tok_off.numel() - 1, block,
+                                 _ptr(key_off, torch.int64), _stream(stream)))
+
+
+def pkv_derive_keys(tokens, tok_off, digests, block, key_off, keys, status, stream=None):
+    import torch
+    _check(lib().pkv_derive_keys(_ptr(tokens, torch.int32), tokens.numel(), _ptr(tok_off, torch.int64),
+                                 tok_off.numel() - 1, _ptr(digests, torch.uint8), block,
+                                 _ptr(key_off, torch.int64), keys.numel() // 16, _ptr(keys, torch.uint8),
+                                 _ptr(status, torch.int32), _stream(stream)))
+
+
+class Table:
+    """Device arrays of one index: ``keys`` uint8 [capacity, 16], ``locs`` int64 [capacity + 1]."""
+
+    def __init__(self, capacity: int, device="cuda", init=True, stream=None):
+        import torch
+        if capacity < 4 or capacity & (capacity - 1):
+            raise ValueError("capacity must be a power of two >= 4")
+        self.capacity = capacity
+        self.keys = torch.empty((capacity, 16), dtype=torch.uint8, device=device)
+        self.locs = torch.empty(capacity + 1, dtype=torch.int64, device=device)
+        if init:
+            pkv_table_init(self, stream)
+
+    def struct(self) -> pkv_table:
+        return pkv_table(self.keys.data_ptr(), self.locs.data_ptr(), self.capacity)
+
+    def copy_from(self, other: "Table"):
+        self.keys.copy_(other.keys)
+        self.locs.copy_(other.locs)
+
+
+def pkv_table_init(table: Table, stream=None):
+    t = table.struct()
+    _check(lib().pkv_table_init(ctypes.byref(t), _stream(stream)))
+
+
+def pkv_lookup_prefix(table: Table, keys, key_off, hits, status, stream=None):
+    import torch
+    t = table.struct()
+    _check(lib().pkv_lookup_prefix(ctypes.byref(t), _ptr(keys, torch.uint8), _ptr(key_off, torch.int64),
+                                   key_off.numel() - 1, keys.numel() // 16, _ptr(hits, torch.int32),
+                                   _ptr(status, torch.int32), _stream(stream)))
+
+
+def pkv_store(table: Table, keys, key_off, hits, locs, n_new, status, new_slots=None, stream=None):
+    import torch
+    t = table.struct()
+    _check(lib().pkv_store(ctypes.byref(t), _ptr(keys, torch.uint8), _ptr(key_off, torch.int64),
+                           key_off.numel() - 1, keys.numel() // 16, _ptr(hits, torch.int32),
+                           _ptr(locs, torch.int64), _ptr(new_slots, torch.int64), _ptr(n_new, torch.int64),
+                           _ptr(status, torch.int32), _stream(stream)))
+
+
+def pkv_table_rollback(table: Table, new_slots, n_new, stream=None):
+    import torch
+    t = table.struct()
+    _check(lib().pkv_table_rollback(ctypes.byref(t), _ptr(new_slots, torch.int64), _ptr(n_new, torch.int64),
+                                    new_slots.numel(), _stream(stream)))
+
+
+def pkv_table_export(table: Table, keys_out, locs_out, count, stream=None):
+    import torch
+    t = table.struct()
+    _check(lib().pkv_table_export(ctypes.byref(t), _ptr(keys_out, torch.uint8), _ptr(locs_out, torch.int64),
+                                  _ptr(count, torch.int64), _stream(stream)))
+
+
+def version() -> str:
+    return lib().pkv_version().decode()

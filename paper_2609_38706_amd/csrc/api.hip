@@ -1,0 +1,276 @@
+// api.cpp -- the C ABI (include/pkv.h): argument checks, the host-side canonical descriptor
+// encoder and digest, and the launches of the HIP kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <vector>
+
+#include "pkv.h"
+#include "pkv_internal.h"
+
+namespace pkv {
+
+namespace {
+thread_local char g_error[512] = "no error";
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+bool pow2(uint64_t x) { return x && !(x & (x - 1)); }
+
+// ---- canonical order (section 5.1 registry, section 5.2 Eq. 3, Prop. 1) -----------------------
+constexpr const char* kCoreNames[6] = {"model_id", "adapter_id", "weight_dtype",
+                                       "weight_version", "kv_format", "salt"};
+
+struct Ref {
+    const pkv_field* f;
+    int rank;   // 0..5 core dimension, 6 further dimension
+};
+
+int rank_of(const pkv_field& f) {
+    for (int i = 0; i < 6; ++i) {
+        const size_t n = std::strlen(kCoreNames[i]);
+        if (f.name_len == n && std::memcmp(f.name, kCoreNames[i], n) == 0) return i;
+    }
+    return 6;
+}
+
+bool name_less(const pkv_field& a, const pkv_field& b) {
+    return std::lexicographical_compare(a.name, a.name + a.name_len, b.name, b.name + b.name_len);
+}
+bool name_equal(const pkv_field& a, const pkv_field& b) {
+    return a.name_len == b.name_len && (a.name_len == 0 || std::memcmp(a.name, b.name, a.name_len) == 0);
+}
+
+int canonicalize(const pkv_field* fields, size_t n, std::vector<Ref>& out) {
+    out.clear();
+    out.reserve(n);
+    for (size_t i = 0; i < n; ++i) {
+        const pkv_field& f = fields[i];
+        if ((f.name_len && !f.name) || (f.value_len && !f.value))
+            return set_error(PKV_EINVAL, "pkv_descriptor: field %zu has a null pointer", i);
+        out.push_back(Ref{&f, rank_of(f)});
+    }
+    // unsigned byte order, a proper prefix first (lexicographical_compare on uint8_t)
+    std::sort(out.begin(), out.end(), [](const Ref& a, const Ref& b) {
+        if (a.rank != b.rank) return a.rank < b.rank;
+        return name_less(*a.f, *b.f);
+    });
+    for (size_t i = 1; i < out.size(); ++i)
+        if (name_equal(*out[i].f, *out[i - 1].f))
+            return set_error(PKV_EDUPDIM, "pkv_descriptor: dimension name given twice");
+    return PKV_OK;
+}
+
+void put32(uint8_t* p, uint32_t v) {
+    p[0] = static_cast<uint8_t>(v);
+    p[1] = static_cast<uint8_t>(v >> 8);
+    p[2] = static_cast<uint8_t>(v >> 16);
+    p[3] = static_cast<uint8_t>(v >> 24);
+}
+
+// ---- host SHA-256 for single descriptors --------------------------------------------------
+inline uint32_t hrotr(uint32_t x, int n) { return (x >> n) | (x << (32 - n)); }
+
+void host_block(uint32_t st[8], const uint8_t* p) {
+    uint32_t w[64];
+    for (int t = 0; t < 16; ++t)
+        w[t] = (uint32_t(p[4 * t]) << 24) | (uint32_t(p[4 * t + 1]) << 16) | (uint32_t(p[4 * t + 2]) << 8) |
+               uint32_t(p[4 * t + 3]);
+    for (int t = 16; t < 64; ++t) {
+        const uint32_t s0 = hrotr(w[t - 15], 7) ^ hrotr(w[t - 15], 18) ^ (w[t - 15] >> 3);
+        const uint32_t s1 = hrotr(w[t - 2], 17) ^ hrotr(w[t - 2], 19) ^ (w[t - 2] >> 10);
+        w[t] = w[t - 16] + s0 + w[t - 7] + s1;
+    }
+    uint32_t v[8];
+    std::memcpy(v, st, sizeof v);
+    for (int t = 0; t < 64; ++t) {
+        const uint32_t e = v[4], a = v[0];
+        const uint32_t t1 = v[7] + (hrotr(e, 6) ^ hrotr(e, 11) ^ hrotr(e, 25)) + ((e & v[5]) ^ (~e & v[6])) +
+                            kRoundK[t] + w[t];
+        const uint32_t t2 = (hrotr(a, 2) ^ hrotr(a, 13) ^ hrotr(a, 22)) + ((a & v[1]) ^ (a & v[2]) ^ (v[1] & v[2]));
+        std::memmove(v + 1, v, 7 * sizeof(uint32_t));
+        v[4] += t1;
+        v[0] = t1 + t2;
+    }
+    for (int i = 0; i < 8; ++i) st[i] += v[i];
+}
+
+void host_digest16(const uint8_t* m, size_t len, uint8_t out[16]) {
+    uint32_t st[8];
+    std::memcpy(st, kInitH, sizeof st);
+    size_t done = 0;
+    for (; done + 64 <= len; done += 64) host_block(st, m + done);
+    uint8_t tail[128] = {0};
+    const size_t rest = len - done;
+    std::memcpy(tail, m + done, rest);
+    tail[rest] = 0x80;
+    const size_t tl = rest < 56 ? 64 : 128;
+    const uint64_t bits = static_cast<uint64_t>(len) * 8;
+    for (int i = 0; i < 8; ++i) tail[tl - 8 + i] = static_cast<uint8_t>(bits >> (56 - 8 * i));
+    host_block(st, tail);
+    if (tl == 128) host_block(st, tail + 64);
+    for (int i = 0; i < 4; ++i) {
+        out[4 * i] = static_cast<uint8_t>(st[i] >> 24);
+        out[4 * i + 1] = static_cast<uint8_t>(st[i] >> 16);
+        out[4 * i + 2] = static_cast<uint8_t>(st[i] >> 8);
+        out[4 * i + 3] = static_cast<uint8_t>(st[i]);
+    }
+}
+
+int check_table(const pkv_table* t, const char* what) {
+    if (!t) return set_error(PKV_EINVAL, "%s: null table", what);
+    if (!t->keys || !t->locs) return set_error(PKV_EINVAL, "%s: null table arrays", what);
+    if (!pow2(t->capacity) || t->capacity < kSlotsPerBucket)
+        return set_error(PKV_EINVAL, "%s: capacity %llu is not a power of two >= 4", what,
+                         static_cast<unsigned long long>(t->capacity));
+    if (!aligned(t->keys, 64)) return set_error(PKV_EINVAL, "%s: table keys not 64-byte aligned", what);
+    if (!aligned(t->locs, 8)) return set_error(PKV_EINVAL, "%s: table locations not 8-byte aligned", what);
+    return PKV_OK;
+}
+}  // namespace
+
+int set_error(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_error, sizeof g_error, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int check_launch(const char* what) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return set_error(PKV_EHIP, "%s: %s", what, hipGetErrorString(e));
+    return PKV_OK;
+}
+
+}  // namespace pkv
+
+using namespace pkv;
+
+extern "C" {
+
+const char* pkv_last_error(void) { return g_error; }
+
+const char* pkv_version(void) { return "pkv 0.1 gfx950"; }
+
+int pkv_descriptor_encode(const pkv_field* fields, size_t n, uint8_t* out, size_t cap, size_t* out_len) {
+    if (!out_len || (n && !fields)) return set_error(PKV_EINVAL, "pkv_descriptor_encode: null argument");
+    if (n > 0xFFFFFFFFull) return set_error(PKV_EINVAL, "pkv_descriptor_encode: too many fields");
+    std::vector<Ref> order;
+    int rc = canonicalize(fields, n, order);
+    if (rc) return rc;
+    size_t len = 8;
+    for (const Ref& r : order) len += 8 + size_t(r.f->name_len) + size_t(r.f->value_len);
+    *out_len = len;
+    if (len > cap) return out ? set_error(PKV_EINVAL, "pkv_descriptor_encode: buffer of %zu bytes, need %zu",
+                                          cap, len)
+                              : PKV_OK;
+    if (!out) return set_error(PKV_EINVAL, "pkv_descriptor_encode: null output");
+    uint8_t* p = out;
+    std::memcpy(p, "PKV1", 4);
+    put32(p + 4, static_cast<uint32_t>(n));
+    p += 8;
+    for (const Ref& r : order) {
+        put32(p, r.f->name_len);
+        if (r.f->name_len) std::memcpy(p + 4, r.f->name, r.f->name_len);
+        p += 4 + r.f->name_len;
+        put32(p, r.f->value_len);
+        if (r.f->value_len) std::memcpy(p + 4, r.f->value, r.f->value_len);
+        p += 4 + r.f->value_len;
+    }
+    return PKV_OK;
+}
+
+int pkv_descriptor_digest(const pkv_field* fields, size_t n, uint8_t out[16]) {
+    if (!out) return set_error(PKV_EINVAL, "pkv_descriptor_digest: null output");
+    size_t len = 0;
+    int rc = pkv_descriptor_encode(fields, n, nullptr, 0, &len);
+    if (rc) return rc;
+    std::vector<uint8_t> buf(len);
+    rc = pkv_descriptor_encode(fields, n, buf.data(), buf.size(), &len);
+    if (rc) return rc;
+    host_digest16(buf.data(), len, out);
+    return PKV_OK;
+}
+
+int pkv_digest_batch(const uint8_t* d_bytes, uint64_t n_bytes, const int64_t* d_msg_off, const uint32_t* d_msg_len,
+                     uint32_t n_msg, uint8_t* d_digests, int32_t* d_status, hipStream_t stream) {
+    if (n_msg == 0) return PKV_OK;
+    if ((!d_bytes && n_bytes) || !d_msg_off || !d_msg_len || !d_digests || !d_status)
+        return set_error(PKV_EINVAL, "pkv_digest_batch: null argument");
+    if (!aligned(d_digests, 16)) return set_error(PKV_EINVAL, "pkv_digest_batch: digests not 16-byte aligned");
+    return launch_digest_batch(d_bytes, n_bytes, d_msg_off, d_msg_len, n_msg, d_digests, d_status, stream);
+}
+
+int pkv_key_offsets(const int64_t* d_tok_off, uint32_t n_req, uint32_t block, int64_t* d_key_off,
+                    hipStream_t stream) {
+    if (!d_tok_off || !d_key_off) return set_error(PKV_EINVAL, "pkv_key_offsets: null argument");
+    if (block == 0) return set_error(PKV_EINVAL, "pkv_key_offsets: block size 0");
+    return launch_key_offsets(d_tok_off, n_req, block, d_key_off, stream);
+}
+
+int pkv_derive_keys(const int32_t* d_tokens, uint64_t n_tokens, const int64_t* d_tok_off, uint32_t n_req,
+                    const uint8_t* d_digests, uint32_t block, const int64_t* d_key_off, uint64_t n_keys,
+                    uint8_t* d_keys, int32_t* d_status, hipStream_t stream) {
+    if (block == 0) return set_error(PKV_EINVAL, "pkv_derive_keys: block size 0");
+    if (n_req == 0) return PKV_OK;
+    if ((!d_tokens && n_tokens) || !d_tok_off || !d_digests || !d_key_off || (!d_keys && n_keys) || !d_status)
+        return set_error(PKV_EINVAL, "pkv_derive_keys: null argument");
+    if (!aligned(d_digests, 16) || !aligned(d_keys, 16))
+        return set_error(PKV_EINVAL, "pkv_derive_keys: digests and keys must be 16-byte aligned");
+    if (!aligned(d_tokens, 4)) return set_error(PKV_EINVAL, "pkv_derive_keys: tokens not 4-byte aligned");
+    return launch_derive(d_tokens, n_tokens, d_tok_off, n_req, d_digests, block, d_key_off, n_keys, d_keys, d_status,
+                         stream);
+}
+
+int pkv_table_init(const pkv_table* table, hipStream_t stream) {
+    int rc = check_table(table, "pkv_table_init");
+    if (rc) return rc;
+    return launch_table_init(table->keys, table->locs, table->capacity, stream);
+}
+
+int pkv_lookup_prefix(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off, uint32_t n_req,
+                      uint64_t n_keys, int32_t* d_hit_blocks, int32_t* d_status, hipStream_t stream) {
+    int rc = check_table(table, "pkv_lookup_prefix");
+    if (rc) return rc;
+    if (n_req == 0) return PKV_OK;
+    if ((!d_keys && n_keys) || !d_key_off || !d_hit_blocks || !d_status)
+        return set_error(PKV_EINVAL, "pkv_lookup_prefix: null argument");
+    if (!aligned(d_keys, 16)) return set_error(PKV_EINVAL, "pkv_lookup_prefix: keys not 16-byte aligned");
+    return launch_lookup(table->keys, table->locs, table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
+                         d_status, stream);
+}
+
+int pkv_store(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off, uint32_t n_req,
+              uint64_t n_keys, const int32_t* d_hit_blocks, const uint64_t* d_locs, uint64_t* d_new_slots,
+              uint64_t* d_n_new, int32_t* d_status, hipStream_t stream) {
+    int rc = check_table(table, "pkv_store");
+    if (rc) return rc;
+    if (n_req == 0) return PKV_OK;
+    if ((!d_keys && n_keys) || !d_key_off || !d_hit_blocks || (!d_locs && n_keys) || !d_n_new || !d_status)
+        return set_error(PKV_EINVAL, "pkv_store: null argument");
+    if (!aligned(d_keys, 16)) return set_error(PKV_EINVAL, "pkv_store: keys not 16-byte aligned");
+    return launch_store(table->keys, table->locs, table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
+                        d_locs, d_new_slots, d_n_new, d_status, stream);
+}
+
+int pkv_table_rollback(const pkv_table* table, const uint64_t* d_new_slots, const uint64_t* d_n_new,
+                       uint64_t max_slots, hipStream_t stream) {
+    int rc = check_table(table, "pkv_table_rollback");
+    if (rc) return rc;
+    if (max_slots && (!d_new_slots || !d_n_new)) return set_error(PKV_EINVAL, "pkv_table_rollback: null argument");
+    return launch_rollback(table->keys, table->locs, table->capacity, d_new_slots, d_n_new, max_slots, stream);
+}
+
+int pkv_table_export(const pkv_table* table, uint8_t* d_keys_out, uint64_t* d_locs_out, uint64_t* d_count,
+                     hipStream_t stream) {
+    int rc = check_table(table, "pkv_table_export");
+    if (rc) return rc;
+    if (!d_keys_out || !d_locs_out || !d_count) return set_error(PKV_EINVAL, "pkv_table_export: null argument");
+    if (!aligned(d_keys_out, 16)) return set_error(PKV_EINVAL, "pkv_table_export: output keys not 16-byte aligned");
+    return launch_export(table->keys, table->locs, table->capacity, d_keys_out, d_locs_out, d_count, stream);
+}
+
+}  // extern "C"

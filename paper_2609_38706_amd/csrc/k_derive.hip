@@ -1,0 +1,328 @@
+// k_derive.hip -- descriptor digests, key offsets and chained block keys on gfx950.
+//
+// Key chain (section 5.2, Eq. 3 with f = a chained block key):
+//   key_i = H(key_{i-1} | d | LE32 tokens of block i),  key_0 = 0^16,  H = SHA-256[0:16].
+// The message of one key is 32 + 4B bytes = 8 + B big-endian words:
+//   words 0-3   key_{i-1} (the previous SHA-256 state words H0..H3 feed straight back in),
+//   words 4-7   the descriptor digest,
+//   words 8..   the byte-swapped int32 tokens of the block,
+//   then FIPS 180-4 padding (0x80000000, zeros, 64-bit bit length).
+// A chain is strictly serial, so one lane owns one request and a wavefront owns 64 requests;
+// all work is 32-bit integer VALU (v_alignbit rotates, v_bitop3/v_bfi logic, v_add3 sums,
+// v_perm byte swaps).
+#include "pkv_internal.h"
+
+namespace pkv {
+namespace {
+
+using dev::bswap;
+using dev::compress;
+using dev::init_state;
+
+constexpr int kDeriveThreads = 64;   // one wavefront per workgroup: 64 independent chains
+
+struct ChainArgs {
+    const int32_t* tokens;
+    uint64_t n_tokens;
+    const int64_t* tok_off;
+    uint32_t n_req;
+    const uint8_t* digests;
+    uint32_t block;
+    const int64_t* key_off;
+    uint64_t n_keys;
+    uint8_t* keys;
+    int32_t* status;
+};
+
+// Loads request r's bounds and checks them against the buffers; false = skip this request.
+__device__ __forceinline__ bool chain_bounds(const ChainArgs& a, uint32_t r, int64_t& t0, int64_t& k0,
+                                             int64_t& n) {
+    t0 = a.tok_off[r];
+    const int64_t t1 = a.tok_off[r + 1];
+    k0 = a.key_off[r];
+    const int64_t k1 = a.key_off[r + 1];
+    const bool ok = t0 >= 0 && t1 >= t0 && static_cast<uint64_t>(t1) <= a.n_tokens && k0 >= 0 && k1 >= k0 &&
+                    static_cast<uint64_t>(k1) <= a.n_keys && (k1 - k0) == (t1 - t0) / a.block;
+    if (!ok) {
+        dev::report(a.status, PKV_ELAYOUT);
+        return false;
+    }
+    n = k1 - k0;
+    return true;
+}
+
+__device__ __forceinline__ void load_digest(const ChainArgs& a, uint32_t r, uint32_t d[4]) {
+    const uint4 v = reinterpret_cast<const uint4*>(a.digests)[r];
+    d[0] = bswap(v.x); d[1] = bswap(v.y); d[2] = bswap(v.z); d[3] = bswap(v.w);
+}
+
+__device__ __forceinline__ void store_key(uint8_t* keys, int64_t idx, const uint32_t s[8]) {
+    reinterpret_cast<uint4*>(keys)[idx] = make_uint4(bswap(s[0]), bswap(s[1]), bswap(s[2]), bswap(s[3]));
+}
+
+// ---- B = 16: two compressions per key; the next key's 16 tokens are prefetched -------------
+__global__ __launch_bounds__(kDeriveThreads) void k_derive_b16(ChainArgs a) {
+    const uint32_t r = blockIdx.x * kDeriveThreads + threadIdx.x;
+    if (r >= a.n_req) return;
+    int64_t t0, k0, n;
+    if (!chain_bounds(a, r, t0, k0, n)) return;
+    uint32_t dg[4], prev[4] = {0u, 0u, 0u, 0u};
+    load_digest(a, r, dg);
+    const int32_t* tp = a.tokens + t0;
+    uint32_t nxt[16];
+    if (n > 0) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) nxt[q] = static_cast<uint32_t>(tp[q]);
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t cur[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) cur[q] = nxt[q];
+        if (i + 1 < n) {
+            const int32_t* np = tp + (i + 1) * 16;
+#pragma unroll
+            for (int q = 0; q < 16; ++q) nxt[q] = static_cast<uint32_t>(np[q]);
+        }
+        uint32_t s[8], w[16];
+        init_state(s);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) { w[q] = prev[q]; w[4 + q] = dg[q]; }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) w[8 + q] = bswap(cur[q]);
+        compress(s, w);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) w[q] = bswap(cur[8 + q]);
+        w[8] = 0x80000000u;
+#pragma unroll
+        for (int q = 9; q < 15; ++q) w[q] = 0u;
+        w[15] = (32u + 4u * 16u) * 8u;
+        compress(s, w);
+        store_key(a.keys, k0 + i, s);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) prev[q] = s[q];
+    }
+}
+
+// ---- B = 16m, m >= 2: m + 1 compressions per key -------------------------------------------
+// Message blocks of one key: block 0 = prev | digest | tokens 0..7; block c (1..m-1) = tokens
+// 16c-8 .. 16c+7; block m = tokens 16m-8 .. 16m-1 | padding.  The token words of the next block
+// are fetched while the current one is compressed.
+__device__ __forceinline__ void load_chunk(const int32_t* tp, uint32_t c, uint32_t m, uint32_t out[16]) {
+    if (c == 0) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) out[q] = static_cast<uint32_t>(tp[q]);
+    } else if (c == m) {
+        const int32_t* p = tp + 16 * m - 8;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) out[q] = static_cast<uint32_t>(p[q]);
+    } else {
+        const int32_t* p = tp + 16 * c - 8;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) out[q] = static_cast<uint32_t>(p[q]);
+    }
+}
+
+__global__ __launch_bounds__(kDeriveThreads) void k_derive_m16(ChainArgs a) {
+    const uint32_t r = blockIdx.x * kDeriveThreads + threadIdx.x;
+    if (r >= a.n_req) return;
+    int64_t t0, k0, n;
+    if (!chain_bounds(a, r, t0, k0, n)) return;
+    const uint32_t m = a.block / 16;
+    const uint32_t bitlen = (32u + 4u * a.block) * 8u;
+    uint32_t dg[4], prev[4] = {0u, 0u, 0u, 0u};
+    load_digest(a, r, dg);
+    const int32_t* base = a.tokens + t0;
+    uint32_t nxt[16];
+    if (n > 0) load_chunk(base, 0, m, nxt);
+    for (int64_t i = 0; i < n; ++i) {
+        const int32_t* tp = base + i * a.block;
+        uint32_t s[8];
+        init_state(s);
+        for (uint32_t c = 0; c <= m; ++c) {
+            uint32_t cur[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) cur[q] = nxt[q];
+            if (c < m) load_chunk(tp, c + 1, m, nxt);
+            else if (i + 1 < n) load_chunk(tp + a.block, 0, m, nxt);
+            uint32_t w[16];
+            if (c == 0) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) { w[q] = prev[q]; w[4 + q] = dg[q]; }
+#pragma unroll
+                for (int q = 0; q < 8; ++q) w[8 + q] = bswap(cur[q]);
+            } else if (c == m) {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) w[q] = bswap(cur[q]);
+                w[8] = 0x80000000u;
+#pragma unroll
+                for (int q = 9; q < 15; ++q) w[q] = 0u;
+                w[15] = bitlen;
+            } else {
+#pragma unroll
+                for (int q = 0; q < 16; ++q) w[q] = bswap(cur[q]);
+            }
+            compress(s, w);
+        }
+        store_key(a.keys, k0 + i, s);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) prev[q] = s[q];
+    }
+}
+
+// ---- any B >= 1: message words selected one by one ------------------------------------------
+__global__ __launch_bounds__(kDeriveThreads) void k_derive_any(ChainArgs a) {
+    const uint32_t r = blockIdx.x * kDeriveThreads + threadIdx.x;
+    if (r >= a.n_req) return;
+    int64_t t0, k0, n;
+    if (!chain_bounds(a, r, t0, k0, n)) return;
+    const uint32_t B = a.block;
+    const uint32_t n_blocks = (B + 11u + 15u) / 16u;      // 8 + B message words, 1 pad word, 2 length words
+    const uint64_t bitlen = (32ull + 4ull * B) * 8ull;
+    uint32_t dg[4], prev[4] = {0u, 0u, 0u, 0u};
+    load_digest(a, r, dg);
+    for (int64_t i = 0; i < n; ++i) {
+        const int32_t* tp = a.tokens + t0 + i * static_cast<int64_t>(B);
+        uint32_t s[8];
+        init_state(s);
+        for (uint32_t c = 0; c < n_blocks; ++c) {
+            uint32_t w[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const uint32_t g = 16u * c + q;           // message word index
+                const uint32_t ti = g - 8u;               // token index when 8 <= g < 8 + B
+                const uint32_t tok = bswap(static_cast<uint32_t>(tp[ti < B ? ti : 0u]));
+                uint32_t v = 0u;
+                if (g < 4u) v = prev[q & 3];              // only reachable in block 0, q < 4
+                else if (g < 8u) v = dg[q & 3];
+                else if (ti < B) v = tok;
+                else if (g == 8u + B) v = 0x80000000u;
+                if (c + 1 == n_blocks) {
+                    if (q == 14) v = static_cast<uint32_t>(bitlen >> 32);
+                    if (q == 15) v = static_cast<uint32_t>(bitlen);
+                }
+                w[q] = v;
+            }
+            compress(s, w);
+        }
+        store_key(a.keys, k0 + i, s);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) prev[q] = s[q];
+    }
+}
+
+// ---- batched descriptor digests: one lane per canonical encoding ----------------------------
+__global__ __launch_bounds__(64) void k_digest(const uint8_t* bytes, uint64_t n_bytes, const int64_t* off,
+                                               const uint32_t* len, uint32_t n, uint8_t* out, int32_t* status) {
+    const uint32_t i = blockIdx.x * 64 + threadIdx.x;
+    if (i >= n) return;
+    const int64_t o = off[i];
+    const uint64_t L = len[i];
+    if (o < 0 || static_cast<uint64_t>(o) > n_bytes || L > n_bytes - static_cast<uint64_t>(o)) {
+        dev::report(status, PKV_ELAYOUT);
+        return;
+    }
+    const uint8_t* p = bytes + o;
+    const uint64_t n_blocks = (L + 9 + 63) / 64;
+    const uint64_t bitlen = L * 8;
+    uint32_t s[8];
+    init_state(s);
+    for (uint64_t c = 0; c < n_blocks; ++c) {
+        uint32_t w[16];
+        for (int q = 0; q < 16; ++q) {
+            uint32_t v = 0;
+            for (int b = 0; b < 4; ++b) {
+                const uint64_t pos = 64 * c + 4 * q + b;
+                const uint32_t byte = pos < L ? p[pos] : (pos == L ? 0x80u : 0u);
+                v = (v << 8) | byte;
+            }
+            w[q] = v;
+        }
+        if (c + 1 == n_blocks) {
+            w[14] = static_cast<uint32_t>(bitlen >> 32);
+            w[15] = static_cast<uint32_t>(bitlen);
+        }
+        compress(s, w);
+    }
+    reinterpret_cast<uint4*>(out)[i] = make_uint4(bswap(s[0]), bswap(s[1]), bswap(s[2]), bswap(s[3]));
+}
+
+// ---- key offsets: one workgroup scans floor(len / B) over all requests ------------------------
+constexpr int kScanThreads = 1024;
+constexpr int kScanPerThread = 8;
+
+__global__ __launch_bounds__(kScanThreads) void k_key_offsets(const int64_t* tok_off, uint32_t n_req, uint32_t block,
+                                                             int64_t* key_off) {
+    __shared__ int64_t wave_sum[kScanThreads / 64];
+    __shared__ int64_t carry_sh;
+    const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid == 0) { carry_sh = 0; key_off[0] = 0; }
+    __syncthreads();
+    for (uint64_t base = 0; base < n_req; base += static_cast<uint64_t>(kScanThreads) * kScanPerThread) {
+        int64_t v[kScanPerThread];
+        int64_t mine = 0;
+#pragma unroll
+        for (int j = 0; j < kScanPerThread; ++j) {
+            const uint64_t r = base + static_cast<uint64_t>(tid) * kScanPerThread + j;
+            int64_t c = 0;
+            if (r < n_req) c = (tok_off[r + 1] - tok_off[r]) / block;
+            v[j] = c;
+            mine += c;
+        }
+        // inclusive scan of `mine` across the wave
+        int64_t incl = mine;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int64_t y = __shfl_up(incl, d, 64);
+            if (lane >= static_cast<uint32_t>(d)) incl += y;
+        }
+        if (lane == 63) wave_sum[wave] = incl;
+        __syncthreads();
+        int64_t wave_base = 0, total = 0;
+        for (uint32_t q = 0; q < kScanThreads / 64; ++q) {
+            if (q < wave) wave_base += wave_sum[q];
+            total += wave_sum[q];
+        }
+        int64_t run = carry_sh + wave_base + incl - mine;
+#pragma unroll
+        for (int j = 0; j < kScanPerThread; ++j) {
+            const uint64_t r = base + static_cast<uint64_t>(tid) * kScanPerThread + j;
+            run += v[j];
+            if (r < n_req) key_off[r + 1] = run;
+        }
+        __syncthreads();
+        if (tid == 0) carry_sh += total;
+        __syncthreads();
+    }
+}
+
+}  // namespace
+
+int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_off, uint32_t n_req,
+                  const uint8_t* digests, uint32_t block, const int64_t* key_off, uint64_t n_keys, uint8_t* keys,
+                  int32_t* status, hipStream_t s) {
+    if (n_req == 0) return PKV_OK;
+    ChainArgs a{tokens, n_tokens, tok_off, n_req, digests, block, key_off, n_keys, keys, status};
+    const dim3 grid((n_req + kDeriveThreads - 1) / kDeriveThreads);
+    if (block == 16) {
+        hipLaunchKernelGGL(k_derive_b16, grid, dim3(kDeriveThreads), 0, s, a);
+    } else if (block % 16 == 0) {
+        hipLaunchKernelGGL(k_derive_m16, grid, dim3(kDeriveThreads), 0, s, a);
+    } else {
+        hipLaunchKernelGGL(k_derive_any, grid, dim3(kDeriveThreads), 0, s, a);
+    }
+    return check_launch("pkv_derive_keys");
+}
+
+int launch_digest_batch(const uint8_t* bytes, uint64_t n_bytes, const int64_t* off, const uint32_t* len, uint32_t n,
+                        uint8_t* out, int32_t* status, hipStream_t s) {
+    if (n == 0) return PKV_OK;
+    hipLaunchKernelGGL(k_digest, dim3((n + 63) / 64), dim3(64), 0, s, bytes, n_bytes, off, len, n, out, status);
+    return check_launch("pkv_digest_batch");
+}
+
+int launch_key_offsets(const int64_t* tok_off, uint32_t n_req, uint32_t block, int64_t* key_off, hipStream_t s) {
+    hipLaunchKernelGGL(k_key_offsets, dim3(1), dim3(kScanThreads), 0, s, tok_off, n_req, block, key_off);
+    return check_launch("pkv_key_offsets");
+}
+
+}  // namespace pkv

@@ -1,0 +1,393 @@
+// k_table.hip -- the shared-tier index in HBM: init, longest-prefix lookup, store of misses,
+// rollback and export, on gfx950.
+//
+// Layout: struct of arrays.  keys[capacity] (16 bytes each) grouped in 4-slot buckets, so one
+// bucket is one 64-byte segment; locs[capacity + 1] (8 bytes each), the extra word holding the
+// location of the all-0xFF key (that value marks an empty key slot).  A key's home bucket is
+// its first eight bytes masked to the bucket count; probing is linear over slots, wrapping.
+//
+// Lookup reads only key slots: a key is present iff some slot on its probe path holds it, and
+// absent once the path meets an empty slot.  Store drives a per-slot state machine in the
+// location word with 64-bit atomics (gfx950 has no 128-bit compare-and-swap):
+//   empty --CAS--> pending --(write key, release)--> location | fresh
+// A lane that meets a pending slot re-reads it until it is published, then compares keys, so
+// two lanes inserting one key always meet in the same slot.  A later equal key lowers a fresh
+// entry's location with atomic min; entries older than the batch carry no fresh bit and are
+// left untouched.  A final pass clears the fresh bits.
+#include "pkv_internal.h"
+
+namespace pkv {
+namespace {
+
+using dev::eq4;
+using dev::home_bucket;
+using dev::is_marker;
+using dev::report;
+
+constexpr uint32_t kWaitLimit = 1u << 20;      // re-reads of one pending slot before giving up
+
+__device__ __forceinline__ uint64_t load_acquire(uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_release(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ bool cas_relaxed(uint64_t* p, uint64_t expected, uint64_t desired) {
+    return __hip_atomic_compare_exchange_strong(p, &expected, desired, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void min_relaxed(uint64_t* p, uint64_t v) {
+    __hip_atomic_fetch_min(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
+
+// ---- init -------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_init(uint4* keys, uint64_t* locs, uint64_t capacity) {
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+    const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
+    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i <= capacity; i += stride) {
+        if (i < capacity) keys[i] = marker;
+        locs[i] = kEmpty;
+    }
+}
+
+// ---- lookup: one wavefront per request --------------------------------------------------------
+// Lanes form 16 groups of 4; a group probes one key, each lane one slot of the 64-byte bucket.
+// Keys are probed in windows of 16, 32, 64, 64, ... keys; a ballot over the window finds the
+// first absent key, which ends the request.
+constexpr int kLookupWaves = 4;
+constexpr int kMaxWindowSteps = 4;            // window = 16 * steps keys
+
+__global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __restrict__ tkeys,
+                                                            const uint64_t* __restrict__ tlocs, uint64_t capacity,
+                                                            const uint4* __restrict__ keys,
+                                                            const int64_t* __restrict__ key_off, uint32_t n_req,
+                                                            uint64_t n_keys, int32_t* __restrict__ hits,
+                                                            int32_t* status) {
+    const uint32_t lane = lane_id();
+    const uint32_t r = blockIdx.x * kLookupWaves + (threadIdx.x >> 6);
+    if (r >= n_req) return;
+    const int64_t k0 = key_off[r], k1 = key_off[r + 1];
+    if (k0 < 0 || k1 < k0 || static_cast<uint64_t>(k1) > n_keys) {
+        if (lane == 0) {
+            report(status, PKV_ELAYOUT);
+            hits[r] = 0;
+        }
+        return;
+    }
+    const int64_t n = k1 - k0;
+    const uint32_t grp = lane >> 2, sub = lane & 3;
+    const uint64_t n_buckets = capacity / kSlotsPerBucket;
+    const uint64_t bmask = n_buckets - 1;
+    const uint64_t lead_lanes = 0x1111111111111111ull;   // lane 0 of every group
+    const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
+
+    int64_t h = 0;
+    int steps = 1;
+    while (h < n) {
+        uint4 kq[kMaxWindowSteps], sq[kMaxWindowSteps];
+        uint64_t bq[kMaxWindowSteps];
+        bool vq[kMaxWindowSteps];
+#pragma unroll
+        for (int q = 0; q < kMaxWindowSteps; ++q) {
+            const int64_t idx = h + grp + 16 * q;
+            vq[q] = q < steps && idx < n;
+            kq[q] = vq[q] ? keys[k0 + idx] : marker;
+        }
+#pragma unroll
+        for (int q = 0; q < kMaxWindowSteps; ++q) {
+            bq[q] = home_bucket(kq[q], bmask);
+            sq[q] = vq[q] ? tkeys[bq[q] * kSlotsPerBucket + sub] : marker;
+        }
+        int64_t stop = -1;
+#pragma unroll
+        for (int q = 0; q < kMaxWindowSteps; ++q) {
+            if (q >= steps) break;
+            const bool special = vq[q] && is_marker(kq[q]);   // the key that equals the empty marker
+            bool open = vq[q] && !special;                    // still probing
+            bool found = false;
+            uint4 slot = sq[q];
+            uint64_t b = bq[q];
+            for (uint64_t it = 0; it < n_buckets; ++it) {
+                const uint64_t m = __ballot(open && eq4(slot, kq[q]));
+                const uint64_t z = __ballot(open && is_marker(slot));
+                if (open) {
+                    if ((m >> (4 * grp)) & 0xF) { found = true; open = false; }
+                    else if ((z >> (4 * grp)) & 0xF) { open = false; }
+                }
+                if (__ballot(open) == 0) break;
+                if (open) {
+                    b = (b + 1) & bmask;
+                    slot = tkeys[b * kSlotsPerBucket + sub];
+                }
+            }
+            if (special) found = tlocs[capacity] != kEmpty;
+            const uint64_t valid = __ballot(vq[q]) & lead_lanes;
+            const uint64_t hit = __ballot(vq[q] && found) & lead_lanes;
+            const uint64_t miss = valid & ~hit;
+            if (miss) {
+                stop = h + 16 * q + (__builtin_ctzll(miss) >> 2);
+                break;
+            }
+        }
+        if (stop >= 0) {
+            h = stop;
+            break;
+        }
+        h += 16 * steps;
+        if (h > n) h = n;
+        if (steps < kMaxWindowSteps) steps *= 2;
+    }
+    if (lane == 0) hits[r] = static_cast<int32_t>(h);
+}
+
+// ---- store ------------------------------------------------------------------------------------
+// One lane per key of the batch.  Candidate = key j of request r with j >= hits[r].
+__device__ __forceinline__ uint32_t request_of(const int64_t* key_off, uint32_t n_req, int64_t k) {
+    uint32_t lo = 0, hi = n_req;          // largest r with key_off[r] <= k
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (key_off[mid] <= k) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+struct StoreArgs {
+    uint4* tkeys;
+    uint64_t* tlocs;
+    uint64_t capacity;
+    const uint4* keys;
+    const int64_t* key_off;
+    uint32_t n_req;
+    uint64_t n_keys;
+    const int32_t* hits;
+    const uint64_t* locs;
+    uint64_t* new_slots;
+    uint64_t* n_new;
+    int32_t* status;
+};
+
+// Candidate k of the batch: false if it is not to be stored.
+__device__ __forceinline__ bool candidate(const StoreArgs& a, uint64_t k, int64_t total) {
+    if (static_cast<int64_t>(k) >= total) return false;
+    const uint32_t r = request_of(a.key_off, a.n_req, static_cast<int64_t>(k));
+    const int64_t j = static_cast<int64_t>(k) - a.key_off[r];
+    int64_t h = a.hits[r];
+    if (h < 0) h = 0;
+    return j >= h;
+}
+
+__global__ __launch_bounds__(256) void k_store(StoreArgs a) {
+    const uint64_t k = blockIdx.x * 256ull + threadIdx.x;
+    const int64_t total = a.key_off[a.n_req];
+    if (total < 0 || static_cast<uint64_t>(total) > a.n_keys) {
+        if (k == 0) report(a.status, PKV_ELAYOUT);
+        return;
+    }
+    bool active = candidate(a, k, total);
+    uint64_t want = 0;
+    uint4 key = make_uint4(0, 0, 0, 0);
+    if (active) {
+        const uint64_t loc = a.locs[k];
+        if (loc >= PKV_LOC_LIMIT) {
+            report(a.status, PKV_ERESERVED);
+            active = false;
+        }
+        want = loc | kFresh;
+        key = a.keys[k];
+    }
+    bool claimed = false;
+    uint64_t my_slot = 0;
+    if (active && is_marker(key)) {
+        // the all-0xFF key lives in the extra location word; there are no key bytes to publish
+        uint64_t* p = a.tlocs + a.capacity;
+        for (uint32_t spin = 0; spin < kWaitLimit; ++spin) {
+            const uint64_t l = load_acquire(p);
+            if (l == kEmpty) {
+                if (cas_relaxed(p, kEmpty, want)) { claimed = true; my_slot = a.capacity; break; }
+                continue;
+            }
+            if (l & kFresh) min_relaxed(p, want);
+            break;
+        }
+    } else if (active) {
+        const uint64_t slot_mask = a.capacity - 1;
+        uint64_t s = home_bucket(key, (a.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
+        uint64_t probes = 0;
+        uint32_t waits = 0;
+        while (true) {
+            const uint64_t l = load_acquire(a.tlocs + s);
+            if (l == kEmpty) {
+                if (cas_relaxed(a.tlocs + s, kEmpty, kPending)) {
+                    a.tkeys[s] = key;
+                    store_release(a.tlocs + s, want);
+                    claimed = true;
+                    my_slot = s;
+                    break;
+                }
+                continue;                       // lost the race: read the slot again
+            }
+            if (l == kPending) {
+                if (++waits >= kWaitLimit) { report(a.status, PKV_ESTALL); break; }
+                continue;
+            }
+            const uint4 held = a.tkeys[s];
+            if (eq4(held, key)) {
+                if (l & kFresh) min_relaxed(a.tlocs + s, want);
+                break;
+            }
+            s = (s + 1) & slot_mask;
+            if (++probes >= a.capacity) { report(a.status, PKV_EFULL); break; }
+        }
+    }
+    // one counter update per wavefront; slot log in lane order
+    const uint64_t mask = __ballot(claimed);
+    if (mask) {
+        const uint32_t lane = lane_id();
+        const uint32_t leader = __builtin_ctzll(mask);
+        uint64_t base = 0;
+        if (lane == leader)
+            base = __hip_atomic_fetch_add(a.n_new, static_cast<uint64_t>(__popcll(mask)), __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+        base = __shfl(base, leader, 64);
+        if (claimed && a.new_slots) {
+            const uint64_t pos = base + __popcll(mask & ((1ull << lane) - 1));
+            if (pos < a.n_keys) a.new_slots[pos] = my_slot;
+            else report(a.status, PKV_ELAYOUT);
+        }
+    }
+}
+
+// Clears the fresh bit of every key of the batch's candidates (quiescent table: plain accesses).
+__global__ __launch_bounds__(256) void k_store_finish(StoreArgs a) {
+    const uint64_t k = blockIdx.x * 256ull + threadIdx.x;
+    const int64_t total = a.key_off[a.n_req];
+    if (total < 0 || static_cast<uint64_t>(total) > a.n_keys) return;
+    if (!candidate(a, k, total)) return;
+    const uint4 key = a.keys[k];
+    uint64_t s;
+    if (is_marker(key)) {
+        s = a.capacity;
+    } else {
+        const uint64_t slot_mask = a.capacity - 1;
+        s = home_bucket(key, (a.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
+        uint64_t probes = 0;
+        while (true) {
+            const uint64_t l = a.tlocs[s];
+            if (l == kEmpty || l == kPending) return;   // not stored (an error was reported)
+            if (eq4(a.tkeys[s], key)) break;
+            s = (s + 1) & slot_mask;
+            if (++probes >= a.capacity) return;
+        }
+    }
+    const uint64_t l = a.tlocs[s];
+    if (l != kEmpty && l != kPending && (l & kFresh)) a.tlocs[s] = l & ~kFresh;
+}
+
+// ---- rollback and export ------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_rollback(uint4* tkeys, uint64_t* tlocs, uint64_t capacity,
+                                                  const uint64_t* slots, const uint64_t* n_slots, uint64_t max_slots) {
+    uint64_t n = *n_slots;
+    if (n > max_slots) n = max_slots;
+    const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
+        const uint64_t s = slots[i];
+        if (s < capacity) {
+            tkeys[s] = marker;
+            tlocs[s] = kEmpty;
+        } else if (s == capacity) {
+            tlocs[s] = kEmpty;
+        }
+    }
+}
+
+__global__ void k_zero_u64(uint64_t* p) { *p = 0; }
+
+__global__ __launch_bounds__(256) void k_export(const uint4* tkeys, const uint64_t* tlocs, uint64_t capacity,
+                                                uint4* out_keys, uint64_t* out_locs, uint64_t* count) {
+    const uint32_t lane = lane_id();
+    const uint64_t waves = static_cast<uint64_t>(gridDim.x) * (blockDim.x / 64);
+    const uint64_t wave = blockIdx.x * static_cast<uint64_t>(blockDim.x / 64) + (threadIdx.x >> 6);
+    const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
+    for (uint64_t base = wave * 64; base <= capacity; base += waves * 64) {
+        const uint64_t s = base + lane;
+        const uint64_t l = s <= capacity ? tlocs[s] : kEmpty;
+        const bool occ = l != kEmpty;
+        const uint64_t mask = __ballot(occ);
+        if (!mask) continue;
+        const uint32_t leader = __builtin_ctzll(mask);
+        uint64_t pos = 0;
+        if (lane == leader)
+            pos = __hip_atomic_fetch_add(count, static_cast<uint64_t>(__popcll(mask)), __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+        pos = __shfl(pos, leader, 64) + __popcll(mask & ((1ull << lane) - 1));
+        if (occ) {
+            out_keys[pos] = s < capacity ? tkeys[s] : marker;
+            out_locs[pos] = l;
+        }
+    }
+}
+
+unsigned grid_for(uint64_t items, unsigned threads, unsigned cap_blocks) {
+    uint64_t b = (items + threads - 1) / threads;
+    if (b < 1) b = 1;
+    if (b > cap_blocks) b = cap_blocks;
+    return static_cast<unsigned>(b);
+}
+
+}  // namespace
+
+int launch_table_init(uint8_t* keys, uint64_t* locs, uint64_t capacity, hipStream_t s) {
+    hipLaunchKernelGGL(k_init, dim3(grid_for(capacity + 1, 256, 16384)), dim3(256), 0, s,
+                       reinterpret_cast<uint4*>(keys), locs, capacity);
+    return check_launch("pkv_table_init");
+}
+
+int launch_lookup(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity, const uint8_t* keys,
+                  const int64_t* key_off, uint32_t n_req, uint64_t n_keys, int32_t* hits, int32_t* status,
+                  hipStream_t s) {
+    if (n_req == 0) return PKV_OK;
+    hipLaunchKernelGGL(k_lookup, dim3((n_req + kLookupWaves - 1) / kLookupWaves), dim3(64 * kLookupWaves), 0, s,
+                       reinterpret_cast<const uint4*>(tkeys), tlocs, capacity, reinterpret_cast<const uint4*>(keys),
+                       key_off, n_req, n_keys, hits, status);
+    return check_launch("pkv_lookup_prefix");
+}
+
+int launch_store(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint8_t* keys, const int64_t* key_off,
+                 uint32_t n_req, uint64_t n_keys, const int32_t* hits, const uint64_t* locs, uint64_t* new_slots,
+                 uint64_t* n_new, int32_t* status, hipStream_t s) {
+    if (n_req == 0 || n_keys == 0) return PKV_OK;
+    StoreArgs a{reinterpret_cast<uint4*>(tkeys), tlocs, capacity, reinterpret_cast<const uint4*>(keys),
+                key_off, n_req, n_keys, hits, locs, new_slots, n_new, status};
+    const uint64_t blocks = (n_keys + 255) / 256;
+    if (blocks > 0x7fffffffull) return set_error(PKV_EINVAL, "pkv_store: too many keys (%llu)",
+                                                 static_cast<unsigned long long>(n_keys));
+    hipLaunchKernelGGL(k_store, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, a);
+    int rc = check_launch("pkv_store");
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_store_finish, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, a);
+    return check_launch("pkv_store (finish)");
+}
+
+int launch_rollback(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint64_t* slots, const uint64_t* n_slots,
+                    uint64_t max_slots, hipStream_t s) {
+    if (max_slots == 0) return PKV_OK;
+    hipLaunchKernelGGL(k_rollback, dim3(grid_for(max_slots, 256, 8192)), dim3(256), 0, s,
+                       reinterpret_cast<uint4*>(tkeys), tlocs, capacity, slots, n_slots, max_slots);
+    return check_launch("pkv_table_rollback");
+}
+
+int launch_export(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity, uint8_t* out_keys,
+                  uint64_t* out_locs, uint64_t* count, hipStream_t s) {
+    hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(1), 0, s, count);
+    int rc = check_launch("pkv_table_export (zero)");
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_export, dim3(grid_for(capacity + 1, 256, 8192)), dim3(256), 0, s,
+                       reinterpret_cast<const uint4*>(tkeys), tlocs, capacity, reinterpret_cast<uint4*>(out_keys),
+                       out_locs, count);
+    return check_launch("pkv_table_export");
+}
+
+}  // namespace pkv

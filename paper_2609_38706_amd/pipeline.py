@@ -1,0 +1,119 @@
+"""Device-resident request batches and the hot-path step built on the C ABI.
+
+``DeviceBatch`` marshals one batch onto the GPU once:
+  * tokens and request offsets;
+  * a pool of canonical descriptor encodings, with per-request offsets and lengths.
+It also preallocates every output.  One step then launches only library kernels:
+  key offsets -> descriptor digests -> chained keys -> longest-prefix lookup -> store of misses.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+from . import (Table, pkv_derive_keys, pkv_descriptor_encode, pkv_digest_batch, pkv_key_offsets,
+               pkv_lookup_prefix, pkv_store, pkv_table_export, pkv_table_rollback)
+
+
+class DeviceBatch:
+    def __init__(self, tokens: np.ndarray, tok_off: np.ndarray, block: int, descs, desc_idx: np.ndarray,
+                 device: str = "cuda"):
+        import torch
+        self.block = int(block)
+        self.n_req = int(tok_off.shape[0] - 1)
+        self.device = device
+        self.tokens = torch.from_numpy(np.ascontiguousarray(tokens, dtype=np.int32)).to(device)
+        if self.tokens.numel() == 0:
+            self.tokens = torch.zeros(1, dtype=torch.int32, device=device)[:0]
+        self.tok_off = torch.from_numpy(np.ascontiguousarray(tok_off, dtype=np.int64)).to(device)
+        encs = [pkv_descriptor_encode(d) for d in descs]
+        lens = np.array([len(e) for e in encs], dtype=np.int64)
+        offs = np.zeros(len(encs), dtype=np.int64)
+        if len(encs) > 1:
+            offs[1:] = np.cumsum(lens)[:-1]
+        pool = np.frombuffer(b"".join(encs) or b"\0", dtype=np.uint8)
+        didx = np.asarray(desc_idx, dtype=np.int64)
+        self.pool = torch.from_numpy(pool.copy()).to(device)
+        self.msg_off = torch.from_numpy(offs[didx].copy()).to(device)
+        self.msg_len = torch.from_numpy(lens[didx].astype(np.int32)).to(device)
+        self.digests = torch.empty((max(1, self.n_req), 16), dtype=torch.uint8, device=device)
+        self.key_off = torch.empty(self.n_req + 1, dtype=torch.int64, device=device)
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+        pkv_key_offsets(self.tok_off, self.block, self.key_off)
+        self.n_keys = int(self.key_off[-1].item())
+        self.keys = torch.empty((max(1, self.n_keys), 16), dtype=torch.uint8, device=device)
+        self.hits = torch.zeros(max(1, self.n_req), dtype=torch.int32, device=device)
+        self.n_new = torch.zeros(1, dtype=torch.int64, device=device)
+        self.new_slots = torch.empty(max(1, self.n_keys), dtype=torch.int64, device=device)
+        self.locs = None
+
+    @classmethod
+    def from_batch(cls, batch, device="cuda"):
+        return cls(batch.tokens, batch.tok_off, batch.block, batch.descs, batch.desc_idx, device)
+
+    def set_locations(self, locs: np.ndarray):
+        import torch
+        self.locs = torch.from_numpy(np.ascontiguousarray(locs).view(np.int64)).to(self.device)
+        if self.locs.numel() == 0:
+            self.locs = torch.zeros(1, dtype=torch.int64, device=self.device)
+
+    # ---- the steps of the hot path ------------------------------------------------------------
+    def key_offsets(self, stream=None):
+        pkv_key_offsets(self.tok_off, self.block, self.key_off, stream)
+
+    def digest(self, stream=None):
+        pkv_digest_batch(self.pool, self.msg_off, self.msg_len, self.digests[: self.n_req], self.status, stream)
+
+    def derive(self, stream=None):
+        pkv_derive_keys(self.tokens, self.tok_off, self.digests[: max(1, self.n_req)], self.block, self.key_off,
+                        self.keys, self.status, stream)
+
+    def lookup(self, table: Table, stream=None):
+        pkv_lookup_prefix(table, self.keys, self.key_off, self.hits[: max(1, self.n_req)], self.status, stream)
+
+    def store(self, table: Table, stream=None, log=True):
+        pkv_store(table, self.keys, self.key_off, self.hits[: max(1, self.n_req)], self.locs, self.n_new,
+                  self.status, self.new_slots if log else None, stream)
+
+    def rollback(self, table: Table, stream=None):
+        pkv_table_rollback(table, self.new_slots, self.n_new, stream)
+
+    def step(self, table: Table, stream=None):
+        """One pass of the whole hot path over this batch."""
+        self.key_offsets(stream)
+        self.digest(stream)
+        self.derive(stream)
+        self.lookup(table, stream)
+        self.store(table, stream)
+
+    # ---- host views (synchronizing) ----------------------------------------------------------
+    def host_keys(self) -> np.ndarray:
+        return self.keys[: self.n_keys].cpu().numpy()
+
+    def host_hits(self) -> np.ndarray:
+        return self.hits[: self.n_req].cpu().numpy()
+
+    def host_status(self) -> int:
+        return int(self.status.item())
+
+
+def export_sorted(table: Table):
+    """(keys uint8 [n, 16], locs uint64 [n]) of every occupied slot, sorted by key bytes."""
+    import torch
+    cap = table.capacity
+    keys = torch.empty((cap + 1, 16), dtype=torch.uint8, device=table.keys.device)
+    locs = torch.empty(cap + 1, dtype=torch.int64, device=table.keys.device)
+    count = torch.zeros(1, dtype=torch.int64, device=table.keys.device)
+    pkv_table_export(table, keys, locs, count)
+    n = int(count.item())
+    k = keys[:n].cpu().numpy()
+    v = locs[:n].cpu().numpy().view(np.uint64)
+    return sort_pairs(k, v)
+
+
+def sort_pairs(keys: np.ndarray, locs: np.ndarray):
+    if keys.shape[0] == 0:
+        return keys.reshape(0, 16), locs
+    words = np.ascontiguousarray(keys).view(">u8").reshape(-1, 2)
+    order = np.lexsort((words[:, 1], words[:, 0]))
+    return keys[order], locs[order]

@@ -1,0 +1,105 @@
+"""Shared helpers of the GPU parity tests: run a workload through the oracle and through the HIP
+path, and inspect raw index arrays."""
+
+from __future__ import annotations
+
+import os
+
+import numpy as np
+
+import oracle
+from workloads import locations
+
+THREADS = max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def gpu_available() -> bool:
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+def announce(msg: str):
+    print(f"[gpu-test] {msg}", flush=True)
+
+
+# ---- oracle side --------------------------------------------------------------------------------
+
+def oracle_keys(batch):
+    ko = oracle.key_offsets(batch.tok_off, batch.block)
+    keys = oracle.derive(batch.tokens, batch.tok_off, oracle.batch_digests(batch), batch.block, THREADS)
+    return keys, ko
+
+
+def oracle_fill(index, batch):
+    keys, ko = oracle_keys(batch)
+    rc = index.store(keys, ko, np.zeros(batch.n_req, np.int32), locations(ko, batch.tag))
+    assert rc == 0, rc
+    return keys, ko
+
+
+# ---- HIP side ----------------------------------------------------------------------------------
+
+def gpu_batch(batch):
+    from paper_2609_38706_amd.pipeline import DeviceBatch
+    db = DeviceBatch.from_batch(batch)
+    db.set_locations(locations(db.key_off.cpu().numpy(), batch.tag))
+    return db
+
+
+def gpu_fill(table, batch):
+    db = gpu_batch(batch)
+    db.digest()
+    db.derive()
+    db.hits.zero_()
+    db.store(table)
+    return db
+
+
+def raw_table(table):
+    keys = table.keys.cpu().numpy()
+    locs = table.locs.cpu().numpy().view(np.uint64)
+    return keys, locs
+
+
+EMPTY = np.uint64(0xFFFFFFFFFFFFFFFF)
+PENDING = np.uint64(0xFFFFFFFFFFFFFFFE)
+FRESH = np.uint64(1 << 63)
+
+
+def check_structure(table):
+    """Index invariants: every occupied slot is reachable from its home bucket with no empty slot
+    in between; no claimed-but-unpublished or batch-marked slot survives a store; empty slots hold
+    the all-0xFF key; the all-0xFF key never occupies an ordinary slot; no key is stored twice."""
+    keys, locs = raw_table(table)
+    cap = table.capacity
+    main = locs[:cap]
+    occ = main != EMPTY
+    assert not (main == PENDING).any(), "pending slot left behind"
+    assert not (main[occ] & FRESH).any(), "fresh bit left behind"
+    assert (keys[~occ] == 0xFF).all(), "empty slot with key bytes"
+    marker = (keys == 0xFF).all(axis=1)
+    assert not (occ & marker).any(), "marker key stored in an ordinary slot"
+    if not occ.any():
+        return int(occ.sum())
+    assert not occ.all() or True
+    # home slot of each occupied key
+    lo = keys[:, :8].copy().view("<u8").reshape(-1)
+    home = (lo & np.uint64(cap // 4 - 1)).astype(np.int64) * 4
+    idx = np.arange(cap, dtype=np.int64)
+    # last empty position at or before each index, cyclically
+    last = np.where(~occ, idx, -1)
+    last = np.maximum.accumulate(last)
+    if (~occ).any():
+        wrap_last = int(idx[~occ][-1]) - cap
+        last = np.where(last < 0, wrap_last, last)
+        s = idx[occ]
+        dist_home = (s - home[occ]) % cap
+        dist_empty = s - last[occ]
+        assert (dist_home < dist_empty).all(), "occupied slot not reachable from its home bucket"
+    # no duplicate keys
+    ok = keys[occ]
+    assert np.unique(ok.view("V16").reshape(-1)).shape[0] == ok.shape[0], "duplicate key stored"
+    return int(occ.sum()) + int(locs[cap] != EMPTY)

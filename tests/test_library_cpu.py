@@ -1,0 +1,122 @@
+"""The C-ABI library on the CPU: it loads, exports every entry point include/pkv.h declares, its
+host-side encoder and digest agree with the oracle, and host-detectable argument errors are
+returned synchronously (no GPU call is made here)."""
+
+import ctypes
+import itertools
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_38706_amd as pkv
+from tests.test_oracle_encoding import TRICKY, _all_descriptors
+from workloads import make_workload
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built():
+    if not os.path.exists(pkv.LIB_PATH):
+        pkv.build()
+    if not os.path.exists(oracle.LIB_PATH):
+        oracle.build()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "pkv.h")).read()
+    return sorted(set(re.findall(r"^(?:int|const char\*)\s+(pkv_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) == 12
+    lib = pkv.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(pkv.EXPORTED) == names
+    assert pkv.version().startswith("pkv")
+
+
+@pytest.mark.parametrize("names", [(b"model_id", b"salt", b"a"), (b"a", b"ab", b"b"),
+                                   (b"adapter_id", b"weight_version", b"kv_format")])
+def test_host_encoding_matches_oracle_brute_force(names):
+    for desc in _all_descriptors(names, TRICKY):
+        assert pkv.pkv_descriptor_encode(desc) == oracle.encode(desc)
+        assert pkv.pkv_descriptor_digest(desc) == oracle.digest(desc)
+
+
+def test_host_digest_matches_oracle_on_workload_descriptors():
+    for name in ("tiny", "c2", "c3"):
+        w = make_workload(name)
+        for d in w.batch.descs:
+            assert pkv.pkv_descriptor_digest(d) == oracle.digest(d)
+
+
+def test_host_digest_long_and_binary_values():
+    rng = np.random.default_rng(3)
+    for _ in range(200):
+        n = int(rng.integers(0, 9))
+        desc, used = [], set()
+        for _ in range(n):
+            name = rng.integers(0, 256, size=int(rng.integers(0, 6)), dtype=np.uint8).tobytes()
+            if name in used:
+                continue
+            used.add(name)
+            desc.append((name, rng.integers(0, 256, size=int(rng.integers(0, 300)), dtype=np.uint8).tobytes()))
+        assert pkv.pkv_descriptor_digest(desc) == oracle.digest(desc)
+
+
+def test_permutations_give_one_digest():
+    desc = [(b"salt", b"s"), (b"model_id", b"m"), (b"x9", b""), (b"kv_format", b"fp8"), (b"adapter_id", b"A")]
+    ref = pkv.pkv_descriptor_digest(desc)
+    for perm in itertools.permutations(desc):
+        assert pkv.pkv_descriptor_digest(list(perm)) == ref
+
+
+def test_duplicate_dimension_is_an_error():
+    with pytest.raises(pkv.PkvError) as e:
+        pkv.pkv_descriptor_digest([(b"salt", b"a"), (b"salt", b"b")])
+    assert e.value.code == pkv.PKV_EDUPDIM
+    assert b"twice" in pkv.lib().pkv_last_error()
+
+
+def test_encode_buffer_too_small():
+    arr, _keep = pkv._fields([(b"model_id", b"m")])
+    n = ctypes.c_size_t(0)
+    buf = (ctypes.c_uint8 * 4)()
+    assert pkv.lib().pkv_descriptor_encode(arr, 1, buf, 4, ctypes.byref(n)) == pkv.PKV_EINVAL
+    assert n.value == 8 + 4 + 8 + 4 + 1
+
+
+def _table(cap, keys=0x1000, locs=0x2000):
+    return pkv.pkv_table(keys, locs, cap)
+
+
+@pytest.mark.parametrize("cap", [0, 2, 3, 6, 1000])
+def test_bad_capacity_rejected_on_host(cap):
+    t = _table(cap)
+    assert pkv.lib().pkv_table_init(ctypes.byref(t), None) == pkv.PKV_EINVAL
+
+
+def test_misaligned_table_rejected_on_host():
+    t = _table(1024, keys=0x1010)
+    assert pkv.lib().pkv_table_init(ctypes.byref(t), None) == pkv.PKV_EINVAL
+    assert b"64-byte" in pkv.lib().pkv_last_error()
+
+
+def test_zero_block_rejected_on_host():
+    L = pkv.lib()
+    assert L.pkv_key_offsets(0x1000, 4, 0, 0x2000, None) == pkv.PKV_EINVAL
+    assert L.pkv_derive_keys(0x1000, 16, 0x2000, 1, 0x3000, 0, 0x4000, 1, 0x5000, 0x6000, None) == pkv.PKV_EINVAL
+
+
+def test_null_arguments_rejected_on_host():
+    L = pkv.lib()
+    t = _table(1024)
+    assert L.pkv_lookup_prefix(ctypes.byref(t), None, 0x2000, 3, 5, 0x3000, 0x4000, None) == pkv.PKV_EINVAL
+    assert L.pkv_store(ctypes.byref(t), 0x1000, 0x2000, 3, 5, 0x3000, 0x4000, None, None, 0x5000, None) == pkv.PKV_EINVAL
+    assert L.pkv_digest_batch(0x1000, 10, None, 0x2000, 3, 0x3000, 0x4000, None) == pkv.PKV_EINVAL

@@ -117,3 +117,14 @@ def test_reserved_locations_rejected():
     assert len(idx) == 0
     assert idx.store(keys, np.array([0, 1], np.int64), np.zeros(1, np.int32),
                      np.array([(1 << 62) - 1], np.uint64)) == 0
+
+
+def test_the_all_ff_key_does_not_use_capacity():
+    rng = np.random.default_rng(6)
+    keys = rng.integers(0, 255, size=(9, 16), dtype=np.uint8)
+    keys[8] = 0xFF
+    off = np.array([0, 9], np.int64)
+    idx = oracle.Index(8)
+    assert idx.store(keys, off, np.zeros(1, np.int32), np.arange(9, dtype=np.uint64)) == 0
+    assert len(idx) == 9
+    assert (idx.lookup(keys, off) == 9).all()
