@@ -51,6 +51,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_TEXT))
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-saturation", action="store_true", help="skip the derive-at-full-occupancy diagnostic")
     p.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (0 = host cores, at most 16)")
     p.add_argument("--calib-copy", action="store_true", help="run only a plain 1 GiB device copy (counter calibration)")
     p.add_argument("--quiet", action="store_true")
@@ -145,6 +146,34 @@ def gpu_leg(args, w):
             "n_req": run.n_req, "hit_blocks": int(hits.sum()), "new_entries": int(run.n_new.item())}
 
 
+def saturation_leg(args, n_chains=131072, blocks=16, reps=5):
+    """Derive alone on a batch with enough chains to fill every SIMD (131072 chains x 16 keys, B=16,
+    random tokens): the one shape where the int32 VALU peak is reachable.  A diagnostic, not the
+    headline value."""
+    import torch
+    from paper_2609_38706_amd.pipeline import DeviceBatch
+    rng = np.random.default_rng(0x5EED0006)
+    tokens = rng.integers(0, 128256, size=n_chains * blocks * 16, dtype=np.int32)
+    off = np.arange(n_chains + 1, dtype=np.int64) * (blocks * 16)
+    descs = [[(b"model_id", b"saturation"), (b"salt", bytes([i]) * 8)] for i in range(16)]
+    db = DeviceBatch(tokens, off, 16, descs, (np.arange(n_chains) % 16).astype(np.int32))
+    db.digest()
+    db.derive()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        db.derive()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    ops = db.n_keys * compressions_per_key(16) * OPS_PER_COMPRESSION
+    return {"chains": n_chains, "keys": db.n_keys, "derive_ms": round(ms, 4),
+            "gkeys_per_s": round(db.n_keys / (ms * 1e-3) / 1e9, 4),
+            "achieved": round(ops / (ms * 1e-3) / 1e12, 4), "peak": round(INT_PEAK / 1e12, 4), "unit": "Tops/s",
+            "frac": round(ops / (ms * 1e-3) / INT_PEAK, 4)}
+
+
 def cpu_leg(args, w):
     """The oracle as it stands, on the host cores: one full step of the same workload."""
     import oracle
@@ -203,6 +232,10 @@ def main():
                 "unit": "Tops/s", "frac": round(achieved / INT_PEAK, 5), "traffic": None,
                 "kernel": "derive", "ops_per_key": compressions_per_key(block) * OPS_PER_COMPRESSION,
                 "chain_ceiling_frac": round(min(1.0, n_chains / (CUS * 4 * 64)), 5)}
+    sat = None
+    if not args.no_saturation:
+        log(args, "saturation leg")
+        sat = saturation_leg(args)
     cpu = None
     if not args.no_cpu_baseline:
         log(args, "cpu leg")
@@ -219,6 +252,7 @@ def main():
                        "store": round(g["store_ms"], 4)},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "derive_saturated": sat,
     }
     print(json.dumps(out), flush=True)
 

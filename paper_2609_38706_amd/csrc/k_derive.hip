@@ -103,6 +103,203 @@ __global__ __launch_bounds__(kDeriveThreads) void k_derive_b16(ChainArgs a) {
     }
 }
 
+// ---- B = 16, two wavefronts per 64 chains (used while chains are scarce) ----------------------
+// A chain's rounds are strictly serial, but much of each key's instruction stream is not on that
+// serial path.  Two wavefronts share the same 64 chains (lane = chain):
+//   consumer (wave 0): only the 2 x 64 SHA-256 rounds of every key, reading K_t + W_t from LDS;
+//   helper   (wave 1): during the first three phases of key i, compression 1's schedule
+//                      W16..W63 (it depends on key i-1), one phase ahead of the consumer; during
+//                      the long last phase, every token-only part of key i+1 (token loads two keys
+//                      ahead, byte swaps, the whole schedule of compression 2) into a double buffer.
+// Per key there are four phases separated by workgroup barriers: phases 0-2 each hold 16 rounds
+// of compression 1, phase 3 holds its last 16 rounds and all of compression 2, whose 64 K + W
+// words the consumer already holds in registers.  The consumer issues about 1850 instructions per
+// key instead of about 2900.
+constexpr int kPcThreads = 128;
+
+struct PcShared {
+    uint4 kw2[2][16][64];      // K_t + W_t of compression 2, 64 words per lane, two keys
+    uint4 w1tok[2][2][64];     // W8..W15 of compression 1 (byte-swapped tokens 0..7), two keys
+    uint4 kw1tok[2][2][64];    // K_t + W_t for t = 8..15 of compression 1, two keys
+    uint4 kw1hi[12][64];       // K_t + W_t for t = 16..63 of compression 1 (current key)
+    uint4 prev[64];            // previous key words (consumer -> helper)
+};
+
+__device__ __forceinline__ void put4(uint4* p, const uint32_t* v) { *p = make_uint4(v[0], v[1], v[2], v[3]); }
+__device__ __forceinline__ void get4(const uint4* p, uint32_t* v) {
+    const uint4 x = *p;
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+}
+
+// 16 consecutive rounds; kw[j] = K_{t0+j} + W_{t0+j}.  16 is a multiple of 8, so the state array
+// keeps its naming across calls.
+__device__ __forceinline__ void rounds16(uint32_t s[8], const uint32_t* kw) {
+    uint32_t a = s[0], b = s[1], c = s[2], d = s[3], e = s[4], f = s[5], g = s[6], h = s[7];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const uint32_t t1 = h + dev::bsig1(e) + dev::choose(e, f, g) + kw[j];
+        const uint32_t t2 = dev::bsig0(a) + dev::majority(a, b, c);
+        h = g; g = f; f = e; e = d + t1;
+        d = c; c = b; b = a; a = t1 + t2;
+    }
+    s[0] = a; s[1] = b; s[2] = c; s[3] = d; s[4] = e; s[5] = f; s[6] = g; s[7] = h;
+}
+
+// 16 schedule steps t = T0 .. T0+15 (T0 >= 16) on the rolling window w; kw receives K_t + W_t.
+template <int T0>
+__device__ __forceinline__ void schedule16(uint32_t w[16], uint32_t kw[16]) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const int t = T0 + j;
+        const uint32_t x = dev::ssig1(w[(t - 2) & 15]) + w[(t - 7) & 15] + dev::ssig0(w[(t - 15) & 15]) + w[t & 15];
+        w[t & 15] = x;
+        kw[j] = x + kRoundK[t];
+    }
+}
+
+__device__ __forceinline__ void lds_put16(uint4 (*dst)[64], uint32_t lane, const uint32_t kw[16]) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) put4(&dst[q][lane], kw + 4 * q);
+}
+__device__ __forceinline__ void lds_get16(const uint4 (*src)[64], uint32_t lane, uint32_t* kw) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) get4(&src[q][lane], kw + 4 * q);
+}
+
+__device__ __forceinline__ int64_t wave_max(int64_t v) {
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int64_t o = __shfl_xor(v, d, 64);
+        v = v > o ? v : o;
+    }
+    return v;
+}
+
+__device__ __forceinline__ void load_tokens16(const int32_t* tp, int64_t key, int64_t n, uint32_t out[16]) {
+    if (key < n) {
+        const int32_t* p = tp + key * 16;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) out[q] = static_cast<uint32_t>(p[q]);
+    } else {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) out[q] = 0u;
+    }
+}
+
+// Token-only data of one key (16 tokens tk) into buffer `buf`.
+__device__ __forceinline__ void produce_key(PcShared& sh, uint32_t lane, int buf, const uint32_t tk[16]) {
+    uint32_t v[8], kv[8], w[16], kw[16];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) { v[q] = bswap(tk[q]); kv[q] = v[q] + kRoundK[8 + q]; }
+    put4(&sh.w1tok[buf][0][lane], v);
+    put4(&sh.w1tok[buf][1][lane], v + 4);
+    put4(&sh.kw1tok[buf][0][lane], kv);
+    put4(&sh.kw1tok[buf][1][lane], kv + 4);
+    // compression 2: tokens 8..15, then the padding of a 96-byte message
+#pragma unroll
+    for (int q = 0; q < 8; ++q) w[q] = bswap(tk[8 + q]);
+    w[8] = 0x80000000u;
+#pragma unroll
+    for (int q = 9; q < 15; ++q) w[q] = 0u;
+    w[15] = (32u + 4u * 16u) * 8u;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) kw[q] = w[q] + kRoundK[q];
+    lds_put16(&sh.kw2[buf][0], lane, kw);
+    schedule16<16>(w, kw);
+    lds_put16(&sh.kw2[buf][4], lane, kw);
+    schedule16<32>(w, kw);
+    lds_put16(&sh.kw2[buf][8], lane, kw);
+    schedule16<48>(w, kw);
+    lds_put16(&sh.kw2[buf][12], lane, kw);
+}
+
+__global__ __launch_bounds__(kPcThreads) void k_derive_b16_pc(ChainArgs a) {
+    __shared__ PcShared sh;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t r = blockIdx.x * 64 + lane;
+    int64_t t0 = 0, k0 = 0, n = 0;
+    bool valid = r < a.n_req;
+    if (valid && !chain_bounds(a, r, t0, k0, n)) valid = false;
+    if (!valid) n = 0;
+    const int64_t nmax = wave_max(n);           // identical in both wavefronts
+    uint32_t dg[4] = {0u, 0u, 0u, 0u};
+    if (valid) load_digest(a, r, dg);
+    const int32_t* tp = a.tokens + t0;
+
+    if (wave == 0) {
+        // ---------------- consumer ----------------
+        uint32_t prev[4] = {0u, 0u, 0u, 0u};
+        uint32_t dgk[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) dgk[q] = dg[q] + kRoundK[4 + q];
+        put4(&sh.prev[lane], prev);
+        __syncthreads();                                       // prologue
+        for (int64_t i = 0; i < nmax; ++i) {
+            const int buf = static_cast<int>(i & 1);
+            uint32_t s[8], kw[16], kw2[64];
+            init_state(s);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) { kw[q] = prev[q] + kRoundK[q]; kw[4 + q] = dgk[q]; }
+            get4(&sh.kw1tok[buf][0][lane], kw + 8);
+            get4(&sh.kw1tok[buf][1][lane], kw + 12);
+#pragma unroll
+            for (int ph = 0; ph < 4; ++ph) lds_get16(&sh.kw2[buf][4 * ph], lane, kw2 + 16 * ph);
+            rounds16(s, kw);                                   // rounds 0..15
+            __syncthreads();
+            lds_get16(&sh.kw1hi[0], lane, kw);
+            rounds16(s, kw);                                   // rounds 16..31
+            __syncthreads();
+            lds_get16(&sh.kw1hi[4], lane, kw);
+            rounds16(s, kw);                                   // rounds 32..47
+            __syncthreads();
+            lds_get16(&sh.kw1hi[8], lane, kw);
+            rounds16(s, kw);                                   // rounds 48..63
+            uint32_t hmid[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) { hmid[q] = s[q] + kInitH[q]; s[q] = hmid[q]; }
+#pragma unroll
+            for (int ph = 0; ph < 4; ++ph) rounds16(s, kw2 + 16 * ph);   // compression 2
+#pragma unroll
+            for (int q = 0; q < 4; ++q) prev[q] = s[q] + hmid[q];
+            if (i < n) store_key(a.keys, k0 + i, prev);
+            put4(&sh.prev[lane], prev);
+            __syncthreads();                                   // end of key
+        }
+    } else {
+        // ---------------- helper ----------------
+        uint32_t tk[16], pre[16];
+        load_tokens16(tp, 0, n, tk);
+        load_tokens16(tp, 1, n, pre);
+        produce_key(sh, lane, 0, tk);
+        __syncthreads();                                       // prologue
+        for (int64_t i = 0; i < nmax; ++i) {
+            const int buf = static_cast<int>(i & 1);
+            uint32_t w[16], kw[16];
+            get4(&sh.prev[lane], w);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) w[4 + q] = dg[q];
+            get4(&sh.w1tok[buf][0][lane], w + 8);
+            get4(&sh.w1tok[buf][1][lane], w + 12);
+            schedule16<16>(w, kw);
+            lds_put16(&sh.kw1hi[0], lane, kw);
+            __syncthreads();
+            schedule16<32>(w, kw);
+            lds_put16(&sh.kw1hi[4], lane, kw);
+            __syncthreads();
+            schedule16<48>(w, kw);
+            lds_put16(&sh.kw1hi[8], lane, kw);
+            __syncthreads();
+            // long phase: the next key's token-only data, and the tokens two keys ahead
+#pragma unroll
+            for (int q = 0; q < 16; ++q) tk[q] = pre[q];
+            load_tokens16(tp, i + 2, n, pre);
+            produce_key(sh, lane, buf ^ 1, tk);
+            __syncthreads();                                   // end of key
+        }
+    }
+}
+
 // ---- B = 16m, m >= 2: m + 1 compressions per key -------------------------------------------
 // Message blocks of one key: block 0 = prev | digest | tokens 0..7; block c (1..m-1) = tokens
 // 16c-8 .. 16c+7; block m = tokens 16m-8 .. 16m-1 | padding.  The token words of the next block
@@ -297,13 +494,28 @@ __global__ __launch_bounds__(kScanThreads) void k_key_offsets(const int64_t* tok
 
 }  // namespace
 
+// Compute units of the current device (cached per device).
+int compute_units() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (!cached[dev]) {
+        int cu = 0;
+        if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
+        cached[dev] = cu;
+    }
+    return cached[dev];
+}
+
 int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_off, uint32_t n_req,
                   const uint8_t* digests, uint32_t block, const int64_t* key_off, uint64_t n_keys, uint8_t* keys,
                   int32_t* status, hipStream_t s) {
     if (n_req == 0) return PKV_OK;
     ChainArgs a{tokens, n_tokens, tok_off, n_req, digests, block, key_off, n_keys, keys, status};
     const dim3 grid((n_req + kDeriveThreads - 1) / kDeriveThreads);
-    if (block == 16) {
+    if (block == 16 && grid.x <= static_cast<unsigned>(compute_units())) {
+        hipLaunchKernelGGL(k_derive_b16_pc, grid, dim3(kPcThreads), 0, s, a);
+    } else if (block == 16) {
         hipLaunchKernelGGL(k_derive_b16, grid, dim3(kDeriveThreads), 0, s, a);
     } else if (block % 16 == 0) {
         hipLaunchKernelGGL(k_derive_m16, grid, dim3(kDeriveThreads), 0, s, a);

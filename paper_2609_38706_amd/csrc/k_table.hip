@@ -9,7 +9,7 @@
 // Lookup reads only key slots: a key is present iff some slot on its probe path holds it, and
 // absent once the path meets an empty slot.  Store drives a per-slot state machine in the
 // location word with 64-bit atomics (gfx950 has no 128-bit compare-and-swap):
-//   empty --CAS--> pending --(write key, release)--> location | fresh
+//   empty --CAS--> pending --(write key, wait, publish)--> location | fresh
 // A lane that meets a pending slot re-reads it until it is published, then compares keys, so
 // two lanes inserting one key always meet in the same slot.  A later equal key lowers a fresh
 // entry's location with atomic min; entries older than the batch carry no fresh bit and are
@@ -26,12 +26,6 @@ using dev::report;
 
 constexpr uint32_t kWaitLimit = 1u << 20;      // re-reads of one pending slot before giving up
 
-__device__ __forceinline__ uint64_t load_acquire(uint64_t* p) {
-    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void store_release(uint64_t* p, uint64_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
 __device__ __forceinline__ bool cas_relaxed(uint64_t* p, uint64_t expected, uint64_t desired) {
     return __hip_atomic_compare_exchange_strong(p, &expected, desired, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
                                                 __HIP_MEMORY_SCOPE_AGENT);
@@ -143,16 +137,9 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
 }
 
 // ---- store ------------------------------------------------------------------------------------
-// One lane per key of the batch.  Candidate = key j of request r with j >= hits[r].
-__device__ __forceinline__ uint32_t request_of(const int64_t* key_off, uint32_t n_req, int64_t k) {
-    uint32_t lo = 0, hi = n_req;          // largest r with key_off[r] <= k
-    while (hi - lo > 1) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (key_off[mid] <= k) lo = mid; else hi = mid;
-    }
-    return lo;
-}
-
+// One lane per key of the batch; candidate = key j of request r with j >= hits[r].  A wavefront
+// covers 64 consecutive keys: one (wave-uniform) binary search finds the request of its first
+// key, and each lane walks forward over the few request boundaries inside the wavefront.
 struct StoreArgs {
     uint4* tkeys;
     uint64_t* tlocs;
@@ -168,24 +155,73 @@ struct StoreArgs {
     int32_t* status;
 };
 
-// Candidate k of the batch: false if it is not to be stored.
-__device__ __forceinline__ bool candidate(const StoreArgs& a, uint64_t k, int64_t total) {
+__device__ __forceinline__ bool candidate(const StoreArgs& a, uint64_t wave_base, uint64_t k, int64_t total) {
+    uint32_t lo = 0, hi = a.n_req;            // largest r with key_off[r] <= wave_base
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (a.key_off[mid] <= static_cast<int64_t>(wave_base)) lo = mid; else hi = mid;
+    }
     if (static_cast<int64_t>(k) >= total) return false;
-    const uint32_t r = request_of(a.key_off, a.n_req, static_cast<int64_t>(k));
+    uint32_t r = lo;
+    while (r + 1 < a.n_req && a.key_off[r + 1] <= static_cast<int64_t>(k)) ++r;
     const int64_t j = static_cast<int64_t>(k) - a.key_off[r];
     int64_t h = a.hits[r];
     if (h < 0) h = 0;
     return j >= h;
 }
 
-__global__ __launch_bounds__(256) void k_store(StoreArgs a) {
-    const uint64_t k = blockIdx.x * 256ull + threadIdx.x;
+__device__ __forceinline__ uint64_t wave_base_of(uint32_t block_threads) {
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    return static_cast<uint64_t>(blockIdx.x) * block_threads + wave * 64ull;
+}
+
+// Key bytes of a slot whose location word was seen published, read as two relaxed 64-bit
+// atomics.  During one store launch a key slot only ever holds the empty marker or its final key,
+// so a half that is not all ones is final.  A half that reads all ones is re-read after an
+// acquire fence: either it really is all ones, or the read was stale.
+__device__ __forceinline__ uint4 read_slot_key(uint4* tkeys, uint64_t s) {
+    uint64_t* p = reinterpret_cast<uint64_t*>(tkeys + s);
+    uint64_t lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint64_t hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (lo == ~0ull || hi == ~0ull) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return make_uint4(static_cast<uint32_t>(lo), static_cast<uint32_t>(lo >> 32), static_cast<uint32_t>(hi),
+                      static_cast<uint32_t>(hi >> 32));
+}
+
+// Writes a claimed slot's key and then publishes its location word.  The two key halves are
+// agent-scope atomic stores (write-through to the device coherence point); the lane waits until
+// both are complete (vmcnt 0) before the location store is issued, so any lane that reads the
+// published location word afterwards reads the final key.  This is the gfx950 agent-scope release
+// without its L2 writeback: that writeback exists for preceding non-atomic stores, and none precede
+// the publication here.  The asm statement's memory clobber also keeps the compiler from moving
+// the stores across the wait.
+__device__ __forceinline__ void publish_slot(uint4* tkeys, uint64_t* tlocs, uint64_t s, const uint4& k, uint64_t v) {
+    uint64_t* p = reinterpret_cast<uint64_t*>(tkeys + s);
+    __hip_atomic_store(p, (static_cast<uint64_t>(k.y) << 32) | k.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p + 1, (static_cast<uint64_t>(k.w) << 32) | k.z, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __hip_atomic_store(tlocs + s, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint64_t load_relaxed(uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+constexpr uint32_t kStoreThreads = 256;
+
+__global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
+    const uint64_t wave_base = wave_base_of(kStoreThreads);
+    const uint64_t k = wave_base + lane_id();
     const int64_t total = a.key_off[a.n_req];
     if (total < 0 || static_cast<uint64_t>(total) > a.n_keys) {
         if (k == 0) report(a.status, PKV_ELAYOUT);
         return;
     }
-    bool active = candidate(a, k, total);
+    bool active = candidate(a, wave_base, k, total);
     uint64_t want = 0;
     uint4 key = make_uint4(0, 0, 0, 0);
     if (active) {
@@ -203,7 +239,7 @@ __global__ __launch_bounds__(256) void k_store(StoreArgs a) {
         // the all-0xFF key lives in the extra location word; there are no key bytes to publish
         uint64_t* p = a.tlocs + a.capacity;
         for (uint32_t spin = 0; spin < kWaitLimit; ++spin) {
-            const uint64_t l = load_acquire(p);
+            const uint64_t l = load_relaxed(p);
             if (l == kEmpty) {
                 if (cas_relaxed(p, kEmpty, want)) { claimed = true; my_slot = a.capacity; break; }
                 continue;
@@ -217,11 +253,10 @@ __global__ __launch_bounds__(256) void k_store(StoreArgs a) {
         uint64_t probes = 0;
         uint32_t waits = 0;
         while (true) {
-            const uint64_t l = load_acquire(a.tlocs + s);
+            const uint64_t l = load_relaxed(a.tlocs + s);
             if (l == kEmpty) {
                 if (cas_relaxed(a.tlocs + s, kEmpty, kPending)) {
-                    a.tkeys[s] = key;
-                    store_release(a.tlocs + s, want);
+                    publish_slot(a.tkeys, a.tlocs, s, key, want);
                     claimed = true;
                     my_slot = s;
                     break;
@@ -232,8 +267,7 @@ __global__ __launch_bounds__(256) void k_store(StoreArgs a) {
                 if (++waits >= kWaitLimit) { report(a.status, PKV_ESTALL); break; }
                 continue;
             }
-            const uint4 held = a.tkeys[s];
-            if (eq4(held, key)) {
+            if (eq4(read_slot_key(a.tkeys, s), key)) {
                 if (l & kFresh) min_relaxed(a.tlocs + s, want);
                 break;
             }
@@ -259,12 +293,27 @@ __global__ __launch_bounds__(256) void k_store(StoreArgs a) {
     }
 }
 
-// Clears the fresh bit of every key of the batch's candidates (quiescent table: plain accesses).
-__global__ __launch_bounds__(256) void k_store_finish(StoreArgs a) {
-    const uint64_t k = blockIdx.x * 256ull + threadIdx.x;
+// Clears the fresh bit of the slots the store logged (the index is quiescent: plain accesses).
+__global__ __launch_bounds__(256) void k_store_finish_log(uint64_t* tlocs, uint64_t capacity, const uint64_t* slots,
+                                                          const uint64_t* n_slots, uint64_t max_slots) {
+    uint64_t n = *n_slots;
+    if (n > max_slots) n = max_slots;
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
+        const uint64_t s = slots[i];
+        if (s > capacity) continue;
+        const uint64_t l = tlocs[s];
+        if (l != kEmpty && l != kPending && (l & kFresh)) tlocs[s] = l & ~kFresh;
+    }
+}
+
+// Without a slot log: re-finds every candidate's slot and clears its fresh bit.
+__global__ __launch_bounds__(kStoreThreads) void k_store_finish_probe(StoreArgs a) {
+    const uint64_t wave_base = wave_base_of(kStoreThreads);
+    const uint64_t k = wave_base + lane_id();
     const int64_t total = a.key_off[a.n_req];
     if (total < 0 || static_cast<uint64_t>(total) > a.n_keys) return;
-    if (!candidate(a, k, total)) return;
+    if (!candidate(a, wave_base, k, total)) return;
     const uint4 key = a.keys[k];
     uint64_t s;
     if (is_marker(key)) {
@@ -361,13 +410,18 @@ int launch_store(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint8
     if (n_req == 0 || n_keys == 0) return PKV_OK;
     StoreArgs a{reinterpret_cast<uint4*>(tkeys), tlocs, capacity, reinterpret_cast<const uint4*>(keys),
                 key_off, n_req, n_keys, hits, locs, new_slots, n_new, status};
-    const uint64_t blocks = (n_keys + 255) / 256;
+    const uint64_t blocks = (n_keys + kStoreThreads - 1) / kStoreThreads;
     if (blocks > 0x7fffffffull) return set_error(PKV_EINVAL, "pkv_store: too many keys (%llu)",
                                                  static_cast<unsigned long long>(n_keys));
-    hipLaunchKernelGGL(k_store, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_store, dim3(static_cast<unsigned>(blocks)), dim3(kStoreThreads), 0, s, a);
     int rc = check_launch("pkv_store");
     if (rc) return rc;
-    hipLaunchKernelGGL(k_store_finish, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, a);
+    if (new_slots) {
+        hipLaunchKernelGGL(k_store_finish_log, dim3(grid_for(n_keys, 256, 4096)), dim3(256), 0, s, tlocs, capacity,
+                           new_slots, n_new, n_keys);
+    } else {
+        hipLaunchKernelGGL(k_store_finish_probe, dim3(static_cast<unsigned>(blocks)), dim3(kStoreThreads), 0, s, a);
+    }
     return check_launch("pkv_store (finish)");
 }
 
