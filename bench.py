@@ -40,6 +40,25 @@ WORKLOAD_TEXT = {
 }
 
 
+DERIVE_SOURCES = ["paper_2609_38706_amd/csrc/k_derive.hip", "paper_2609_38706_amd/csrc/pkv_internal.h"]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per derive launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary, or None
+    when there is none for this workload or the derive source has changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"derive_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    h = hashlib.sha256()
+    for f in DERIVE_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if rec.get("source_sha256") != h.hexdigest():
+        return None
+    return int(round(rec["bytes_per_launch"]))
+
+
 def compressions_per_key(block: int) -> int:
     return (block + 11 + 15) // 16
 
@@ -229,7 +248,7 @@ def main():
     achieved = ops / (g["derive_ms"] * 1e-3)
     n_chains = w.batch.n_req
     roofline = {"bound": "alu", "achieved": round(achieved / 1e12, 4), "peak": round(INT_PEAK / 1e12, 4),
-                "unit": "Tops/s", "frac": round(achieved / INT_PEAK, 5), "traffic": None,
+                "unit": "Tops/s", "frac": round(achieved / INT_PEAK, 5), "traffic": measured_traffic(args.workload),
                 "kernel": "derive", "ops_per_key": compressions_per_key(block) * OPS_PER_COMPRESSION,
                 "chain_ceiling_frac": round(min(1.0, n_chains / (CUS * 4 * 64)), 5)}
     sat = None

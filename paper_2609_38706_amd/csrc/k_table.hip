@@ -47,11 +47,39 @@ __global__ __launch_bounds__(256) void k_init(uint4* keys, uint64_t* locs, uint6
 }
 
 // ---- lookup: one wavefront per request --------------------------------------------------------
-// Lanes form 16 groups of 4; a group probes one key, each lane one slot of the 64-byte bucket.
-// Keys are probed in windows of 16, 32, 64, 64, ... keys; a ballot over the window finds the
-// first absent key, which ends the request.
+// A request's keys are probed in windows of 64 x CHUNKS keys, one lane per key; a lane loads its
+// key's whole 64-byte bucket with four 16-byte loads issued together, and the next window's keys
+// are fetched while the current window's buckets are in flight.  A ballot over each 64-key chunk
+// finds the first absent key, which ends the request.  The first window is a single chunk; later
+// windows grow to LOOKUP_CHUNKS chunks.  Probes past the first miss are wasted bandwidth, traded
+// for fewer serial round trips per request.
+#ifndef PKV_LOOKUP_CHUNKS
+#define PKV_LOOKUP_CHUNKS 1
+#endif
 constexpr int kLookupWaves = 4;
-constexpr int kMaxWindowSteps = 4;            // window = 16 * steps keys
+constexpr int kChunks = PKV_LOOKUP_CHUNKS;
+
+// Probe of one key (lane-private): bucket slots already loaded in sl[0..3].  Returns 1 = present,
+// 0 = absent; continues to later buckets while a full bucket neither matches nor ends the path.
+__device__ __forceinline__ bool probe_key(const uint4* __restrict__ tkeys, const uint64_t* __restrict__ tlocs,
+                                          uint64_t capacity, uint64_t bmask, const uint4& key, uint64_t b,
+                                          uint4 sl[4]) {
+    if (is_marker(key)) return tlocs[capacity] != kEmpty;
+    const uint64_t n_buckets = bmask + 1;
+    for (uint64_t it = 0; it < n_buckets; ++it) {
+        bool empty = false;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (eq4(sl[j], key)) return true;
+            empty |= is_marker(sl[j]);
+        }
+        if (empty) return false;
+        b = (b + 1) & bmask;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sl[j] = tkeys[b * kSlotsPerBucket + j];
+    }
+    return false;
+}
 
 __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __restrict__ tkeys,
                                                             const uint64_t* __restrict__ tlocs, uint64_t capacity,
@@ -71,57 +99,53 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
         return;
     }
     const int64_t n = k1 - k0;
-    const uint32_t grp = lane >> 2, sub = lane & 3;
-    const uint64_t n_buckets = capacity / kSlotsPerBucket;
-    const uint64_t bmask = n_buckets - 1;
-    const uint64_t lead_lanes = 0x1111111111111111ull;   // lane 0 of every group
+    const uint64_t bmask = capacity / kSlotsPerBucket - 1;
     const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
 
-    int64_t h = 0;
-    int steps = 1;
-    while (h < n) {
-        uint4 kq[kMaxWindowSteps], sq[kMaxWindowSteps];
-        uint64_t bq[kMaxWindowSteps];
-        bool vq[kMaxWindowSteps];
+    // Key idx of the request, or the marker past its end (the load index stays inside the request,
+    // so the load itself is always in bounds when n > 0).
+    auto key_at = [&](int64_t idx, bool want) {
+        const int64_t j = idx < n ? idx : n - 1;
+        const uint4 x = keys[k0 + j];
+        return (want && idx < n) ? x : marker;
+    };
+    if (n == 0) {
+        if (lane == 0) hits[r] = 0;
+        return;
+    }
+    int64_t base = 0;
+    int chunks = 1;
+    uint4 nk[kChunks];
 #pragma unroll
-        for (int q = 0; q < kMaxWindowSteps; ++q) {
-            const int64_t idx = h + grp + 16 * q;
-            vq[q] = q < steps && idx < n;
-            kq[q] = vq[q] ? keys[k0 + idx] : marker;
-        }
+    for (int c = 0; c < kChunks; ++c) nk[c] = key_at(base + 64 * c + lane, c < chunks);
+    int64_t h = n;
+    while (base < n) {
+        uint4 ck[kChunks], sl[kChunks][4];
+        bool v[kChunks];
+        uint64_t bk[kChunks];
 #pragma unroll
-        for (int q = 0; q < kMaxWindowSteps; ++q) {
-            bq[q] = home_bucket(kq[q], bmask);
-            sq[q] = vq[q] ? tkeys[bq[q] * kSlotsPerBucket + sub] : marker;
+        for (int c = 0; c < kChunks; ++c) {
+            ck[c] = nk[c];
+            v[c] = c < chunks && base + 64 * c + lane < n;
+            bk[c] = home_bucket(ck[c], bmask);
+            if (v[c]) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) sl[c][j] = tkeys[bk[c] * kSlotsPerBucket + j];
+            }
         }
+        // next window: twice as many chunks, up to kChunks
+        const int next_chunks = chunks * 2 < kChunks ? chunks * 2 : kChunks;
+        const int64_t next_base = base + 64 * chunks;
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) nk[c] = key_at(next_base + 64 * c + lane, c < next_chunks);
         int64_t stop = -1;
 #pragma unroll
-        for (int q = 0; q < kMaxWindowSteps; ++q) {
-            if (q >= steps) break;
-            const bool special = vq[q] && is_marker(kq[q]);   // the key that equals the empty marker
-            bool open = vq[q] && !special;                    // still probing
-            bool found = false;
-            uint4 slot = sq[q];
-            uint64_t b = bq[q];
-            for (uint64_t it = 0; it < n_buckets; ++it) {
-                const uint64_t m = __ballot(open && eq4(slot, kq[q]));
-                const uint64_t z = __ballot(open && is_marker(slot));
-                if (open) {
-                    if ((m >> (4 * grp)) & 0xF) { found = true; open = false; }
-                    else if ((z >> (4 * grp)) & 0xF) { open = false; }
-                }
-                if (__ballot(open) == 0) break;
-                if (open) {
-                    b = (b + 1) & bmask;
-                    slot = tkeys[b * kSlotsPerBucket + sub];
-                }
-            }
-            if (special) found = tlocs[capacity] != kEmpty;
-            const uint64_t valid = __ballot(vq[q]) & lead_lanes;
-            const uint64_t hit = __ballot(vq[q] && found) & lead_lanes;
-            const uint64_t miss = valid & ~hit;
+        for (int c = 0; c < kChunks; ++c) {
+            if (c >= chunks) break;
+            const bool found = v[c] && probe_key(tkeys, tlocs, capacity, bmask, ck[c], bk[c], sl[c]);
+            const uint64_t miss = __ballot(v[c] && !found);
             if (miss) {
-                stop = h + 16 * q + (__builtin_ctzll(miss) >> 2);
+                stop = base + 64 * c + __builtin_ctzll(miss);
                 break;
             }
         }
@@ -129,11 +153,10 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
             h = stop;
             break;
         }
-        h += 16 * steps;
-        if (h > n) h = n;
-        if (steps < kMaxWindowSteps) steps *= 2;
+        base = next_base;
+        chunks = next_chunks;
     }
-    if (lane == 0) hits[r] = static_cast<int32_t>(h);
+    if (lane == 0) hits[r] = static_cast<int32_t>(h < n ? h : n);
 }
 
 // ---- store ------------------------------------------------------------------------------------
