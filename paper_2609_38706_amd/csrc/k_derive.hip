@@ -300,6 +300,198 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_b16_pc(ChainArgs a) {
     }
 }
 
+// ---- B = 16m (m >= 2), two wavefronts per 64 chains (used while chains are scarce) -------------
+// Same split as for B = 16: the consumer issues only rounds.  Compression 1 of each key (previous
+// key | digest | tokens 0..7) runs in four barrier phases while the helper computes its schedule;
+// the m token-only compressions that follow (tokens 16c-8 .. 16c+7, the last one padded) are
+// produced by the helper two compressions ahead into a ring of three LDS slots, and the consumer
+// holds the next compression's 64 K + W words in registers while it runs the current one.
+struct PcmShared {
+    uint4 kwt[3][16][64];      // K_t + W_t of token-only compressions, three slots
+    uint4 w1tok[2][2][64];     // W8..W15 of compression 1 (byte-swapped tokens 0..7), two keys
+    uint4 kw1tok[2][2][64];    // K_t + W_t for t = 8..15 of compression 1, two keys
+    uint4 kw1hi[12][64];       // K_t + W_t for t = 16..63 of compression 1 (current key)
+    uint4 prev[64];            // previous key words (consumer -> helper)
+};
+
+// Token words of one production: the 16 (or, for the last compression, 8) words of token
+// compression (key, c), and for c == 1 also tokens 0..7 of that key (compression 1's words).
+struct Production {
+    uint32_t head[8];
+    uint32_t w[16];
+};
+
+// Production g (global, g = key * m + (c - 1)) of one lane: compression c (1..m) of `key`.
+// Every word is written on every path (zeros past the lane's last key or past the block).
+__device__ __forceinline__ void load_production(const int32_t* tp, uint32_t B, uint32_t m, int64_t n, int64_t g,
+                                                Production& pr) {
+    const int64_t key = g / m;
+    const uint32_t c = static_cast<uint32_t>(g - key * m) + 1;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) pr.head[q] = 0u;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) pr.w[q] = 0u;
+    if (key < n) {
+        const int32_t* k = tp + key * static_cast<int64_t>(B);
+        if (c == 1) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) pr.head[q] = static_cast<uint32_t>(k[q]);
+        }
+        const int32_t* src = k + 16 * c - 8;
+        if (c < m) {
+#pragma unroll
+            for (int q = 0; q < 16; ++q) pr.w[q] = static_cast<uint32_t>(src[q]);
+        } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) pr.w[q] = static_cast<uint32_t>(src[q]);
+        }
+    }
+}
+
+__device__ __forceinline__ void produce_comp(PcmShared& sh, uint32_t lane, uint32_t m, uint32_t bitlen, int64_t g,
+                                             const Production& pr) {
+    const int64_t key = g / m;
+    const uint32_t c = static_cast<uint32_t>(g - key * m) + 1;
+    if (c == 1) {
+        const int kb = static_cast<int>(key & 1);
+        uint32_t v[8], kv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) { v[q] = bswap(pr.head[q]); kv[q] = v[q] + kRoundK[8 + q]; }
+        put4(&sh.w1tok[kb][0][lane], v);
+        put4(&sh.w1tok[kb][1][lane], v + 4);
+        put4(&sh.kw1tok[kb][0][lane], kv);
+        put4(&sh.kw1tok[kb][1][lane], kv + 4);
+    }
+    uint32_t w[16], kw[16];
+    if (c < m) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) w[q] = bswap(pr.w[q]);
+    } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) w[q] = bswap(pr.w[q]);
+        w[8] = 0x80000000u;
+#pragma unroll
+        for (int q = 9; q < 15; ++q) w[q] = 0u;
+        w[15] = bitlen;
+    }
+    const int slot = static_cast<int>(g % 3);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) kw[q] = w[q] + kRoundK[q];
+    lds_put16(&sh.kwt[slot][0], lane, kw);
+    schedule16<16>(w, kw);
+    lds_put16(&sh.kwt[slot][4], lane, kw);
+    schedule16<32>(w, kw);
+    lds_put16(&sh.kwt[slot][8], lane, kw);
+    schedule16<48>(w, kw);
+    lds_put16(&sh.kwt[slot][12], lane, kw);
+}
+
+__global__ __launch_bounds__(kPcThreads) void k_derive_m16_pc(ChainArgs a) {
+    __shared__ PcmShared sh;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t r = blockIdx.x * 64 + lane;
+    const uint32_t B = a.block, m = B / 16;
+    const uint32_t bitlen = (32u + 4u * B) * 8u;
+    int64_t t0 = 0, k0 = 0, n = 0;
+    bool valid = r < a.n_req;
+    if (valid && !chain_bounds(a, r, t0, k0, n)) valid = false;
+    if (!valid) n = 0;
+    const int64_t nmax = wave_max(n);           // identical in both wavefronts
+    uint32_t dg[4] = {0u, 0u, 0u, 0u};
+    if (valid) load_digest(a, r, dg);
+    const int32_t* tp = a.tokens + t0;
+
+    if (wave == 0) {
+        // ---------------- consumer ----------------
+        uint32_t prev[4] = {0u, 0u, 0u, 0u};
+        uint32_t dgk[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) dgk[q] = dg[q] + kRoundK[4 + q];
+        put4(&sh.prev[lane], prev);
+        __syncthreads();                                       // prologue
+        for (int64_t i = 0; i < nmax; ++i) {
+            const int kb = static_cast<int>(i & 1);
+            uint32_t s[8], h[8], kw[16];
+            init_state(s);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) { kw[q] = prev[q] + kRoundK[q]; kw[4 + q] = dgk[q]; }
+            get4(&sh.kw1tok[kb][0][lane], kw + 8);
+            get4(&sh.kw1tok[kb][1][lane], kw + 12);
+            rounds16(s, kw);                                   // rounds 0..15
+            __syncthreads();
+            lds_get16(&sh.kw1hi[0], lane, kw);
+            rounds16(s, kw);                                   // rounds 16..31
+            __syncthreads();
+            lds_get16(&sh.kw1hi[4], lane, kw);
+            rounds16(s, kw);                                   // rounds 32..47
+            __syncthreads();
+            lds_get16(&sh.kw1hi[8], lane, kw);
+            rounds16(s, kw);                                   // rounds 48..63
+#pragma unroll
+            for (int q = 0; q < 8; ++q) h[q] = s[q] + kInitH[q];
+            __syncthreads();                                   // end of compression 1
+            for (uint32_t c = 1; c <= m; ++c) {
+                const int64_t g = i * m + (c - 1);             // produced two compressions ago
+                uint32_t kwc[64];
+#pragma unroll
+                for (int ph = 0; ph < 4; ++ph) lds_get16(&sh.kwt[g % 3][4 * ph], lane, kwc + 16 * ph);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) s[q] = h[q];
+#pragma unroll
+                for (int ph = 0; ph < 4; ++ph) rounds16(s, kwc + 16 * ph);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) h[q] += s[q];
+                if (c == m) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) prev[q] = h[q];
+                    if (i < n) store_key(a.keys, k0 + i, prev);
+                    put4(&sh.prev[lane], prev);
+                }
+                __syncthreads();                               // end of token compression c
+            }
+        }
+    } else {
+        // ---------------- helper ----------------
+        const int64_t total = nmax * m;                        // token compressions of the wavefront
+        Production p0, p1, p2;
+        load_production(tp, B, m, n, 0, p0);
+        load_production(tp, B, m, n, 1, p1);
+        produce_comp(sh, lane, m, bitlen, 0, p0);
+        produce_comp(sh, lane, m, bitlen, 1, p1);
+        load_production(tp, B, m, n, 2, p0);                   // p0, p1 = productions g + 2, g + 3
+        load_production(tp, B, m, n, 3, p1);
+        __syncthreads();                                       // prologue
+        for (int64_t i = 0; i < nmax; ++i) {
+            const int kb = static_cast<int>(i & 1);
+            uint32_t w[16], kw[16];
+            get4(&sh.prev[lane], w);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) w[4 + q] = dg[q];
+            get4(&sh.w1tok[kb][0][lane], w + 8);
+            get4(&sh.w1tok[kb][1][lane], w + 12);
+            schedule16<16>(w, kw);
+            lds_put16(&sh.kw1hi[0], lane, kw);
+            __syncthreads();
+            schedule16<32>(w, kw);
+            lds_put16(&sh.kw1hi[4], lane, kw);
+            __syncthreads();
+            schedule16<48>(w, kw);
+            lds_put16(&sh.kw1hi[8], lane, kw);
+            __syncthreads();
+            __syncthreads();                                   // end of compression 1
+            for (uint32_t c = 1; c <= m; ++c) {
+                const int64_t g = i * m + (c - 1) + 2;         // production made during compression (i, c)
+                p2 = p0;
+                p0 = p1;
+                load_production(tp, B, m, n, g + 2, p1);
+                if (g < total) produce_comp(sh, lane, m, bitlen, g, p2);
+                __syncthreads();                               // end of token compression c
+            }
+        }
+    }
+}
+
 // ---- B = 16m, m >= 2: m + 1 compressions per key -------------------------------------------
 // Message blocks of one key: block 0 = prev | digest | tokens 0..7; block c (1..m-1) = tokens
 // 16c-8 .. 16c+7; block m = tokens 16m-8 .. 16m-1 | padding.  The token words of the next block
@@ -517,6 +709,8 @@ int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_o
         hipLaunchKernelGGL(k_derive_b16_pc, grid, dim3(kPcThreads), 0, s, a);
     } else if (block == 16) {
         hipLaunchKernelGGL(k_derive_b16, grid, dim3(kDeriveThreads), 0, s, a);
+    } else if (block % 16 == 0 && grid.x <= static_cast<unsigned>(compute_units())) {
+        hipLaunchKernelGGL(k_derive_m16_pc, grid, dim3(kPcThreads), 0, s, a);
     } else if (block % 16 == 0) {
         hipLaunchKernelGGL(k_derive_m16, grid, dim3(kDeriveThreads), 0, s, a);
     } else {
