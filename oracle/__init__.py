@@ -14,7 +14,8 @@ import subprocess
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "liboracle.so")
+# PKV_ORACLE_LIB points the tests at another build of this oracle (the mutation tests use it).
+LIB_PATH = os.environ.get("PKV_ORACLE_LIB") or os.path.join(HERE, "liboracle.so")
 SOURCES = [os.path.join(HERE, "pkv_oracle.c")]
 
 OK, EINVAL, EDUPDIM, ERESERVED, EFULL = 0, -1, -2, -3, -4

@@ -143,8 +143,9 @@ def test_lookup_and_store_random_keys(pkv, seed, capacity):
         hits = torch.zeros(max(1, n_req), dtype=torch.int32, device="cuda")
         pkv.pkv_lookup_prefix(table, dk, dko, hits[:n_req], status)
         assert (hits[:n_req].cpu().numpy() == hits_o).all(), (rnd, hits[:n_req].cpu().numpy(), hits_o)
-        # store from the lookup result, or from a lower arbitrary hit count
-        h = np.minimum(hits_o, rng.integers(0, 12, size=n_req)).astype(np.int32) if rnd == 2 else hits_o
+        # store from the lookup result, or (last round) from arbitrary hit counts, which may exceed
+        # the lookup's: keys below the given count are never inserted
+        h = rng.integers(0, 14, size=n_req).astype(np.int32) if rnd == 2 else hits_o
         rc = idx.store(keys, ko, h, locs)
         pkv.pkv_store(table, dk, dko, _dev(h, torch.int32), _dev(locs, torch.int64), n_new, status)
         torch.cuda.synchronize()

@@ -98,3 +98,27 @@ def test_threads_do_not_change_results():
     a = _req(reqs, 16, d, threads=1)
     b = _req(reqs, 16, d, threads=5)
     assert all((x == y).all() for x, y in zip(a, b))
+
+
+def _library_chain(tokens, digest: bytes, block: int):
+    """The chain written out with the library SHA-256: key_i = SHA-256(key_{i-1} | d | LE32 tokens)[:16]."""
+    prev, out = bytes(16), []
+    for i in range(len(tokens) // block):
+        blk = struct.pack("<%di" % block, *[int(t) for t in tokens[i * block:(i + 1) * block]])
+        prev = hashlib.sha256(prev + digest + blk).digest()[:16]
+        out.append(prev)
+    return out
+
+
+@pytest.mark.parametrize("block", [1, 2, 5, 16, 17, 64, 256])
+def test_whole_chains_match_library_sha256(block):
+    """Brute force on tiny inputs: every key of several ragged requests, recomputed from the byte-level
+    definition with the library routine (OpenSSL SHA-256), not with the oracle's own hash."""
+    rng = np.random.default_rng(100 + block)
+    reqs = [rng.integers(-2**31, 2**31, size=int(rng.integers(0, 5 * block + 3)), dtype=np.int64).astype(np.int32)
+            for _ in range(6)]
+    digs = rng.integers(0, 256, size=(6, 16), dtype=np.uint8)
+    got = _req(reqs, block, digs)
+    for r in range(6):
+        want = _library_chain(reqs[r], digs[r].tobytes(), block)
+        assert [bytes(k) for k in got[r]] == want

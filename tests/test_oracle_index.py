@@ -128,3 +128,22 @@ def test_the_all_ff_key_does_not_use_capacity():
     assert idx.store(keys, off, np.zeros(1, np.int32), np.arange(9, dtype=np.uint64)) == 0
     assert len(idx) == 9
     assert (idx.lookup(keys, off) == 9).all()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_store_skips_keys_below_the_given_hits(seed):
+    """The store path inserts only keys j >= hits[r], whatever the hits say: a caller that already holds
+    a prefix (for instance from a local cache) passes its length and those keys stay out of the index."""
+    rng = np.random.default_rng(300 + seed)
+    pool = rng.integers(0, 256, size=(50, 16), dtype=np.uint8)
+    n_req = int(rng.integers(1, 10))
+    lens = rng.integers(0, 9, size=n_req)
+    key_off = np.zeros(n_req + 1, np.int64)
+    key_off[1:] = np.cumsum(lens)
+    keys = _rand_keys(rng, int(key_off[-1]), pool)
+    locs = rng.permutation(10_000)[: int(key_off[-1])].astype(np.uint64)
+    hits = np.array([int(rng.integers(0, n + 2)) for n in lens], np.int32)     # may exceed the true hits
+    idx = oracle.Index(1024)
+    assert idx.store(keys, key_off, hits, locs) == 0
+    dk, dl = idx.dump()
+    assert {bytes(k): int(v) for k, v in zip(dk, dl)} == _brute_store({}, keys, key_off, hits, locs)
