@@ -600,6 +600,34 @@ __global__ __launch_bounds__(kDeriveThreads) void k_derive_any(ChainArgs a) {
 }
 
 // ---- batched descriptor digests: one lane per canonical encoding ----------------------------
+// Message word q (big-endian) of a message of L bytes at p with the FIPS 180-4 padding applied
+// (bytes past L become 0x80 then zeros), assembled byte by byte: the path for messages that are
+// unaligned or empty.
+__device__ __forceinline__ uint32_t msg_word_bytes(const uint8_t* p, uint64_t L, uint64_t q) {
+    const uint64_t b0 = 4 * q;
+    if (b0 >= L) return b0 == L ? 0x80000000u : 0u;
+    uint32_t v = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+        const uint64_t pos = b0 + b;
+        const uint32_t byte = pos < L ? p[pos] : (pos == L ? 0x80u : 0u);
+        v = (v << 8) | byte;
+    }
+    return v;
+}
+
+// The same word from an aligned message whose rounded-up length lies inside the pool: the dword
+// is loaded unconditionally (index clamped to the message's last word) and padded with selects,
+// so loads of a whole block can be issued together.
+__device__ __forceinline__ uint32_t msg_word_fast(const uint32_t* p4, uint64_t L, uint64_t q) {
+    const uint64_t last = (L - 1) >> 2;                  // L > 0 on this path
+    const uint32_t be = bswap(p4[q < last ? q : last]);
+    const int64_t r = static_cast<int64_t>(L) - static_cast<int64_t>(4 * q);   // message bytes in this word
+    const uint32_t keep = r >= 4 ? 0xFFFFFFFFu : (r <= 0 ? 0u : (0xFFFFFFFFu << (8 * (4 - r))));
+    const uint32_t pad = (r >= 0 && r < 4) ? (0x80u << (8 * (3 - r))) : 0u;
+    return (be & keep) | pad;
+}
+
 __global__ __launch_bounds__(64) void k_digest(const uint8_t* bytes, uint64_t n_bytes, const int64_t* off,
                                                const uint32_t* len, uint32_t n, uint8_t* out, int32_t* status) {
     const uint32_t i = blockIdx.x * 64 + threadIdx.x;
@@ -611,22 +639,33 @@ __global__ __launch_bounds__(64) void k_digest(const uint8_t* bytes, uint64_t n_
         return;
     }
     const uint8_t* p = bytes + o;
+    const bool fast = L > 0 && (reinterpret_cast<uintptr_t>(p) & 3) == 0 &&
+                      static_cast<uint64_t>(o) + ((L + 3) & ~3ull) <= n_bytes;
+    const uint32_t* p4 = reinterpret_cast<const uint32_t*>(p);
     const uint64_t n_blocks = (L + 9 + 63) / 64;
     const uint64_t bitlen = L * 8;
-    uint32_t s[8];
+    uint32_t s[8], nxt[16];
     init_state(s);
+    if (fast) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) nxt[q] = msg_word_fast(p4, L, q);
+    } else {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) nxt[q] = msg_word_bytes(p, L, q);
+    }
     for (uint64_t c = 0; c < n_blocks; ++c) {
         uint32_t w[16];
-        for (int q = 0; q < 16; ++q) {
-            uint32_t v = 0;
-            for (int b = 0; b < 4; ++b) {
-                const uint64_t pos = 64 * c + 4 * q + b;
-                const uint32_t byte = pos < L ? p[pos] : (pos == L ? 0x80u : 0u);
-                v = (v << 8) | byte;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) w[q] = nxt[q];
+        if (c + 1 < n_blocks) {                        // the next block's words load under this compression
+            if (fast) {
+#pragma unroll
+                for (int q = 0; q < 16; ++q) nxt[q] = msg_word_fast(p4, L, 16 * (c + 1) + q);
+            } else {
+#pragma unroll
+                for (int q = 0; q < 16; ++q) nxt[q] = msg_word_bytes(p, L, 16 * (c + 1) + q);
             }
-            w[q] = v;
-        }
-        if (c + 1 == n_blocks) {
+        } else {
             w[14] = static_cast<uint32_t>(bitlen >> 32);
             w[15] = static_cast<uint32_t>(bitlen);
         }

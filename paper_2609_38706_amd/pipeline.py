@@ -28,10 +28,12 @@ class DeviceBatch:
         self.tok_off = torch.from_numpy(np.ascontiguousarray(tok_off, dtype=np.int64)).to(device)
         encs = [pkv_descriptor_encode(d) for d in descs]
         lens = np.array([len(e) for e in encs], dtype=np.int64)
+        # each encoding starts on a 4-byte boundary, so the digest kernel reads whole words
+        padded = [e + b"\0" * (-len(e) % 4) for e in encs]
         offs = np.zeros(len(encs), dtype=np.int64)
         if len(encs) > 1:
-            offs[1:] = np.cumsum(lens)[:-1]
-        pool = np.frombuffer(b"".join(encs) or b"\0", dtype=np.uint8)
+            offs[1:] = np.cumsum([len(e) for e in padded])[:-1]
+        pool = np.frombuffer(b"".join(padded) or b"\0", dtype=np.uint8)
         didx = np.asarray(desc_idx, dtype=np.int64)
         self.pool = torch.from_numpy(pool.copy()).to(device)
         self.msg_off = torch.from_numpy(offs[didx].copy()).to(device)

@@ -52,6 +52,34 @@ def test_digest_batch_matches_oracle(pkv):
     assert (got == oracle.batch_digests(b)).all()
 
 
+def test_digest_batch_unaligned_pool(pkv):
+    """Messages at odd byte offsets, one ending on the pool's last byte, and empty messages."""
+    import torch
+    rng = np.random.default_rng(1)
+    encs, offs, pool = [], [], b""
+    for i in range(70):
+        n = int(rng.integers(0, 6))
+        desc = [(b"f%d" % j, rng.bytes(int(rng.integers(0, 90)))) for j in range(n)]
+        e = oracle.encode(desc)
+        pool += rng.bytes(int(rng.integers(1, 4)))          # junk: the next message starts unaligned
+        offs.append(len(pool))
+        pool += e
+        encs.append(e)
+    offs.append(len(pool))                                   # an empty message at the very end
+    encs.append(b"")
+    lens = [len(e) for e in encs]
+    d_pool = torch.from_numpy(np.frombuffer(pool, np.uint8).copy()).cuda()
+    d_off = torch.tensor(offs, dtype=torch.int64, device="cuda")
+    d_len = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    out = torch.zeros((len(encs), 16), dtype=torch.uint8, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pkv.pkv_digest_batch(d_pool, d_off, d_len, out, status)
+    got = out.cpu().numpy()
+    assert int(status.item()) == 0
+    for i, e in enumerate(encs):
+        assert got[i].tobytes() == oracle.sha256(e)[:16]
+
+
 @pytest.mark.parametrize("block", [1, 2, 3, 7, 15, 16, 17, 31, 32, 48, 64, 100, 256, 257])
 def test_derive_matches_oracle_any_block(pkv, block):
     rng = np.random.default_rng(block)
