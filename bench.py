@@ -4,7 +4,9 @@
 One step = one pass of the whole hot path over one synthetic request batch, inputs resident in
 HBM: key offsets -> descriptor digests -> chained block keys -> longest-prefix lookup -> store of
 the misses (then the step's new entries are rolled back so that every step meets the same
-index).  The default workload is 1024 requests x 2048 tokens, block 16, against a 4M-slot index
+index).  Consecutive steps run on two streams: the derive of step k+1 overlaps the index work of
+step k, which stays in step order on its own stream.  A serial run of the same steps is reported
+beside it.  The default workload is 1024 requests x 2048 tokens, block 16, against a 4M-slot index
 at load 0.5.
 
 Prints one JSON line: Gkeys/s (keys derived and probed per second), the derive kernel's share of
@@ -114,16 +116,19 @@ def setup_gpu(args, w):
         if db.host_status() != 0:
             raise RuntimeError(f"index preparation failed: status {db.host_status()}")
         del db
-    run = DeviceBatch.from_batch(w.batch)
-    run.set_locations(locations(run.key_off.cpu().numpy(), w.batch.tag))
-    return pkv, table, run
+    # two buffer sets of the same batch, so that consecutive steps can overlap on two streams
+    runs = []
+    for _ in range(2):
+        run = DeviceBatch.from_batch(w.batch)
+        run.set_locations(locations(run.key_off.cpu().numpy(), w.batch.tag))
+        runs.append(run)
+    return pkv, table, runs
 
 
-def gpu_leg(args, w):
+def serial_leg(args, table, run):
+    """Steps one after another on one stream, every kernel bracketed by events: the per-kernel times."""
     import torch
-    pkv, table, run = setup_gpu(args, w)
     stream = torch.cuda.current_stream()
-    n_keys = run.n_keys
 
     def step(ev=None):
         run.n_new.zero_()
@@ -144,9 +149,6 @@ def gpu_leg(args, w):
 
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-    if run.host_status() != 0:
-        raise RuntimeError(f"step failed: status {run.host_status()}")
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -156,13 +158,41 @@ def gpu_leg(args, w):
     t1 = time.perf_counter()
     if run.host_status() != 0:
         raise RuntimeError(f"step failed: status {run.host_status()}")
-    ms = (t1 - t0) * 1e3 / args.steps
-    derive_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    lookup_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    store_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    return {"ms": (t1 - t0) * 1e3 / args.steps,
+            "derive_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evs])),
+            "lookup_ms": float(np.mean([e[1].elapsed_time(e[2]) for e in evs])),
+            "store_ms": float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))}
+
+
+def gpu_leg(args, w):
+    """The timed region: K steps, consecutive steps overlapped on two streams (the derive of step k+1
+    runs while step k is looked up, stored and rolled back).  Only the derive is bracketed by events,
+    on the stream it is launched on."""
+    import torch
+    from paper_2609_38706_amd.pipeline import TwoStreamRunner
+    pkv, table, runs = setup_gpu(args, w)
+    serial = serial_leg(args, table, runs[0])
+    runner = TwoStreamRunner(table)
+    order = [runs[i % 2] for i in range(max(args.steps, args.warmup))]
+    runner.run(order[: args.warmup], rollback=True)
+    torch.cuda.synchronize()
+    for r in runs:
+        if r.host_status() != 0:
+            raise RuntimeError(f"step failed: status {r.host_status()}")
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    runner.run(order[: args.steps], rollback=True, derive_events=evs)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for r in runs:
+        if r.host_status() != 0:
+            raise RuntimeError(f"step failed: status {r.host_status()}")
+    run = runs[(args.steps - 1) % 2]
     hits = run.host_hits()
-    return {"ms": ms, "derive_ms": derive_ms, "lookup_ms": lookup_ms, "store_ms": store_ms, "n_keys": n_keys,
-            "n_req": run.n_req, "hit_blocks": int(hits.sum()), "new_entries": int(run.n_new.item())}
+    return {"ms": (t1 - t0) * 1e3 / args.steps, "derive_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evs])),
+            "serial": serial, "n_keys": run.n_keys, "n_req": run.n_req, "hit_blocks": int(hits.sum()),
+            "new_entries": int(run.n_new.item())}
 
 
 def saturation_leg(args, n_chains=131072, blocks=16, reps=5):
@@ -267,8 +297,12 @@ def main():
         "dtype": "u32", "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload, "requests": g["n_req"],
                    "keys": g["n_keys"], "block": block, "capacity": w.capacity, "parallelism": "1 GPU"},
-        "kernels_ms": {"derive": round(g["derive_ms"], 4), "lookup": round(g["lookup_ms"], 4),
-                       "store": round(g["store_ms"], 4)},
+        "kernels_ms": {"derive": round(g["derive_ms"], 4), "lookup": round(g["serial"]["lookup_ms"], 4),
+                       "store": round(g["serial"]["store_ms"], 4), "derive_serial": round(g["serial"]["derive_ms"], 4)},
+        "pipeline": {"streams": 2, "overlap": "derive of step k+1 with lookup/store/rollback of step k",
+                     "serial_ms_per_step": round(g["serial"]["ms"], 4),
+                     "serial_value": round(g["n_keys"] / (g["serial"]["ms"] * 1e-3) / 1e9, 6),
+                     "hit_blocks": g["hit_blocks"], "new_entries": g["new_entries"]},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "derive_saturated": sat,

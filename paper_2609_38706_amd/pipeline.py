@@ -119,3 +119,66 @@ def sort_pairs(keys: np.ndarray, locs: np.ndarray):
     words = np.ascontiguousarray(keys).view(">u8").reshape(-1, 2)
     order = np.lexsort((words[:, 1], words[:, 0]))
     return keys[order], locs[order]
+
+
+class TwoStreamRunner:
+    """Runs consecutive batches through the hot path on two HIP streams.
+
+    Key derivation touches no index state, so the derive of batch k+1 can run while batch k is looked
+    up and stored.  Every index operation (lookup, store, rollback) stays on one stream in batch
+    order, so the hit lengths and the index contents equal those of running the batches one after
+    another.  The preparation of a batch (key offsets, descriptor digests) also runs on the index
+    stream, after the previous use of that batch's buffers, which keeps it off the derive stream.
+
+    Both streams have the default priority.  A ``DeviceBatch`` may be reused (its buffers are
+    recycled once its previous pass has finished) but not twice in a row.
+    """
+
+    def __init__(self, table: Table):
+        import torch
+        self.table = table
+        self.s_derive = torch.cuda.Stream()
+        self.s_index = torch.cuda.Stream()
+
+    def run(self, batches, rollback: bool = False, derive_events=None):
+        """Enqueue one pass per entry of ``batches``; returns without synchronizing.
+        ``derive_events[k]`` (a pair of timing events), when given, brackets the derive of pass k on
+        the derive stream."""
+        import torch
+        batches = list(batches)
+        for a, b in zip(batches, batches[1:]):
+            if a is b:
+                raise ValueError("the same DeviceBatch cannot run twice in a row")
+        cur = torch.cuda.current_stream()
+        self.s_derive.wait_stream(cur)
+        self.s_index.wait_stream(cur)
+        if not batches:
+            return
+
+        def prepare(db):
+            db.key_offsets(self.s_index)
+            db.digest(self.s_index)
+            ev = torch.cuda.Event()
+            ev.record(self.s_index)
+            return ev
+
+        ready = prepare(batches[0])
+        for k, db in enumerate(batches):
+            self.s_derive.wait_event(ready)
+            ev = derive_events[k] if derive_events is not None else None
+            if ev is not None:
+                ev[0].record(self.s_derive)
+            db.derive(self.s_derive)
+            done = ev[1] if ev is not None else torch.cuda.Event()
+            done.record(self.s_derive)
+            if k + 1 < len(batches):
+                ready = prepare(batches[k + 1])     # after the index work of its previous pass
+            self.s_index.wait_event(done)
+            with torch.cuda.stream(self.s_index):
+                db.n_new.zero_()
+            db.lookup(self.table, self.s_index)
+            db.store(self.table, self.s_index)
+            if rollback:
+                db.rollback(self.table, self.s_index)
+        cur.wait_stream(self.s_derive)
+        cur.wait_stream(self.s_index)
