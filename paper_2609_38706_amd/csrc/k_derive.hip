@@ -157,7 +157,8 @@ __device__ __forceinline__ void schedule16(uint32_t w[16], uint32_t kw[16]) {
     }
 }
 
-__device__ __forceinline__ void lds_put16(uint4 (*dst)[64], uint32_t lane, const uint32_t kw[16]) {
+template <unsigned N>
+__device__ __forceinline__ void lds_put16(uint4 (*dst)[N], uint32_t lane, const uint32_t kw[16]) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) put4(&dst[q][lane], kw + 4 * q);
 }
@@ -186,8 +187,9 @@ __device__ __forceinline__ void load_tokens16(const int32_t* tp, int64_t key, in
     }
 }
 
-// Token-only data of one key (16 tokens tk) into buffer `buf`.
-__device__ __forceinline__ void produce_key(PcShared& sh, uint32_t lane, int buf, const uint32_t tk[16]) {
+// Token-only data of one key (16 tokens tk) into buffer `buf` of column `lane`.
+template <typename Shared>
+__device__ __forceinline__ void produce_key(Shared& sh, uint32_t lane, int buf, const uint32_t tk[16]) {
     uint32_t v[8], kv[8], w[16], kw[16];
 #pragma unroll
     for (int q = 0; q < 8; ++q) { v[q] = bswap(tk[q]); kv[q] = v[q] + kRoundK[8 + q]; }
@@ -295,6 +297,232 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_b16_pc(ChainArgs a) {
             for (int q = 0; q < 16; ++q) tk[q] = pre[q];
             load_tokens16(tp, i + 2, n, pre);
             produce_key(sh, lane, buf ^ 1, tk);
+            __syncthreads();                                   // end of key
+        }
+    }
+}
+
+// ---- B = 16, each chain on a lane pair (used while chains are very scarce) ---------------------
+// Within one SHA-256 round the e-half (Sigma1, Ch, h + K_t + W_t) and the a-half (Sigma0, Maj) are
+// independent until the final sums.  The consumer wavefront gives each chain two lanes: the even
+// lane holds e, f, g, h and the odd lane a, b, c, d.  Both lanes run one instruction stream:
+//   * three rotates with per-lane amounts and a 3-input XOR give Sigma1 / Sigma0;
+//   * Maj(a, b, c) = Ch(~(a ^ b), b, c), so one select operand (x0 on the even lane, ~(x0 ^ x1) on
+//     the odd lane) and one Ch give Ch / Maj;
+//   * Y = Sigma + Ch/Maj + Q, where Q = h + K_t + W_t on the even lane and 0 on the odd lane, so
+//     Y = T1 on the even lane and Sigma0 + Maj on the odd lane;
+//   * one swap of neighbouring lanes (DPP) hands d to the even lane and T1 to the odd lane, and
+//     one add gives e' = d + T1 and a' = T1 + Sigma0 + Maj.
+// That is 11 instructions per round per wavefront instead of 14, which shortens the serial chain
+// by a fifth at 32 chains per wavefront.  The rounds are written as fixed instruction blocks: the
+// next round's Q sits between the producer of the swapped value and the DPP read, which covers
+// the two wait states a DPP read of a just-written register needs.  The helper wavefront splits
+// each chain's message schedule the same way (even words on the even lane, odd words on the odd
+// lane), so it keeps ahead of the faster consumer; the token-only work of the next key is done by
+// one helper lane per chain, as in the two-wavefront kernel above.
+constexpr uint32_t kPpChains = 32;
+
+struct PpShared {
+    uint4 kw2[2][16][kPpChains];      // K_t + W_t of compression 2, two keys
+    uint4 w1tok[2][2][kPpChains];     // W8..W15 of compression 1, two keys
+    uint4 kw1tok[2][2][kPpChains];    // K_t + W_t, t = 8..15 of compression 1, two keys
+    uint4 kw1hi[12][kPpChains];       // K_t + W_t, t = 16..63 of compression 1 (current key)
+    uint4 prev[kPpChains];            // previous key words
+};
+
+struct PairLane {
+    uint32_t m, nm, r1, r2, r3;       // all-ones on the odd (a) lane; its rotate amounts
+};
+
+// One paired round with the operand roles (x0, x1, x2, x3); the new x0 is written into x3's
+// register and Q of the next round is formed from x2 (next round's x3) and KWN.
+#define PKV_PAIR_ROUND(X0, X1, X2, X3, KWN)                                                        \
+    "v_alignbit_b32 %[t0], %[" #X0 "], %[" #X0 "], %[r1]\n"                                       \
+    "v_alignbit_b32 %[t1], %[" #X0 "], %[" #X0 "], %[r2]\n"                                       \
+    "v_alignbit_b32 %[t2], %[" #X0 "], %[" #X0 "], %[r3]\n"                                       \
+    "v_bitop3_b32 %[t0], %[t0], %[t1], %[t2] bitop3:0x96\n"                                       \
+    "v_bitop3_b32 %[t1], %[" #X0 "], %[" #X1 "], %[m] bitop3:0xd2\n"                              \
+    "v_bitop3_b32 %[t1], %[t1], %[" #X1 "], %[" #X2 "] bitop3:0xca\n"                             \
+    "v_add3_u32 %[t0], %[t0], %[t1], %[q]\n"                                                      \
+    "v_bitop3_b32 %[t1], %[m], %[" #X3 "], %[t0] bitop3:0xca\n"                                   \
+    "v_add_u32_e32 %[q], %[" #X2 "], %[" #KWN "]\n"                                               \
+    "v_and_b32_e32 %[q], %[q], %[nm]\n"                                                           \
+    "v_add_u32_dpp %[" #X3 "], %[t1], %[t0] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+
+// Four paired rounds; k1..k4 are K + W of the four rounds that follow each of them.  Afterwards
+// the state registers hold (x0, x1, x2, x3) in the same roles again.  Bit tables of v_bitop3
+// index the operands as (S0, S1, S2) = (0xF0, 0xCC, 0xAA): 0x96 = 3-input XOR,
+// 0xCA = S0 ? S1 : S2, 0xD2 = S2 ? ~(S0 ^ S1) : S0.
+__device__ __forceinline__ void pair_rounds4(uint32_t& x0, uint32_t& x1, uint32_t& x2, uint32_t& x3, uint32_t& q,
+                                             const PairLane& pl, uint32_t k1, uint32_t k2, uint32_t k3,
+                                             uint32_t k4) {
+    uint32_t t0, t1, t2;
+    asm volatile(PKV_PAIR_ROUND(a, b, c, d, k1) PKV_PAIR_ROUND(d, a, b, c, k2) PKV_PAIR_ROUND(c, d, a, b, k3)
+                     PKV_PAIR_ROUND(b, c, d, a, k4)
+                 : [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [q] "+v"(q), [a] "+v"(x0), [b] "+v"(x1),
+                   [c] "+v"(x2), [d] "+v"(x3)
+                 : [m] "v"(pl.m), [nm] "v"(pl.nm), [r1] "v"(pl.r1), [r2] "v"(pl.r2), [r3] "v"(pl.r3), [k1] "v"(k1),
+                   [k2] "v"(k2), [k3] "v"(k3), [k4] "v"(k4));
+}
+#undef PKV_PAIR_ROUND
+
+// 16 paired rounds; kw[j] = K + W of round t0 + j, `after` = K + W of round t0 + 16 (any value
+// when the caller recomputes q before the next round).
+__device__ __forceinline__ void pair_rounds16(uint32_t x[4], uint32_t& q, const PairLane& pl, const uint32_t* kw,
+                                              uint32_t after) {
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[1], kw[2], kw[3], kw[4]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[5], kw[6], kw[7], kw[8]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[9], kw[10], kw[11], kw[12]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[13], kw[14], kw[15], after);
+}
+
+__device__ __forceinline__ uint32_t lane_swap(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0xB1, 0xF, 0xF, false));
+}
+
+// One step of a message schedule split over a lane pair: the even lane computes W_{2j}, the odd
+// lane W_{2j+1}.  v[k] is the lane's own word k+1 steps back.  The even lane needs its partner's
+// W_{2j-7} and W_{2j-15}, the odd lane its partner's W_{2j-6} and W_{2j-14}; each lane sends
+// sigma0 of the older one plus the newer one.
+__device__ __forceinline__ uint32_t pair_schedule_step(uint32_t v[8], bool odd) {
+    const uint32_t z = dev::ssig0(odd ? v[7] : v[6]) + (odd ? v[3] : v[2]);
+    const uint32_t w = dev::ssig1(v[0]) + v[7] + lane_swap(z);
+#pragma unroll
+    for (int k = 7; k > 0; --k) v[k] = v[k - 1];
+    v[0] = w;
+    return w;
+}
+
+// Steps j = J0 .. J0+7 of the paired schedule; each lane writes K + W of its word into kw1hi.
+template <int J0>
+__device__ __forceinline__ void pair_schedule8(uint32_t v[8], bool odd, uint32_t* kw1hi_col) {
+#pragma unroll
+    for (int j = J0; j < J0 + 8; ++j) {
+        const uint32_t w = pair_schedule_step(v, odd);
+        const uint32_t k = odd ? kRoundK[2 * j + 1] : kRoundK[2 * j];
+        // word t = 2j + odd lives at [(t - 16) / 4][chain].component(t % 4); the lane's column
+        // pointer already includes its chain and parity
+        kw1hi_col[((2 * j - 16) >> 2) * (kPpChains * 4) + ((2 * j) & 3)] = w + k;
+    }
+}
+
+__global__ __launch_bounds__(kPcThreads) void k_derive_b16_pp(ChainArgs a) {
+    __shared__ PpShared sh;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t c = lane >> 1;                  // chain of this lane pair
+    const bool odd = (lane & 1) != 0;
+    const uint32_t r = blockIdx.x * kPpChains + c;
+    int64_t t0 = 0, k0 = 0, n = 0;
+    bool valid = r < a.n_req;
+    if (valid && !chain_bounds(a, r, t0, k0, n)) valid = false;
+    if (!valid) n = 0;
+    const int64_t nmax = wave_max(n);           // identical in both wavefronts
+    uint32_t dg[4] = {0u, 0u, 0u, 0u};
+    if (valid) load_digest(a, r, dg);
+
+    if (wave == 0) {
+        // ---------------- consumer: lane pair per chain ----------------
+        PairLane pl;
+        pl.m = odd ? ~0u : 0u;
+        pl.nm = ~pl.m;
+        pl.r1 = odd ? 2u : 6u;
+        pl.r2 = odd ? 13u : 11u;
+        pl.r3 = odd ? 22u : 25u;
+        uint32_t iv[4], dgk[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            iv[q] = odd ? kInitH[q] : kInitH[4 + q];
+            dgk[q] = dg[q] + kRoundK[4 + q];
+        }
+        if (odd) sh.prev[c] = make_uint4(0u, 0u, 0u, 0u);
+        __syncthreads();                                       // prologue
+        for (int64_t i = 0; i < nmax; ++i) {
+            const int buf = static_cast<int>(i & 1);
+            uint32_t x[4], kw[16], kw2[64], hmid[4], q;
+            get4(&sh.prev[c], kw);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) { kw[j] += kRoundK[j]; kw[4 + j] = dgk[j]; }
+            get4(&sh.kw1tok[buf][0][c], kw + 8);
+            get4(&sh.kw1tok[buf][1][c], kw + 12);
+#pragma unroll
+            for (int ph = 0; ph < 16; ++ph) get4(&sh.kw2[buf][ph][c], kw2 + 4 * ph);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) x[j] = iv[j];
+            q = (x[3] + kw[0]) & pl.nm;
+            pair_rounds16(x, q, pl, kw, 0u);                   // rounds 0..15
+            __syncthreads();
+#pragma unroll
+            for (int ph = 0; ph < 3; ++ph) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) get4(&sh.kw1hi[4 * ph + j][c], kw + 4 * j);
+                q = (x[3] + kw[0]) & pl.nm;
+                pair_rounds16(x, q, pl, kw, 0u);               // rounds 16(ph+1) .. 16(ph+1)+15
+                if (ph < 2) __syncthreads();
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) { hmid[j] = x[j] + iv[j]; x[j] = hmid[j]; }
+            q = (x[3] + kw2[0]) & pl.nm;
+#pragma unroll
+            for (int ph = 0; ph < 4; ++ph)                     // compression 2
+                pair_rounds16(x, q, pl, kw2 + 16 * ph, ph < 3 ? kw2[16 * ph + 16] : 0u);
+            if (odd) {
+                uint32_t key[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) key[j] = x[j] + hmid[j];
+                if (i < n)
+                    reinterpret_cast<uint4*>(a.keys)[k0 + i] =
+                        make_uint4(bswap(key[0]), bswap(key[1]), bswap(key[2]), bswap(key[3]));
+                put4(&sh.prev[c], key);
+            }
+            __syncthreads();                                   // end of key
+        }
+    } else {
+        // ---------------- helper ----------------
+        // producer view: lanes 0..31 own chain `lane` for the token-only work
+        const bool producer = lane < kPpChains;
+        const uint32_t rp = blockIdx.x * kPpChains + lane;
+        int64_t pt0 = 0, pk0 = 0, pn = 0;
+        if (producer && rp < a.n_req && !chain_bounds(a, rp, pt0, pk0, pn)) pn = 0;
+        if (!(producer && rp < a.n_req)) pn = 0;
+        const int32_t* tp = a.tokens + pt0;
+        // schedule view: the lane pair of chain c; odd lanes take odd message words
+        uint32_t dsel[2];
+        dsel[0] = odd ? dg[1] : dg[0];     // W4 / W5
+        dsel[1] = odd ? dg[3] : dg[2];     // W6 / W7
+        uint32_t* kw1hi_col = reinterpret_cast<uint32_t*>(&sh.kw1hi[0][c]) + (odd ? 1 : 0);
+        uint32_t tk[16], pre[16];
+        if (producer) {
+            load_tokens16(tp, 0, pn, tk);
+            load_tokens16(tp, 1, pn, pre);
+            produce_key(sh, lane, 0, tk);
+        }
+        __syncthreads();                                       // prologue
+        for (int64_t i = 0; i < nmax; ++i) {
+            const int buf = static_cast<int>(i & 1);
+            uint32_t pv[4], tw[8], v[8];
+            get4(&sh.prev[c], pv);
+            get4(&sh.w1tok[buf][0][c], tw);
+            get4(&sh.w1tok[buf][1][c], tw + 4);
+            // own words, newest first: W14 W12 .. W0 (even lane) or W15 W13 .. W1 (odd lane)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = odd ? tw[7 - 2 * k] : tw[6 - 2 * k];
+            v[4] = dsel[1];
+            v[5] = dsel[0];
+            v[6] = odd ? pv[3] : pv[2];
+            v[7] = odd ? pv[1] : pv[0];
+            pair_schedule8<8>(v, odd, kw1hi_col);
+            __syncthreads();
+            pair_schedule8<16>(v, odd, kw1hi_col);
+            __syncthreads();
+            pair_schedule8<24>(v, odd, kw1hi_col);
+            __syncthreads();
+            if (producer) {                                    // the next key's token-only data
+#pragma unroll
+                for (int q = 0; q < 16; ++q) tk[q] = pre[q];
+                load_tokens16(tp, i + 2, pn, pre);
+                produce_key(sh, lane, buf ^ 1, tk);
+            }
             __syncthreads();                                   // end of key
         }
     }
@@ -744,7 +972,10 @@ int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_o
     if (n_req == 0) return PKV_OK;
     ChainArgs a{tokens, n_tokens, tok_off, n_req, digests, block, key_off, n_keys, keys, status};
     const dim3 grid((n_req + kDeriveThreads - 1) / kDeriveThreads);
-    if (block == 16 && grid.x <= static_cast<unsigned>(compute_units())) {
+    const unsigned pp_grid = (n_req + kPpChains - 1) / kPpChains;
+    if (block == 16 && pp_grid <= static_cast<unsigned>(compute_units())) {
+        hipLaunchKernelGGL(k_derive_b16_pp, dim3(pp_grid), dim3(kPcThreads), 0, s, a);
+    } else if (block == 16 && grid.x <= static_cast<unsigned>(compute_units())) {
         hipLaunchKernelGGL(k_derive_b16_pc, grid, dim3(kPcThreads), 0, s, a);
     } else if (block == 16) {
         hipLaunchKernelGGL(k_derive_b16, grid, dim3(kDeriveThreads), 0, s, a);

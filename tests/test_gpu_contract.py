@@ -1,5 +1,5 @@
 """The contract's properties and the degenerate inputs, exercised on the HIP path (through the C ABI):
-empty and ragged batches, requests shorter than one block, the switch between the two derive
+empty and ragged batches, requests shorter than one block, the switches between the derive
 kernels, every-key-changes on a one-dimension change (Eq. 4), token-only erasure (Def. 1), the
 binding pattern (section 6.1) and storage growth (section 6.5)."""
 
@@ -78,10 +78,11 @@ def test_ragged_with_empty_requests_in_between(pkv):
     assert [k.shape[0] for k in ks] == [n // 16 for n in lens]
 
 
-@pytest.mark.parametrize("n_req", [16384, 16385])
-def test_both_derive_kernels_agree_at_the_switch(pkv, n_req):
-    """16384 requests = 256 workgroups of 64 chains (two-wavefront kernel); one more request switches to
-    the one-wavefront kernel.  Both must give the oracle's keys."""
+@pytest.mark.parametrize("n_req", [8192, 8193, 16384, 16385])
+def test_derive_kernels_agree_at_the_switches(pkv, n_req):
+    """8192 requests = 256 workgroups of 32 lane-pair chains (the last size of the lane-pair kernel);
+    8193..16384 run the two-wavefront kernel with one lane per chain; from 16385 on the
+    one-wavefront kernel.  Every kernel must give the oracle's keys."""
     rng = np.random.default_rng(n_req)
     lens = rng.integers(0, 64, size=n_req)
     off = np.zeros(n_req + 1, np.int64)
