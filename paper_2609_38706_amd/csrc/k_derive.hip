@@ -435,14 +435,18 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_b16_pp(ChainArgs a) {
             iv[q] = odd ? kInitH[q] : kInitH[4 + q];
             dgk[q] = dg[q] + kRoundK[4 + q];
         }
+        // K + W of rounds 0..3 of the next key (W0..W3 = previous key, held by the odd lane and
+        // swapped over to the even lane, the only lane whose Q uses it)
+        uint32_t kwp[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) kwp[j] = kRoundK[j];
         if (odd) sh.prev[c] = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();                                       // prologue
         for (int64_t i = 0; i < nmax; ++i) {
             const int buf = static_cast<int>(i & 1);
             uint32_t x[4], kw[16], kw2[64], hmid[4], q;
-            get4(&sh.prev[c], kw);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) { kw[j] += kRoundK[j]; kw[4 + j] = dgk[j]; }
+            for (int j = 0; j < 4; ++j) { kw[j] = kwp[j]; kw[4 + j] = dgk[j]; }
             get4(&sh.kw1tok[buf][0][c], kw + 8);
             get4(&sh.kw1tok[buf][1][c], kw + 12);
 #pragma unroll
@@ -466,10 +470,12 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_b16_pp(ChainArgs a) {
 #pragma unroll
             for (int ph = 0; ph < 4; ++ph)                     // compression 2
                 pair_rounds16(x, q, pl, kw2 + 16 * ph, ph < 3 ? kw2[16 * ph + 16] : 0u);
-            if (odd) {
-                uint32_t key[4];
+            uint32_t key[4];                                   // the key on the odd lane
 #pragma unroll
-                for (int j = 0; j < 4; ++j) key[j] = x[j] + hmid[j];
+            for (int j = 0; j < 4; ++j) key[j] = x[j] + hmid[j];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) kwp[j] = lane_swap(key[j]) + kRoundK[j];
+            if (odd) {
                 if (i < n)
                     reinterpret_cast<uint4*>(a.keys)[k0 + i] =
                         make_uint4(bswap(key[0]), bswap(key[1]), bswap(key[2]), bswap(key[3]));
