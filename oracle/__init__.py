@@ -57,6 +57,8 @@ def lib():
         L.orc_index_new.argtypes = [ctypes.c_uint64]
         L.orc_index_new.restype = P
         L.orc_index_free.argtypes = [P]
+        L.orc_index_clone.argtypes = [P]
+        L.orc_index_clone.restype = P
         L.orc_index_size.argtypes = [P]
         L.orc_index_size.restype = ctypes.c_uint64
         L.orc_index_dump.argtypes = [P, P, P]
@@ -154,9 +156,15 @@ def batch_digests(batch) -> np.ndarray:
 class Index:
     """The oracle's index: a sorted set of (key, location) pairs with a capacity."""
 
-    def __init__(self, capacity: int):
+    def __init__(self, capacity: int, _handle=None):
         self.capacity = capacity
-        self._h = lib().orc_index_new(capacity)
+        self._h = _handle if _handle is not None else lib().orc_index_new(capacity)
+
+    def clone(self) -> "Index":
+        h = lib().orc_index_clone(self._h)
+        if not h:
+            raise MemoryError("oracle index clone")
+        return Index(self.capacity, h)
 
     def __del__(self):
         if getattr(self, "_h", None):

@@ -295,6 +295,18 @@ void orc_index_free(orc_index* t) {
     if (t) { free(t->e); free(t); }
 }
 
+orc_index* orc_index_clone(const orc_index* t) {
+    orc_index* c = orc_index_new(t->capacity);
+    if (!c) return NULL;
+    if (t->size) {
+        c->e = (entry*)malloc(t->size * sizeof(entry));
+        if (!c->e) { free(c); return NULL; }
+        memcpy(c->e, t->e, t->size * sizeof(entry));
+    }
+    c->size = t->size;
+    return c;
+}
+
 uint64_t orc_index_size(const orc_index* t) { return t->size; }
 
 void orc_index_dump(const orc_index* t, uint8_t* keys, uint64_t* locs) {

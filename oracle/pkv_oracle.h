@@ -72,6 +72,8 @@ typedef struct orc_index orc_index;
 
 orc_index* orc_index_new(uint64_t capacity);
 void orc_index_free(orc_index* t);
+/* An independent copy of t (same capacity and pairs); NULL if out of memory. */
+orc_index* orc_index_clone(const orc_index* t);
 uint64_t orc_index_size(const orc_index* t);
 /* Copies the pairs out in ascending key order (byte-wise unsigned comparison). */
 void orc_index_dump(const orc_index* t, uint8_t* keys, uint64_t* locs);

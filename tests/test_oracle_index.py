@@ -147,3 +147,18 @@ def test_store_skips_keys_below_the_given_hits(seed):
     assert idx.store(keys, key_off, hits, locs) == 0
     dk, dl = idx.dump()
     assert {bytes(k): int(v) for k, v in zip(dk, dl)} == _brute_store({}, keys, key_off, hits, locs)
+
+
+def test_clone_is_an_independent_copy():
+    idx = oracle.Index(64)
+    k = np.random.default_rng(5).integers(0, 256, size=(10, 16), dtype=np.uint8)
+    ko = np.array([0, 10], np.int64)
+    assert idx.store(k[:6], np.array([0, 6], np.int64), np.zeros(1, np.int32), np.arange(6, dtype=np.uint64)) == 0
+    c = idx.clone()
+    a0, b0 = idx.dump()
+    a1, b1 = c.dump()
+    assert (a0 == a1).all() and (b0 == b1).all() and c.capacity == idx.capacity
+    assert c.store(k, ko, np.zeros(1, np.int32), np.arange(10, dtype=np.uint64) + 100) == 0
+    assert len(c) == 10 and len(idx) == 6
+    a2, b2 = idx.dump()
+    assert (a0 == a2).all() and (b0 == b2).all()
