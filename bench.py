@@ -39,6 +39,8 @@ WORKLOAD_TEXT = {
     "c3": "4096 req x 8192 tok, chunk 256, Zipf(1.1) over 512 prefixes, 16 descriptors, 512K-slot index",
     "c4": "16384 req x 4096 tok, block 16, 20 dimensions, 64M-slot index with 2^25 entries",
     "c5": "256 req x 131072 tok, block 16, groups of 4 with uniform fork points, 4M-slot index",
+    "omission": "differential omission test (Eq. 4): 512 req x 1024 tok, block 16, 20 registered dimensions, "
+                "22 bindings (complete, 20 leave-one-out, token-only) x (base + 20 one-dimension variants)",
 }
 
 
@@ -235,6 +237,52 @@ def saturation_leg(args, n_chains=131072, blocks=16, reps=5):
             "frac": round(ops / (ms * 1e-3) / INT_PEAK, 4)}
 
 
+def omission_leg(args):
+    """Key-level differential omission test: every (binding, dimension) variant of a 20-dimension
+    registry derived in one launch, base keys stored, variant keys looked up, hits summed."""
+    import torch
+    from paper_2609_38706_amd.omission import OmissionRun
+    from workloads import make_omission
+    case = make_omission()
+    run = OmissionRun(case)
+    for _ in range(args.warmup):
+        run.run()
+    torch.cuda.synchronize()
+    res = run.result()
+    expect = np.array([[0 if (names is None or d in names) else res["blocks"] for d in case.dims]
+                       for _label, names in case.bindings])
+    if not (res["collisions"] == expect).all():
+        raise RuntimeError("omission test: collision matrix differs from its closed form")
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        run.run(derive_events=evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    run.result()
+    return {"ms": (t1 - t0) * 1e3 / args.steps, "derive_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evs])),
+            "n_keys": run.n_keys, "n_req": run.db.n_req, "block": case.batch.block, "case": case,
+            "omissions": int(res["omission"].sum())}
+
+
+def omission_cpu_leg(args, case, n_keys, target_s=10.0):
+    """The oracle's omission matrix on the same case, repeated until about `target_s` seconds."""
+    from oracle.omission import omission_matrix
+    threads = args.cpu_threads or max(1, min(16, len(os.sched_getaffinity(0))))
+    total, reps = 0.0, 0
+    while total < target_s:
+        t0 = time.perf_counter()
+        omission_matrix(case, threads)
+        total += time.perf_counter() - t0
+        reps += 1
+    return {"value": round(reps * n_keys / total / 1e9, 6), "unit": "Gkeys/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} full omission tests ({len(case.bindings)} bindings x {len(case.dims)} dimensions over "
+                      f"{case.batch.n_req} requests; the oracle derives both configurations of every pair and "
+                      f"compares keys position by position, derive on {threads} threads); {total:.2f} s; rate in "
+                      f"the test's own {n_keys} keys", "seconds": round(total, 3), "steps": reps}
+
+
 def cpu_leg(args, w, target_s=10.0, max_reps=2000):
     """The oracle as it stands, on the host cores: full steps of the same workload, each on a fresh
     copy of the prepared index, repeated until about `target_s` seconds of timed CPU work."""
@@ -287,6 +335,29 @@ def main():
     torch.cuda.set_device(0)
     if args.calib_copy:
         calib_copy()
+        return
+    if args.workload == "omission":
+        log(args, "omission test")
+        g = omission_leg(args)
+        ops = g["n_keys"] * compressions_per_key(g["block"]) * OPS_PER_COMPRESSION
+        achieved = ops / (g["derive_ms"] * 1e-3)
+        cpu = None if args.no_cpu_baseline else omission_cpu_leg(args, g["case"], g["n_keys"])
+        out = {
+            "metric": "provenance-bound block keys derived+probed per second (Gkeys/s); % of roofline",
+            "value": round(g["n_keys"] / (g["ms"] * 1e-3) / 1e9, 6), "unit": "Gkeys/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(g["ms"], 4), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "u32", "data": "synthetic",
+            "config": {"workload": WORKLOAD_TEXT["omission"], "name": "omission", "requests": g["n_req"],
+                       "keys": g["n_keys"], "block": g["block"], "parallelism": "1 GPU"},
+            "kernels_ms": {"derive": round(g["derive_ms"], 4)},
+            "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 4), "peak": round(INT_PEAK / 1e12, 4),
+                         "unit": "Tops/s", "frac": round(achieved / INT_PEAK, 5), "traffic": None, "kernel": "derive",
+                         "ops_per_key": compressions_per_key(g["block"]) * OPS_PER_COMPRESSION,
+                         "chain_ceiling_frac": round(chain_ceiling_frac(g["n_req"]), 5)},
+            "cpu_baseline": cpu,
+            "omissions_reported": g["omissions"],
+        }
+        print(json.dumps(out), flush=True)
         return
     from workloads import make_workload
     log(args, "generating workload", args.workload)

@@ -159,6 +159,17 @@ int pkv_table_rollback(const pkv_table* table, const uint64_t* d_new_slots, cons
 int pkv_table_export(const pkv_table* table, uint8_t* d_keys_out, uint64_t* d_locs_out,
                      uint64_t* d_count, hipStream_t stream);
 
+/* Store-side form of the differential omission test (section 5.4, Eq. 4; section 6.4 omission
+ * detection).  The keys of base configurations are stored, the keys of configurations that differ
+ * from them in one dimension are looked up, and a key found is a key the two configurations
+ * share.  This call sums the hit lengths per group of requests:
+ *   d_sums[g] = sum of max(d_hit_blocks[r], 0) over r in [d_group_off[g], d_group_off[g+1]).
+ * d_hit_blocks: n_req int32 (as written by pkv_lookup_prefix); d_group_off: n_groups + 1 int64,
+ * non-decreasing, within [0, n_req]; d_sums: n_groups uint64.  A group whose bounds are
+ * inconsistent gets 0 and sets PKV_ELAYOUT. */
+int pkv_sum_hits(const int32_t* d_hit_blocks, uint32_t n_req, const int64_t* d_group_off, uint32_t n_groups,
+                 uint64_t* d_sums, int32_t* d_status, hipStream_t stream);
+
 /* Text describing the last non-OK return on this thread. */
 const char* pkv_last_error(void);
 

@@ -19,7 +19,7 @@ ERROR_NAMES = {0: "PKV_OK", -1: "PKV_EINVAL", -2: "PKV_EDUPDIM", -3: "PKV_ERESER
 
 EXPORTED = ["pkv_descriptor_encode", "pkv_descriptor_digest", "pkv_digest_batch", "pkv_key_offsets",
             "pkv_derive_keys", "pkv_table_init", "pkv_lookup_prefix", "pkv_store", "pkv_table_rollback",
-            "pkv_table_export", "pkv_last_error", "pkv_version"]
+            "pkv_table_export", "pkv_sum_hits", "pkv_last_error", "pkv_version"]
 
 
 class PkvError(RuntimeError):
@@ -59,6 +59,7 @@ def lib() -> ctypes.CDLL:
             "pkv_store": [P, P, P, U32, U64, P, P, P, P, P, P],
             "pkv_table_rollback": [P, P, P, U64, P],
             "pkv_table_export": [P, P, P, P, P],
+            "pkv_sum_hits": [P, U32, P, U32, P, P, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -200,6 +201,13 @@ def pkv_table_export(table: Table, keys_out, locs_out, count, stream=None):
     t = table.struct()
     _check(lib().pkv_table_export(ctypes.byref(t), _ptr(keys_out, torch.uint8), _ptr(locs_out, torch.int64),
                                   _ptr(count, torch.int64), _stream(stream)))
+
+
+def pkv_sum_hits(hits, group_off, sums, status, stream=None):
+    import torch
+    _check(lib().pkv_sum_hits(_ptr(hits, torch.int32), hits.numel(), _ptr(group_off, torch.int64),
+                              group_off.numel() - 1, _ptr(sums, torch.int64), _ptr(status, torch.int32),
+                              _stream(stream)))
 
 
 def version() -> str:

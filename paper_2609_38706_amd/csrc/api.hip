@@ -273,4 +273,12 @@ int pkv_table_export(const pkv_table* table, uint8_t* d_keys_out, uint64_t* d_lo
     return launch_export(table->keys, table->locs, table->capacity, d_keys_out, d_locs_out, d_count, stream);
 }
 
+int pkv_sum_hits(const int32_t* d_hit_blocks, uint32_t n_req, const int64_t* d_group_off, uint32_t n_groups,
+                 uint64_t* d_sums, int32_t* d_status, hipStream_t stream) {
+    if (n_groups == 0) return PKV_OK;
+    if ((!d_hit_blocks && n_req) || !d_group_off || !d_sums || !d_status)
+        return set_error(PKV_EINVAL, "pkv_sum_hits: null argument");
+    return launch_sum_hits(d_hit_blocks, n_req, d_group_off, n_groups, d_sums, d_status, stream);
+}
+
 }  // extern "C"

@@ -402,6 +402,36 @@ __global__ __launch_bounds__(256) void k_export(const uint4* tkeys, const uint64
     }
 }
 
+// ---- hit sums per request group (omission test) -------------------------------------------------
+// One workgroup per group: sums[g] = sum of max(hits[r], 0) over r in [group_off[g], group_off[g+1]).
+constexpr uint32_t kSumThreads = 256;
+
+__global__ __launch_bounds__(kSumThreads) void k_sum_hits(const int32_t* hits, uint32_t n_req, const int64_t* group_off,
+                                                          uint64_t* sums, int32_t* status) {
+    __shared__ uint64_t part[kSumThreads / 64];
+    const uint32_t g = blockIdx.x;
+    const int64_t r0 = group_off[g], r1 = group_off[g + 1];
+    const bool ok = r0 >= 0 && r1 >= r0 && r1 <= static_cast<int64_t>(n_req);
+    uint64_t acc = 0;
+    if (ok) {
+        for (int64_t r = r0 + threadIdx.x; r < r1; r += kSumThreads) {
+            const int32_t h = hits[r];
+            acc += h > 0 ? static_cast<uint64_t>(h) : 0u;
+        }
+    }
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) acc += __shfl_xor(acc, d, 64);
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t total = 0;
+#pragma unroll
+        for (uint32_t w = 0; w < kSumThreads / 64; ++w) total += part[w];
+        sums[g] = ok ? total : 0u;
+        if (!ok) report(status, PKV_ELAYOUT);
+    }
+}
+
 unsigned grid_for(uint64_t items, unsigned threads, unsigned cap_blocks) {
     uint64_t b = (items + threads - 1) / threads;
     if (b < 1) b = 1;
@@ -410,6 +440,13 @@ unsigned grid_for(uint64_t items, unsigned threads, unsigned cap_blocks) {
 }
 
 }  // namespace
+
+int launch_sum_hits(const int32_t* hits, uint32_t n_req, const int64_t* group_off, uint32_t n_groups, uint64_t* sums,
+                    int32_t* status, hipStream_t s) {
+    if (n_groups == 0) return PKV_OK;
+    hipLaunchKernelGGL(k_sum_hits, dim3(n_groups), dim3(kSumThreads), 0, s, hits, n_req, group_off, sums, status);
+    return check_launch("pkv_sum_hits");
+}
 
 int launch_table_init(uint8_t* keys, uint64_t* locs, uint64_t capacity, hipStream_t s) {
     hipLaunchKernelGGL(k_init, dim3(grid_for(capacity + 1, 256, 16384)), dim3(256), 0, s,

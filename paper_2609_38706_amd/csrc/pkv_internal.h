@@ -114,6 +114,8 @@ int launch_store(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint8
                  uint64_t* new_slots, uint64_t* n_new, int32_t* status, hipStream_t s);
 int launch_rollback(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint64_t* slots,
                     const uint64_t* n_slots, uint64_t max_slots, hipStream_t s);
+int launch_sum_hits(const int32_t* hits, uint32_t n_req, const int64_t* group_off, uint32_t n_groups, uint64_t* sums,
+                    int32_t* status, hipStream_t s);
 int launch_export(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity, uint8_t* out_keys,
                   uint64_t* out_locs, uint64_t* count, hipStream_t s);
 

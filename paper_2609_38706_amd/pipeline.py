@@ -22,7 +22,12 @@ class DeviceBatch:
         self.block = int(block)
         self.n_req = int(tok_off.shape[0] - 1)
         self.device = device
-        self.tokens = torch.from_numpy(np.ascontiguousarray(tokens, dtype=np.int32)).to(device)
+        if isinstance(tokens, torch.Tensor):             # already on the device: used as is
+            if tokens.dtype != torch.int32 or not tokens.is_contiguous() or not tokens.is_cuda:
+                raise ValueError("device tokens must be a contiguous int32 GPU tensor")
+            self.tokens = tokens
+        else:
+            self.tokens = torch.from_numpy(np.ascontiguousarray(tokens, dtype=np.int32)).to(device)
         if self.tokens.numel() == 0:
             self.tokens = torch.zeros(1, dtype=torch.int32, device=device)[:0]
         self.tok_off = torch.from_numpy(np.ascontiguousarray(tok_off, dtype=np.int64)).to(device)

@@ -13,4 +13,8 @@ from .recipes import (  # noqa: F401
     make_workload,
     locations,
     WORKLOADS,
+    OmissionCase,
+    OMISSION_CASES,
+    make_omission,
+    make_omission_tiny,
 )

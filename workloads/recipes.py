@@ -22,7 +22,8 @@ import numpy as np
 
 CORE_NAMES = (b"model_id", b"adapter_id", b"weight_dtype", b"weight_version", b"kv_format", b"salt")
 
-SEEDS = {"tiny": 0x5EED0001, "c2": 0x5EED0002, "c3": 0x5EED0003, "c4": 0x5EED0004, "c5": 0x5EED0005}
+SEEDS = {"tiny": 0x5EED0001, "c2": 0x5EED0002, "c3": 0x5EED0003, "c4": 0x5EED0004, "c5": 0x5EED0005,
+         "omission": 0x5EED0007, "omission-tiny": 0x5EED0008}
 
 TAG_STEP, TAG_FILL, TAG_WARMUP = 0, 1, 2
 
@@ -358,6 +359,82 @@ def make_c5(seed=SEEDS["c5"]) -> Workload:
 
 
 WORKLOADS = {"tiny": make_tiny, "c2": make_c2, "c3": make_c3, "c4": make_c4, "c5": make_c5}
+
+
+# ---- differential omission test inputs (section 5.4, Eq. 4) -------------------------------------
+
+@dataclass
+class OmissionCase:
+    """Inputs of one differential omission test: fixed token sequences x, base configurations c,
+    one replacement value v' per registered dimension, the declared effect of varying each
+    dimension, and the key bindings to test.
+
+    ``bindings`` is a list of ``(label, names)``: ``names`` is the set of dimension names the key
+    binds (``None`` = every field of the descriptor, an empty set = a token-only key)."""
+    batch: Batch                # tokens, request offsets, block, base descriptors, desc_idx
+    dims: list                  # registered dimension names, in report order
+    variants: dict              # name -> replacement value v' (differs from every base value)
+    changes: dict               # name -> True if varying it changes KV state or sharing permission
+    bindings: list              # [(label, frozenset of names or None)]
+    name: str = "omission"
+
+
+def make_omission(seed=SEEDS["omission"], n_req=512, length=1024, block=16, n_base=64, n_extra=14,
+                  name="omission") -> OmissionCase:
+    """A registry of 6 core + ``n_extra`` further dimensions (8-byte values), ``n_base`` base
+    descriptors over it, ``n_req`` random token sequences of ``length`` tokens.  Bindings: the
+    complete registry, each leave-one-dimension-out projection, and the token-only key.  Every
+    dimension is declared to change state or sharing permission (the salt changes permission
+    only; the others change the computed state)."""
+    g_desc, g_ord, g_tok, g_var = _streams(seed, 4)
+    extras = [b"x%02d" % i for i in range(n_extra)]
+    dims = list(CORE_NAMES) + extras
+    dtypes = [b"bfloat16", b"float16", b"float8_e4m3fn"]
+    kv = [b"bfloat16", b"fp8_e4m3"]
+
+    def base_desc():
+        f = [(b"model_id", b"model-" + g_desc.bytes(3).hex().encode()),
+             (b"adapter_id", b"adapter-" + g_desc.bytes(4).hex().encode()),
+             (b"weight_dtype", dtypes[int(g_desc.integers(len(dtypes)))]),
+             (b"weight_version", _u64(int(g_desc.integers(1, 1 << 20)))),
+             (b"kv_format", kv[int(g_desc.integers(len(kv)))]),
+             (b"salt", g_desc.bytes(8))]
+        f += [(x, g_desc.bytes(8)) for x in extras]
+        return f
+
+    base = [base_desc() for _ in range(n_base)]
+    variants = {}
+    for d in dims:
+        taken = {v for desc in base for n, v in desc if n == d}
+        while True:
+            v = b"variant-" + g_var.bytes(8)
+            if v not in taken:
+                variants[d] = v
+                break
+    didx = g_tok.integers(0, n_base, size=n_req).astype(np.int32)
+    tok = g_tok.integers(0, 128256, size=n_req * length, dtype=np.int32)
+    batch = Batch(tok, np.arange(n_req + 1, dtype=np.int64) * length, block,
+                  [_shuffled(d, g_ord) for d in base], didx, TAG_STEP)
+    bindings = [("complete", None)]
+    bindings += [("without " + d.decode(), frozenset(x for x in dims if x != d)) for d in dims]
+    bindings += [("token-only", frozenset())]
+    return OmissionCase(batch, dims, variants, {d: True for d in dims}, bindings, name)
+
+
+def make_omission_tiny(seed=SEEDS["omission-tiny"]) -> OmissionCase:
+    """Small case for parity tests: 12 requests of 100..200 tokens (ragged tails), 2 extras."""
+    case = make_omission(seed, n_req=12, length=160, n_base=5, n_extra=2, name="omission-tiny")
+    g = np.random.default_rng(seed)
+    lens = g.integers(100, 201, size=12)
+    toks = [case.batch.tokens[r * 160:(r + 1) * 160] for r in range(12)]
+    toks = [np.concatenate([t, g.integers(0, 128256, size=max(0, n - 160), dtype=np.int32)])[:n]
+            for t, n in zip(toks, lens)]
+    t, o = _ragged(toks)
+    case.batch = Batch(t, o, 16, case.batch.descs, case.batch.desc_idx, TAG_STEP)
+    return case
+
+
+OMISSION_CASES = {"omission": make_omission, "omission-tiny": make_omission_tiny}
 
 
 def make_workload(name: str, **kw) -> Workload:
