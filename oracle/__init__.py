@@ -64,6 +64,11 @@ def lib():
         L.orc_index_dump.argtypes = [P, P, P]
         L.orc_lookup.argtypes = [P, P, P, ctypes.c_uint32, P]
         L.orc_store.argtypes = [P, P, P, ctypes.c_uint32, P, P]
+        L.orc_index_dump_epochs.argtypes = [P, P]
+        L.orc_lookup_touch.argtypes = [P, P, P, ctypes.c_uint32, P, ctypes.c_uint32]
+        L.orc_store_touch.argtypes = [P, P, P, ctypes.c_uint32, P, P, ctypes.c_uint32]
+        L.orc_evict.argtypes = [P, ctypes.c_uint64]
+        L.orc_evict.restype = ctypes.c_uint64
         _lib = L
     return _lib
 
@@ -180,6 +185,30 @@ class Index:
         locs = np.zeros(max(1, n), np.uint64)
         lib().orc_index_dump(self._h, _ptr(keys), _ptr(locs))
         return keys[:n], locs[:n]
+
+    def dump_epochs(self) -> np.ndarray:
+        n = len(self)
+        ep = np.zeros(max(1, n), np.uint32)
+        lib().orc_index_dump_epochs(self._h, _ptr(ep))
+        return ep[:n]
+
+    def lookup_touch(self, keys, key_off, epoch: int) -> np.ndarray:
+        keys = np.ascontiguousarray(keys, dtype=np.uint8)
+        key_off = np.ascontiguousarray(key_off, dtype=np.int64)
+        hits = np.zeros(max(1, key_off.shape[0] - 1), np.int32)
+        lib().orc_lookup_touch(self._h, _ptr(keys), _ptr(key_off), key_off.shape[0] - 1, _ptr(hits), epoch)
+        return hits[: key_off.shape[0] - 1]
+
+    def store_touch(self, keys, key_off, hits, locs, epoch: int) -> int:
+        keys = np.ascontiguousarray(keys, dtype=np.uint8)
+        key_off = np.ascontiguousarray(key_off, dtype=np.int64)
+        hits = np.ascontiguousarray(hits, dtype=np.int32)
+        locs = np.ascontiguousarray(locs, dtype=np.uint64)
+        return int(lib().orc_store_touch(self._h, _ptr(keys), _ptr(key_off), key_off.shape[0] - 1, _ptr(hits),
+                                         _ptr(locs), epoch))
+
+    def evict(self, budget: int) -> int:
+        return int(lib().orc_evict(self._h, budget))
 
     def lookup(self, keys, key_off) -> np.ndarray:
         keys = np.ascontiguousarray(keys, dtype=np.uint8)

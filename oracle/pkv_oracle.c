@@ -274,7 +274,7 @@ int orc_derive(const int32_t* tokens, const int64_t* tok_off, uint32_t n_req,
  * The index as a plain sorted set of (key, location) pairs.
  * ------------------------------------------------------------------------------------------ */
 
-typedef struct { uint8_t key[16]; uint64_t loc; } entry;
+typedef struct { uint8_t key[16]; uint64_t loc; uint32_t epoch; } entry;
 
 struct orc_index { uint64_t capacity, size; entry* e; };
 
@@ -316,16 +316,23 @@ void orc_index_dump(const orc_index* t, uint8_t* keys, uint64_t* locs) {
     }
 }
 
-static int contains(const orc_index* t, const uint8_t key[16]) {
+void orc_index_dump_epochs(const orc_index* t, uint32_t* epochs) {
+    for (uint64_t i = 0; i < t->size; ++i) epochs[i] = t->e[i].epoch;
+}
+
+/* Position of key in the sorted entries, or -1. */
+static int64_t find(const orc_index* t, const uint8_t key[16]) {
     uint64_t lo = 0, hi = t->size;              /* search [lo, hi) */
     while (lo < hi) {
         uint64_t mid = lo + (hi - lo) / 2;
         int c = memcmp(t->e[mid].key, key, 16);
-        if (c == 0) return 1;
+        if (c == 0) return (int64_t)mid;
         if (c < 0) lo = mid + 1; else hi = mid;
     }
-    return 0;
+    return -1;
 }
+
+static int contains(const orc_index* t, const uint8_t key[16]) { return find(t, key) >= 0; }
 
 int orc_lookup(const orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
                int32_t* hits) {
@@ -338,16 +345,27 @@ int orc_lookup(const orc_index* t, const uint8_t* keys, const int64_t* key_off, 
     return ORC_OK;
 }
 
-#define ORC_LOC_LIMIT ((uint64_t)1 << 62)
-
-static int all_ff(const uint8_t key[16]) {
-    for (int i = 0; i < 16; ++i)
-        if (key[i] != 0xFF) return 0;
-    return 1;
+int orc_lookup_touch(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
+                     int32_t* hits, uint32_t epoch) {
+    orc_lookup(t, keys, key_off, n_req, hits);
+    for (uint32_t r = 0; r < n_req; ++r)
+        for (int64_t j = 0; j < hits[r]; ++j) t->e[find(t, keys + 16 * (key_off[r] + j))].epoch = epoch;
+    return ORC_OK;
 }
 
-int orc_store(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
-              const int32_t* hits, const uint64_t* locs) {
+#define ORC_LOC_LIMIT ((uint64_t)1 << 62)
+
+/* The two byte patterns an index reserves to mark free key slots: all 0xFF (empty) and all 0xFF
+ * but a last byte of 0xFE (a removed entry).  Keys equal to either pattern have reserved places
+ * of their own and do not count against the capacity. */
+static int reserved_key(const uint8_t key[16]) {
+    for (int i = 0; i < 15; ++i)
+        if (key[i] != 0xFF) return 0;
+    return key[15] == 0xFF || key[15] == 0xFE;
+}
+
+static int store_impl(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
+                      const int32_t* hits, const uint64_t* locs, int touch, uint32_t epoch) {
     /* S = every (k_{r,j}, loc_{r,j}) with j >= h_r */
     uint64_t ns = 0;
     for (uint32_t r = 0; r < n_req; ++r) {
@@ -365,6 +383,7 @@ int orc_store(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_
             if (locs[idx] >= ORC_LOC_LIMIT) { free(s); return ORC_ERESERVED; }
             memcpy(s[k].key, keys + 16 * idx, 16);
             s[k].loc = locs[idx];
+            s[k].epoch = touch ? epoch : 0;
             ++k;
         }
     }
@@ -376,12 +395,21 @@ int orc_store(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_
         if (contains(t, s[i].key)) continue;
         s[n_new++] = s[i];                       /* compact the new keys in place, still sorted */
     }
-    /* Capacity counts ordinary keys; the one key whose 16 bytes are all 0xFF has a reserved
-     * place of its own (that byte pattern marks an empty slot of the index). */
+    /* Capacity counts ordinary keys (see reserved_key). */
     uint64_t ordinary = 0;
-    for (uint64_t i = 0; i < t->size; ++i) ordinary += !all_ff(t->e[i].key);
-    for (uint64_t i = 0; i < n_new; ++i) ordinary += !all_ff(s[i].key);
+    for (uint64_t i = 0; i < t->size; ++i) ordinary += !reserved_key(t->e[i].key);
+    for (uint64_t i = 0; i < n_new; ++i) ordinary += !reserved_key(s[i].key);
     if (ordinary > t->capacity) { free(s); return ORC_EFULL; }
+    /* a touching store refreshes the epoch of every candidate key already present */
+    if (touch) {
+        for (uint32_t r = 0; r < n_req; ++r) {
+            int64_t n = key_off[r + 1] - key_off[r];
+            for (int64_t j = hits[r] < 0 ? 0 : hits[r]; j < n; ++j) {
+                int64_t p = find(t, keys + 16 * (key_off[r] + j));
+                if (p >= 0) t->e[p].epoch = epoch;
+            }
+        }
+    }
     /* merge the two sorted runs */
     entry* m = (entry*)malloc(sizeof(entry) * ((t->size + n_new) ? (t->size + n_new) : 1));
     if (!m) { free(s); return ORC_EINVAL; }
@@ -395,4 +423,35 @@ int orc_store(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_
     t->size = o;
     free(s);
     return ORC_OK;
+}
+
+int orc_store(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
+              const int32_t* hits, const uint64_t* locs) {
+    return store_impl(t, keys, key_off, n_req, hits, locs, 0, 0);
+}
+
+int orc_store_touch(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
+                    const int32_t* hits, const uint64_t* locs, uint32_t epoch) {
+    return store_impl(t, keys, key_off, n_req, hits, locs, 1, epoch);
+}
+
+static int epoch_desc(const void* a, const void* b) {
+    uint32_t x = *(const uint32_t*)a, y = *(const uint32_t*)b;
+    return (x < y) - (x > y);
+}
+
+uint64_t orc_evict(orc_index* t, uint64_t budget) {
+    if (t->size <= budget) return 0;
+    /* E* = smallest E with #{epoch >= E} <= budget = 1 + the (budget+1)-th largest epoch */
+    uint32_t* ep = (uint32_t*)malloc(sizeof(uint32_t) * t->size);
+    for (uint64_t i = 0; i < t->size; ++i) ep[i] = t->e[i].epoch;
+    qsort(ep, t->size, sizeof(uint32_t), epoch_desc);
+    uint64_t cut = (uint64_t)ep[budget] + 1;
+    free(ep);
+    uint64_t o = 0;
+    for (uint64_t i = 0; i < t->size; ++i)
+        if ((uint64_t)t->e[i].epoch >= cut) t->e[o++] = t->e[i];
+    uint64_t evicted = t->size - o;
+    t->size = o;
+    return evicted;
 }

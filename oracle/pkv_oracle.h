@@ -77,14 +77,28 @@ orc_index* orc_index_clone(const orc_index* t);
 uint64_t orc_index_size(const orc_index* t);
 /* Copies the pairs out in ascending key order (byte-wise unsigned comparison). */
 void orc_index_dump(const orc_index* t, uint8_t* keys, uint64_t* locs);
+/* The epochs of the pairs, in the same order. */
+void orc_index_dump_epochs(const orc_index* t, uint32_t* epochs);
 
 int orc_lookup(const orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
                int32_t* hits);
 
 /* Inserts every key k_{r,j} with j >= hits[r] (0-based) that the index lacks.  On ORC_EFULL
- * or ORC_ERESERVED the index is left unchanged. */
+ * or ORC_ERESERVED the index is left unchanged.  Capacity counts keys other than the two
+ * reserved byte patterns (all 0xFF; all 0xFF with a last byte 0xFE). */
 int orc_store(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
               const int32_t* hits, const uint64_t* locs);
+
+/* Fixed-budget tier (section 6.5).  Every pair carries the epoch of its last use.  The touching
+ * lookup sets the epoch of every hit key to `epoch`; the touching store inserts like orc_store
+ * with new pairs at `epoch` and sets the epoch of every candidate key already present. */
+int orc_lookup_touch(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
+                     int32_t* hits, uint32_t epoch);
+int orc_store_touch(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
+                    const int32_t* hits, const uint64_t* locs, uint32_t epoch);
+/* Generational eviction to a budget: with E* the smallest epoch such that at most `budget`
+ * pairs have epoch >= E*, removes every pair older than E*.  Returns the number removed. */
+uint64_t orc_evict(orc_index* t, uint64_t budget);
 
 #ifdef __cplusplus
 }

@@ -13,7 +13,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SOURCE = os.path.join(ROOT, "oracle", "pkv_oracle.c")
 PINS = ["tests/test_oracle_sha256.py", "tests/test_oracle_encoding.py", "tests/test_oracle_chain.py",
-        "tests/test_oracle_index.py", "tests/test_contract_oracle.py"]
+        "tests/test_oracle_index.py", "tests/test_contract_oracle.py", "tests/test_oracle_budget.py"]
 
 # (name, [(old, new), ...]); every `old` must occur in the source.
 MUTANTS = [
@@ -53,6 +53,12 @@ MUTANTS = [
     ("present keys inserted again", [("if (contains(t, s[i].key)) continue;", "")]),
     ("capacity off by one", [("if (ordinary > t->capacity)", "if (ordinary >= t->capacity)")]),
     ("hit lengths ignored by the store", [("hits[r] < 0 ? 0 : hits[r]", "0")]),
+    ("eviction cut one generation late", [("uint64_t cut = (uint64_t)ep[budget] + 1;",
+                                           "uint64_t cut = (uint64_t)ep[budget];")]),
+    ("touching store leaves present keys", [("if (p >= 0) t->e[p].epoch = epoch;", "if (p >= 0) (void)0;")]),
+    ("touching lookup skips the first hit", [("for (int64_t j = 0; j < hits[r]; ++j) t->e[find",
+                                              "for (int64_t j = 1; j < hits[r]; ++j) t->e[find")]),
+    ("removed-entry pattern counted", [("return key[15] == 0xFF || key[15] == 0xFE;", "return key[15] == 0xFF;")]),
 ]
 
 
