@@ -37,6 +37,11 @@
  *   - Locations are caller-defined 64-bit values below PKV_LOC_LIMIT (the top two bits are
  *     reserved for the insert protocol).
  *   - Device errors leave the index contents unspecified.
+ *   - Index layout (pkv_table): keys = capacity x 16 bytes (64-byte aligned, capacity a power of
+ *     two >= 4), locs = capacity + 2 uint64 words.  Two key byte patterns are reserved to mark free
+ *     key slots (all 0xFF: never used; all 0xFF with a last byte 0xFE: removed by eviction); a key
+ *     equal to either keeps its location in locs[capacity] / locs[capacity + 1] and does not count
+ *     against the capacity.  A fixed-budget tier adds an epochs array of capacity + 2 uint32.
  */
 #ifndef PKV_H
 #define PKV_H
@@ -76,8 +81,8 @@ typedef struct {
 /* The shared-tier index (section 2.1 shared KV-cache tier): open addressing over 4-slot
  * buckets of 64 bytes, struct-of-arrays in HBM.
  *   keys     : capacity x 16 bytes, 64-byte aligned.
- *   locs     : capacity + 1 words (the extra word serves the one key that equals the
- *              all-0xFF empty marker).
+ *   locs     : capacity + 2 words (the two extra words serve the keys that equal the two
+ *              reserved patterns: all 0xFF, and all 0xFF with a last byte 0xFE).
  *   capacity : a power of two, >= 4.
  * The struct itself is host memory; the arrays are device memory owned by the caller. */
 typedef struct {
@@ -141,7 +146,8 @@ int pkv_lookup_prefix(const pkv_table* table, const uint8_t* d_keys, const int64
  * d_locs: n_keys uint64 (< PKV_LOC_LIMIT, else PKV_ERESERVED).
  * d_n_new: one uint64 counter that the call increments by the number of new entries; the
  * caller zeroes it.  d_new_slots: NULL, or room for n_keys uint64: the slot index of each new
- * entry is appended at d_new_slots[old *d_n_new ...] (the all-0xFF key's slot is `capacity`).
+ * entry is appended at d_new_slots[old *d_n_new ...] (a reserved key's slot is `capacity` or
+ * `capacity + 1`; bit 63 marks a slot that was removed by eviction before).
  * No free slot for a new key sets PKV_EFULL. */
 int pkv_store(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off,
               uint32_t n_req, uint64_t n_keys, const int32_t* d_hit_blocks, const uint64_t* d_locs,
@@ -154,10 +160,35 @@ int pkv_table_rollback(const pkv_table* table, const uint64_t* d_new_slots, cons
                        uint64_t max_slots, hipStream_t stream);
 
 /* Copies every occupied (key, location) pair out, in no particular order.  d_keys_out: room for
- * capacity + 1 keys; d_locs_out: capacity + 1 words; *d_count receives the number of pairs (the
+ * capacity + 2 keys; d_locs_out: capacity + 2 words; *d_count receives the number of pairs (the
  * call zeroes it first). */
 int pkv_table_export(const pkv_table* table, uint8_t* d_keys_out, uint64_t* d_locs_out,
                      uint64_t* d_count, hipStream_t stream);
+
+/* Fixed-budget shared tier (section 6.5, eviction under a fixed budget).  Every entry carries
+ * the epoch of its last use in d_epochs (capacity + 2 uint32, owned by the caller; only entries
+ * written through the touching calls have meaningful epochs).
+ *
+ * pkv_lookup_prefix_touch: pkv_lookup_prefix, and every hit key's epoch becomes `epoch`.
+ * pkv_store_touch: pkv_store, and every candidate key (j >= hit length), new or already present,
+ * gets epoch `epoch`; present entries keep their locations.  Slots removed by eviction are reused;
+ * the slot log marks such a slot with bit 63 so that pkv_table_rollback restores it as removed. */
+int pkv_lookup_prefix_touch(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off,
+                            uint32_t n_req, uint64_t n_keys, uint32_t* d_epochs, uint32_t epoch,
+                            int32_t* d_hit_blocks, int32_t* d_status, hipStream_t stream);
+int pkv_store_touch(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off,
+                    uint32_t n_req, uint64_t n_keys, const int32_t* d_hit_blocks, const uint64_t* d_locs,
+                    uint64_t* d_new_slots, uint64_t* d_n_new, uint32_t* d_epochs, uint32_t epoch,
+                    int32_t* d_status, hipStream_t stream);
+
+/* Generational eviction to a budget: with E* the smallest epoch such that at most `budget`
+ * entries were last used at or after E*, every entry used before E* is removed (probe paths
+ * stay intact: its slot is marked removed, not empty).  d_work: PKV_EVICT_WORK_BYTES of device
+ * memory (8-byte aligned, contents overwritten); *d_n_evicted receives the number removed.  The
+ * index must not be accessed by other calls while this runs (stream order suffices). */
+#define PKV_EVICT_WORK_BYTES ((size_t)(2 * 65536 * 4 + 64))
+int pkv_table_evict(const pkv_table* table, const uint32_t* d_epochs, uint64_t budget, void* d_work,
+                    uint64_t* d_n_evicted, hipStream_t stream);
 
 /* Store-side form of the differential omission test (section 5.4, Eq. 4; section 6.4 omission
  * detection).  The keys of base configurations are stored, the keys of configurations that differ

@@ -19,7 +19,10 @@ ERROR_NAMES = {0: "PKV_OK", -1: "PKV_EINVAL", -2: "PKV_EDUPDIM", -3: "PKV_ERESER
 
 EXPORTED = ["pkv_descriptor_encode", "pkv_descriptor_digest", "pkv_digest_batch", "pkv_key_offsets",
             "pkv_derive_keys", "pkv_table_init", "pkv_lookup_prefix", "pkv_store", "pkv_table_rollback",
-            "pkv_table_export", "pkv_sum_hits", "pkv_last_error", "pkv_version"]
+            "pkv_table_export", "pkv_sum_hits", "pkv_lookup_prefix_touch", "pkv_store_touch",
+            "pkv_table_evict", "pkv_last_error", "pkv_version"]
+
+EVICT_WORK_BYTES = 2 * 65536 * 4 + 64   # PKV_EVICT_WORK_BYTES
 
 
 class PkvError(RuntimeError):
@@ -60,6 +63,9 @@ def lib() -> ctypes.CDLL:
             "pkv_table_rollback": [P, P, P, U64, P],
             "pkv_table_export": [P, P, P, P, P],
             "pkv_sum_hits": [P, U32, P, U32, P, P, P],
+            "pkv_lookup_prefix_touch": [P, P, P, U32, U64, P, U32, P, P, P],
+            "pkv_store_touch": [P, P, P, U32, U64, P, P, P, P, P, U32, P, P],
+            "pkv_table_evict": [P, P, U64, P, P, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -147,15 +153,19 @@ def pkv_derive_keys(tokens, tok_off, digests, block, key_off, keys, status, stre
 
 
 class Table:
-    """Device arrays of one index: ``keys`` uint8 [capacity, 16], ``locs`` int64 [capacity + 1]."""
+    """Device arrays of one index: ``keys`` uint8 [capacity, 16], ``locs`` int64 [capacity + 2];
+    with ``epochs=True`` also ``epochs`` int32 [capacity + 2] (the fixed-budget tier) and the
+    eviction work area."""
 
-    def __init__(self, capacity: int, device="cuda", init=True, stream=None):
+    def __init__(self, capacity: int, device="cuda", init=True, stream=None, epochs=False):
         import torch
         if capacity < 4 or capacity & (capacity - 1):
             raise ValueError("capacity must be a power of two >= 4")
         self.capacity = capacity
         self.keys = torch.empty((capacity, 16), dtype=torch.uint8, device=device)
-        self.locs = torch.empty(capacity + 1, dtype=torch.int64, device=device)
+        self.locs = torch.empty(capacity + 2, dtype=torch.int64, device=device)
+        self.epochs = torch.zeros(capacity + 2, dtype=torch.int32, device=device) if epochs else None
+        self.work = torch.empty(EVICT_WORK_BYTES // 8, dtype=torch.int64, device=device) if epochs else None
         if init:
             pkv_table_init(self, stream)
 
@@ -165,6 +175,8 @@ class Table:
     def copy_from(self, other: "Table"):
         self.keys.copy_(other.keys)
         self.locs.copy_(other.locs)
+        if self.epochs is not None and other.epochs is not None:
+            self.epochs.copy_(other.epochs)
 
 
 def pkv_table_init(table: Table, stream=None):
@@ -201,6 +213,32 @@ def pkv_table_export(table: Table, keys_out, locs_out, count, stream=None):
     t = table.struct()
     _check(lib().pkv_table_export(ctypes.byref(t), _ptr(keys_out, torch.uint8), _ptr(locs_out, torch.int64),
                                   _ptr(count, torch.int64), _stream(stream)))
+
+
+def pkv_lookup_prefix_touch(table: Table, keys, key_off, epoch: int, hits, status, stream=None):
+    import torch
+    t = table.struct()
+    _check(lib().pkv_lookup_prefix_touch(ctypes.byref(t), _ptr(keys, torch.uint8), _ptr(key_off, torch.int64),
+                                         key_off.numel() - 1, keys.numel() // 16, _ptr(table.epochs, torch.int32),
+                                         epoch, _ptr(hits, torch.int32), _ptr(status, torch.int32), _stream(stream)))
+
+
+def pkv_store_touch(table: Table, keys, key_off, hits, locs, n_new, status, epoch: int, new_slots=None,
+                    stream=None):
+    import torch
+    t = table.struct()
+    _check(lib().pkv_store_touch(ctypes.byref(t), _ptr(keys, torch.uint8), _ptr(key_off, torch.int64),
+                                 key_off.numel() - 1, keys.numel() // 16, _ptr(hits, torch.int32),
+                                 _ptr(locs, torch.int64), _ptr(new_slots, torch.int64), _ptr(n_new, torch.int64),
+                                 _ptr(table.epochs, torch.int32), epoch, _ptr(status, torch.int32),
+                                 _stream(stream)))
+
+
+def pkv_table_evict(table: Table, budget: int, n_evicted, stream=None):
+    import torch
+    t = table.struct()
+    _check(lib().pkv_table_evict(ctypes.byref(t), _ptr(table.epochs, torch.int32), budget,
+                                 _ptr(table.work, torch.int64), _ptr(n_evicted, torch.int64), _stream(stream)))
 
 
 def pkv_sum_hits(hits, group_off, sums, status, stream=None):

@@ -240,7 +240,20 @@ int pkv_lookup_prefix(const pkv_table* table, const uint8_t* d_keys, const int64
         return set_error(PKV_EINVAL, "pkv_lookup_prefix: null argument");
     if (!aligned(d_keys, 16)) return set_error(PKV_EINVAL, "pkv_lookup_prefix: keys not 16-byte aligned");
     return launch_lookup(table->keys, table->locs, table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
-                         d_status, stream);
+                         nullptr, 0, d_status, stream);
+}
+
+int pkv_lookup_prefix_touch(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off, uint32_t n_req,
+                            uint64_t n_keys, uint32_t* d_epochs, uint32_t epoch, int32_t* d_hit_blocks,
+                            int32_t* d_status, hipStream_t stream) {
+    int rc = check_table(table, "pkv_lookup_prefix_touch");
+    if (rc) return rc;
+    if (n_req == 0) return PKV_OK;
+    if ((!d_keys && n_keys) || !d_key_off || !d_hit_blocks || !d_status || !d_epochs)
+        return set_error(PKV_EINVAL, "pkv_lookup_prefix_touch: null argument");
+    if (!aligned(d_keys, 16)) return set_error(PKV_EINVAL, "pkv_lookup_prefix_touch: keys not 16-byte aligned");
+    return launch_lookup(table->keys, table->locs, table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
+                         d_epochs, epoch, d_status, stream);
 }
 
 int pkv_store(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off, uint32_t n_req,
@@ -253,7 +266,31 @@ int pkv_store(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_ke
         return set_error(PKV_EINVAL, "pkv_store: null argument");
     if (!aligned(d_keys, 16)) return set_error(PKV_EINVAL, "pkv_store: keys not 16-byte aligned");
     return launch_store(table->keys, table->locs, table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
-                        d_locs, d_new_slots, d_n_new, d_status, stream);
+                        d_locs, d_new_slots, d_n_new, nullptr, 0, d_status, stream);
+}
+
+int pkv_store_touch(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off, uint32_t n_req,
+                    uint64_t n_keys, const int32_t* d_hit_blocks, const uint64_t* d_locs, uint64_t* d_new_slots,
+                    uint64_t* d_n_new, uint32_t* d_epochs, uint32_t epoch, int32_t* d_status, hipStream_t stream) {
+    int rc = check_table(table, "pkv_store_touch");
+    if (rc) return rc;
+    if (n_req == 0) return PKV_OK;
+    if ((!d_keys && n_keys) || !d_key_off || !d_hit_blocks || (!d_locs && n_keys) || !d_n_new || !d_status ||
+        !d_epochs)
+        return set_error(PKV_EINVAL, "pkv_store_touch: null argument");
+    if (!aligned(d_keys, 16)) return set_error(PKV_EINVAL, "pkv_store_touch: keys not 16-byte aligned");
+    return launch_store(table->keys, table->locs, table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
+                        d_locs, d_new_slots, d_n_new, d_epochs, epoch, d_status, stream);
+}
+
+int pkv_table_evict(const pkv_table* table, const uint32_t* d_epochs, uint64_t budget, void* d_work,
+                    uint64_t* d_n_evicted, hipStream_t stream) {
+    int rc = check_table(table, "pkv_table_evict");
+    if (rc) return rc;
+    if (!d_epochs || !d_work || !d_n_evicted) return set_error(PKV_EINVAL, "pkv_table_evict: null argument");
+    if (!aligned(d_work, 8)) return set_error(PKV_EINVAL, "pkv_table_evict: work area not 8-byte aligned");
+    return launch_evict(table->keys, table->locs, table->capacity, d_epochs, budget, static_cast<uint32_t*>(d_work),
+                        d_n_evicted, stream);
 }
 
 int pkv_table_rollback(const pkv_table* table, const uint64_t* d_new_slots, const uint64_t* d_n_new,

@@ -1,19 +1,23 @@
 // k_table.hip -- the shared-tier index in HBM: init, longest-prefix lookup, store of misses,
-// rollback and export, on gfx950.
+// rollback, export and eviction to a budget, on gfx950.
 //
 // Layout: struct of arrays.  keys[capacity] (16 bytes each) grouped in 4-slot buckets, so one
-// bucket is one 64-byte segment; locs[capacity + 1] (8 bytes each), the extra word holding the
-// location of the all-0xFF key (that value marks an empty key slot).  A key's home bucket is
-// its first eight bytes masked to the bucket count; probing is linear over slots, wrapping.
+// bucket is one 64-byte segment; locs[capacity + 2] (8 bytes each), the two extra words holding
+// the locations of the two reserved key patterns (all 0xFF marks an empty key slot, all 0xFF with
+// a last byte 0xFE a removed one).  A key's home bucket is its first eight bytes masked to the
+// bucket count; probing is linear over slots, wrapping.  A fixed-budget tier adds epochs[capacity
+// + 2] (uint32): the epoch of each entry's last use.
 //
 // Lookup reads only key slots: a key is present iff some slot on its probe path holds it, and
-// absent once the path meets an empty slot.  Store drives a per-slot state machine in the
-// location word with 64-bit atomics (gfx950 has no 128-bit compare-and-swap):
-//   empty --CAS--> pending --(write key, wait, publish)--> location | fresh
-// A lane that meets a pending slot re-reads it until it is published, then compares keys, so
-// two lanes inserting one key always meet in the same slot.  A later equal key lowers a fresh
-// entry's location with atomic min; entries older than the batch carry no fresh bit and are
-// left untouched.  A final pass clears the fresh bits.
+// absent once the path meets an empty slot (removed slots carry a pattern no probe key equals,
+// so paths run through them).  Store drives a per-slot state machine in the location word with
+// 64-bit atomics (gfx950 has no 128-bit compare-and-swap):
+//   empty or removed --CAS--> pending --(write key, wait, publish)--> location | fresh
+// A lane first scans its key's path up to the first empty slot, remembering the first removed
+// slot; it then claims that slot (or the empty one).  A lane that meets a pending slot re-reads it
+// until it is published, then compares keys, so two lanes inserting one key always meet in the
+// same slot.  A later equal key lowers a fresh entry's location with atomic min; entries older
+// than the batch carry no fresh bit and are left untouched.  A final pass clears the fresh bits.
 #include "pkv_internal.h"
 
 namespace pkv {
@@ -40,7 +44,7 @@ __device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
 __global__ __launch_bounds__(256) void k_init(uint4* keys, uint64_t* locs, uint64_t capacity) {
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
-    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i <= capacity; i += stride) {
+    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i <= capacity + 1; i += stride) {
         if (i < capacity) keys[i] = marker;
         locs[i] = kEmpty;
     }
@@ -59,26 +63,28 @@ __global__ __launch_bounds__(256) void k_init(uint4* keys, uint64_t* locs, uint6
 constexpr int kLookupWaves = 4;
 constexpr int kChunks = PKV_LOOKUP_CHUNKS;
 
-// Probe of one key (lane-private): bucket slots already loaded in sl[0..3].  Returns 1 = present,
-// 0 = absent; continues to later buckets while a full bucket neither matches nor ends the path.
-__device__ __forceinline__ bool probe_key(const uint4* __restrict__ tkeys, const uint64_t* __restrict__ tlocs,
-                                          uint64_t capacity, uint64_t bmask, const uint4& key, uint64_t b,
-                                          uint4 sl[4]) {
-    if (is_marker(key)) return tlocs[capacity] != kEmpty;
+// Probe of one key (lane-private): bucket slots already loaded in sl[0..3].  Returns the slot
+// holding the key, or -1 when it is absent; continues to later buckets while a full bucket
+// neither matches nor ends the path.
+__device__ __forceinline__ int64_t probe_key(const uint4* __restrict__ tkeys, const uint64_t* __restrict__ tlocs,
+                                             uint64_t capacity, uint64_t bmask, const uint4& key, uint64_t b,
+                                             uint4 sl[4]) {
+    const uint64_t rs = dev::reserved_slot(key, capacity);
+    if (rs) return tlocs[rs] != kEmpty ? static_cast<int64_t>(rs) : -1;
     const uint64_t n_buckets = bmask + 1;
     for (uint64_t it = 0; it < n_buckets; ++it) {
         bool empty = false;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            if (eq4(sl[j], key)) return true;
+            if (eq4(sl[j], key)) return static_cast<int64_t>(b * kSlotsPerBucket + j);
             empty |= is_marker(sl[j]);
         }
-        if (empty) return false;
+        if (empty) return -1;
         b = (b + 1) & bmask;
 #pragma unroll
         for (int j = 0; j < 4; ++j) sl[j] = tkeys[b * kSlotsPerBucket + j];
     }
-    return false;
+    return -1;
 }
 
 __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __restrict__ tkeys,
@@ -86,6 +92,7 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
                                                             const uint4* __restrict__ keys,
                                                             const int64_t* __restrict__ key_off, uint32_t n_req,
                                                             uint64_t n_keys, int32_t* __restrict__ hits,
+                                                            uint32_t* __restrict__ epochs, uint32_t epoch,
                                                             int32_t* status) {
     const uint32_t lane = lane_id();
     const uint32_t r = blockIdx.x * kLookupWaves + (threadIdx.x >> 6);
@@ -139,14 +146,24 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
 #pragma unroll
         for (int c = 0; c < kChunks; ++c) nk[c] = key_at(next_base + 64 * c + lane, c < next_chunks);
         int64_t stop = -1;
+        int64_t fslot[kChunks];
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) fslot[c] = -1;
 #pragma unroll
         for (int c = 0; c < kChunks; ++c) {
             if (c >= chunks) break;
-            const bool found = v[c] && probe_key(tkeys, tlocs, capacity, bmask, ck[c], bk[c], sl[c]);
-            const uint64_t miss = __ballot(v[c] && !found);
+            fslot[c] = v[c] ? probe_key(tkeys, tlocs, capacity, bmask, ck[c], bk[c], sl[c]) : -1;
+            const uint64_t miss = __ballot(v[c] && fslot[c] < 0);
             if (miss) {
                 stop = base + 64 * c + __builtin_ctzll(miss);
                 break;
+            }
+        }
+        if (epochs) {                           // a touching lookup refreshes every hit key
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) {
+                const int64_t idx = base + 64 * c + lane;
+                if (c < chunks && fslot[c] >= 0 && (stop < 0 || idx < stop)) epochs[fslot[c]] = epoch;
             }
         }
         if (stop >= 0) {
@@ -175,6 +192,8 @@ struct StoreArgs {
     const uint64_t* locs;
     uint64_t* new_slots;
     uint64_t* n_new;
+    uint32_t* epochs;          // null unless the store refreshes epochs
+    uint32_t epoch;
     int32_t* status;
 };
 
@@ -199,14 +218,16 @@ __device__ __forceinline__ uint64_t wave_base_of(uint32_t block_threads) {
 }
 
 // Key bytes of a slot whose location word was seen published, read as two relaxed 64-bit
-// atomics.  During one store launch a key slot only ever holds the empty marker or its final key,
-// so a half that is not all ones is final.  A half that reads all ones is re-read after an
-// acquire fence: either it really is all ones, or the read was stale.
+// atomics.  During one store launch a key slot only ever holds a marker pattern (empty or removed)
+// or its final key, so a half that matches neither marker's half is final.  A half that does is
+// re-read after an acquire fence: either it really has that value, or the read was stale.
+constexpr uint64_t kTombHi = (static_cast<uint64_t>(kTombW) << 32) | 0xFFFFFFFFull;
+
 __device__ __forceinline__ uint4 read_slot_key(uint4* tkeys, uint64_t s) {
     uint64_t* p = reinterpret_cast<uint64_t*>(tkeys + s);
     uint64_t lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     uint64_t hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (lo == ~0ull || hi == ~0ull) {
+    if (lo == ~0ull || hi == ~0ull || hi == kTombHi) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -258,44 +279,68 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
     }
     bool claimed = false;
     uint64_t my_slot = 0;
-    if (active && is_marker(key)) {
-        // the all-0xFF key lives in the extra location word; there are no key bytes to publish
-        uint64_t* p = a.tlocs + a.capacity;
+    const uint64_t rs = active ? dev::reserved_slot(key, a.capacity) : 0;
+    if (rs) {
+        // a reserved key lives in its own location word; there are no key bytes to publish
+        uint64_t* p = a.tlocs + rs;
         for (uint32_t spin = 0; spin < kWaitLimit; ++spin) {
             const uint64_t l = load_relaxed(p);
             if (l == kEmpty) {
-                if (cas_relaxed(p, kEmpty, want)) { claimed = true; my_slot = a.capacity; break; }
+                if (cas_relaxed(p, kEmpty, want)) { claimed = true; my_slot = rs; break; }
                 continue;
             }
             if (l & kFresh) min_relaxed(p, want);
             break;
         }
+        if (a.epochs) a.epochs[rs] = a.epoch;
     } else if (active) {
         const uint64_t slot_mask = a.capacity - 1;
         uint64_t s = home_bucket(key, (a.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
-        uint64_t probes = 0;
+        uint64_t steps = 0, first_free = ~0ull;  // slots passed in the current phase; first removed slot
         uint32_t waits = 0;
+        bool scanning = true;                    // phase 1: the key may still sit further along
         while (true) {
             const uint64_t l = load_relaxed(a.tlocs + s);
-            if (l == kEmpty) {
-                if (cas_relaxed(a.tlocs + s, kEmpty, kPending)) {
-                    publish_slot(a.tkeys, a.tlocs, s, key, want);
-                    claimed = true;
-                    my_slot = s;
-                    break;
-                }
-                continue;                       // lost the race: read the slot again
-            }
             if (l == kPending) {
                 if (++waits >= kWaitLimit) { report(a.status, PKV_ESTALL); break; }
                 continue;
             }
-            if (eq4(read_slot_key(a.tkeys, s), key)) {
+            const bool free_slot = l == kEmpty || l == kTomb;
+            if (free_slot && !(scanning && l == kTomb)) {
+                if (scanning) {                  // an empty slot ends the path: the key is absent
+                    scanning = false;
+                    steps = 0;
+                    if (first_free != ~0ull) {   // claim the first removed slot on the path instead
+                        s = first_free;
+                        continue;
+                    }
+                }
+                if (cas_relaxed(a.tlocs + s, l, kPending)) {
+                    publish_slot(a.tkeys, a.tlocs, s, key, want);
+                    if (a.epochs) a.epochs[s] = a.epoch;
+                    claimed = true;
+                    my_slot = s | (l == kTomb ? kFromTomb : 0);
+                    break;
+                }
+                continue;                       // lost the race: read the slot again
+            }
+            if (!free_slot && eq4(read_slot_key(a.tkeys, s), key)) {
                 if (l & kFresh) min_relaxed(a.tlocs + s, want);
+                if (a.epochs) a.epochs[s] = a.epoch;
                 break;
             }
+            if (free_slot && first_free == ~0ull) first_free = s;   // a removed slot met while scanning
             s = (s + 1) & slot_mask;
-            if (++probes >= a.capacity) { report(a.status, PKV_EFULL); break; }
+            if (++steps >= a.capacity) {         // a whole cycle
+                if (scanning && first_free != ~0ull) {
+                    scanning = false;
+                    steps = 0;
+                    s = first_free;
+                    continue;
+                }
+                report(a.status, PKV_EFULL);
+                break;
+            }
         }
     }
     // one counter update per wavefront; slot log in lane order
@@ -323,10 +368,10 @@ __global__ __launch_bounds__(256) void k_store_finish_log(uint64_t* tlocs, uint6
     if (n > max_slots) n = max_slots;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
-        const uint64_t s = slots[i];
-        if (s > capacity) continue;
+        const uint64_t s = slots[i] & ~kFromTomb;
+        if (s > capacity + 1) continue;
         const uint64_t l = tlocs[s];
-        if (l != kEmpty && l != kPending && (l & kFresh)) tlocs[s] = l & ~kFresh;
+        if (l != kEmpty && l != kPending && l != kTomb && (l & kFresh)) tlocs[s] = l & ~kFresh;
     }
 }
 
@@ -338,23 +383,21 @@ __global__ __launch_bounds__(kStoreThreads) void k_store_finish_probe(StoreArgs 
     if (total < 0 || static_cast<uint64_t>(total) > a.n_keys) return;
     if (!candidate(a, wave_base, k, total)) return;
     const uint4 key = a.keys[k];
-    uint64_t s;
-    if (is_marker(key)) {
-        s = a.capacity;
-    } else {
+    uint64_t s = dev::reserved_slot(key, a.capacity);
+    if (!s) {
         const uint64_t slot_mask = a.capacity - 1;
         s = home_bucket(key, (a.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
         uint64_t probes = 0;
         while (true) {
             const uint64_t l = a.tlocs[s];
             if (l == kEmpty || l == kPending) return;   // not stored (an error was reported)
-            if (eq4(a.tkeys[s], key)) break;
+            if (l != kTomb && eq4(a.tkeys[s], key)) break;
             s = (s + 1) & slot_mask;
             if (++probes >= a.capacity) return;
         }
     }
     const uint64_t l = a.tlocs[s];
-    if (l != kEmpty && l != kPending && (l & kFresh)) a.tlocs[s] = l & ~kFresh;
+    if (l != kEmpty && l != kPending && l != kTomb && (l & kFresh)) a.tlocs[s] = l & ~kFresh;
 }
 
 // ---- rollback and export ------------------------------------------------------------------------
@@ -365,11 +408,12 @@ __global__ __launch_bounds__(256) void k_rollback(uint4* tkeys, uint64_t* tlocs,
     const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
-        const uint64_t s = slots[i];
+        const uint64_t s = slots[i] & ~kFromTomb;
         if (s < capacity) {
-            tkeys[s] = marker;
-            tlocs[s] = kEmpty;
-        } else if (s == capacity) {
+            const bool tomb = (slots[i] & kFromTomb) != 0;   // back to the state the store found
+            tkeys[s] = tomb ? make_uint4(~0u, ~0u, ~0u, kTombW) : marker;
+            tlocs[s] = tomb ? kTomb : kEmpty;
+        } else if (s <= capacity + 1) {
             tlocs[s] = kEmpty;
         }
     }
@@ -383,10 +427,10 @@ __global__ __launch_bounds__(256) void k_export(const uint4* tkeys, const uint64
     const uint64_t waves = static_cast<uint64_t>(gridDim.x) * (blockDim.x / 64);
     const uint64_t wave = blockIdx.x * static_cast<uint64_t>(blockDim.x / 64) + (threadIdx.x >> 6);
     const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
-    for (uint64_t base = wave * 64; base <= capacity; base += waves * 64) {
+    for (uint64_t base = wave * 64; base <= capacity + 1; base += waves * 64) {
         const uint64_t s = base + lane;
-        const uint64_t l = s <= capacity ? tlocs[s] : kEmpty;
-        const bool occ = l != kEmpty;
+        const uint64_t l = s <= capacity + 1 ? tlocs[s] : kEmpty;
+        const bool occ = l != kEmpty && !(s < capacity && l == kTomb);
         const uint64_t mask = __ballot(occ);
         if (!mask) continue;
         const uint32_t leader = __builtin_ctzll(mask);
@@ -396,9 +440,154 @@ __global__ __launch_bounds__(256) void k_export(const uint4* tkeys, const uint64
                                          __HIP_MEMORY_SCOPE_AGENT);
         pos = __shfl(pos, leader, 64) + __popcll(mask & ((1ull << lane) - 1));
         if (occ) {
-            out_keys[pos] = s < capacity ? tkeys[s] : marker;
+            out_keys[pos] = s < capacity ? tkeys[s] : (s == capacity ? marker : make_uint4(~0u, ~0u, ~0u, kTombW));
             out_locs[pos] = l;
         }
+    }
+}
+
+// ---- eviction to a budget (quiescent index) ---------------------------------------------------
+// Generational: with E* the smallest epoch such that at most `budget` live entries were last used
+// at or after E*, every live entry used before E* is removed (its key slot becomes a removed
+// slot; a reserved key's location word becomes empty).  E* is found by a radix select over the
+// 32-bit epochs in two 16-bit digits: a histogram pass over the index and a one-workgroup scan per
+// digit.  The work area holds the two histograms and a small control block.
+constexpr uint32_t kHistBins = 65536;
+constexpr uint32_t kSelectThreads = 1024;
+struct EvictCtl {
+    uint64_t cut;      // E*: entries with epoch < cut are removed
+    uint64_t above;    // live entries whose high digit exceeds h0
+    uint32_t h0;       // high digit of E* - 1
+    uint32_t done;     // 1 when nothing has to be removed, or the selection is complete
+};
+
+__device__ __forceinline__ bool live_slot(uint64_t s, uint64_t l, uint64_t capacity) {
+    return l != kEmpty && !(s < capacity && (l == kTomb || l == kPending));
+}
+
+// Histogram increment aggregated over the wavefront: lanes with equal bins share one atomic.
+// Every lane of the wavefront must call it (the loop is wavefront-uniform).
+__device__ __forceinline__ void hist_add(uint32_t* hist, bool act, uint32_t bin) {
+    uint64_t todo = __ballot(act);
+    while (todo) {
+        const uint32_t leader = __builtin_ctzll(todo);
+        const uint32_t b = __shfl(bin, leader, 64);
+        const uint64_t same = __ballot(act && bin == b) & todo;
+        if (lane_id() == leader) atomicAdd(hist + b, static_cast<uint32_t>(__popcll(same)));
+        todo &= ~same;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_evict_clear(uint32_t* work, uint64_t* n_evicted) {
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < 2 * kHistBins; i += stride)
+        work[i] = 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        EvictCtl* c = reinterpret_cast<EvictCtl*>(work + 2 * kHistBins);
+        c->cut = 0;
+        c->above = 0;
+        c->h0 = 0;
+        c->done = 0;
+        *n_evicted = 0;
+    }
+}
+
+// digit 0: high 16 bits of every live entry's epoch; digit 1: low 16 bits of the entries whose high
+// digit is h0.
+__global__ __launch_bounds__(256) void k_evict_hist(const uint64_t* tlocs, uint64_t capacity, const uint32_t* epochs,
+                                                    uint32_t* work, int digit) {
+    const EvictCtl* c = reinterpret_cast<const EvictCtl*>(work + 2 * kHistBins);
+    if (digit == 1 && c->done) return;
+    uint32_t* hist = work + digit * kHistBins;
+    const uint32_t h0 = c->h0;
+    const uint64_t waves = static_cast<uint64_t>(gridDim.x) * (blockDim.x / 64);
+    const uint64_t wave = blockIdx.x * static_cast<uint64_t>(blockDim.x / 64) + (threadIdx.x >> 6);
+    for (uint64_t base = wave * 64; base < capacity + 2; base += waves * 64) {
+        const uint64_t s = base + lane_id();
+        bool act = false;
+        uint32_t bin = 0;
+        if (s < capacity + 2 && live_slot(s, tlocs[s], capacity)) {
+            const uint32_t e = epochs[s];
+            act = digit == 0 || (e >> 16) == h0;
+            bin = digit == 0 ? (e >> 16) : (e & 0xFFFFu);
+        }
+        hist_add(hist, act, bin);
+    }
+}
+
+// One workgroup.  With G(b) = base + sum of hist[b'] over b' >= b, finds the largest b with
+// G(b) > budget (it exists whenever G(0) > budget).
+__global__ __launch_bounds__(kSelectThreads) void k_evict_select(uint32_t* work, uint64_t budget, int digit) {
+    __shared__ uint64_t part[kSelectThreads];
+    __shared__ uint32_t best;
+    __shared__ uint64_t total;
+    EvictCtl* c = reinterpret_cast<EvictCtl*>(work + 2 * kHistBins);
+    if (digit == 1 && c->done) return;
+    const uint32_t* hist = work + digit * kHistBins;
+    const uint32_t t = threadIdx.x;
+    constexpr uint32_t per = kHistBins / kSelectThreads;
+    uint64_t mine = 0;
+    for (uint32_t i = 0; i < per; ++i) mine += hist[t * per + i];
+    part[t] = mine;
+    if (t == 0) best = 0;          // raised by atomicMax; some thread always finds a bin when not done
+    __syncthreads();
+    // exclusive suffix sum over threads: the live entries in bins above this thread's range
+    uint64_t above_t = digit == 0 ? 0 : c->above;
+    for (uint32_t u = t + 1; u < kSelectThreads; ++u) above_t += part[u];
+    if (t == 0) total = above_t + mine;
+    __syncthreads();
+    if (digit == 0 && total <= budget) {          // everything fits: nothing to remove
+        if (t == 0) {
+            c->cut = 0;
+            c->done = 1;
+        }
+        return;
+    }
+    uint64_t acc = above_t;
+    uint32_t found = 0xFFFFFFFFu;
+    uint64_t before = 0;
+    for (int i = static_cast<int>(per) - 1; i >= 0; --i) {
+        const uint64_t prev = acc;
+        acc += hist[t * per + i];
+        if (acc > budget) { found = t * per + i; before = prev; break; }
+    }
+    if (found != 0xFFFFFFFFu) atomicMax(&best, found);
+    __syncthreads();
+    if (found != 0xFFFFFFFFu && found == best) {
+        if (digit == 0) {
+            c->h0 = found;
+            c->above = before;                // G(h0 + 1)
+        } else {
+            c->cut = (static_cast<uint64_t>(c->h0) << 16) + found + 1;
+            c->done = 1;
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_evict_apply(uint4* tkeys, uint64_t* tlocs, uint64_t capacity,
+                                                     const uint32_t* epochs, const uint32_t* work,
+                                                     uint64_t* n_evicted) {
+    const EvictCtl* c = reinterpret_cast<const EvictCtl*>(work + 2 * kHistBins);
+    const uint64_t cut = c->cut;
+    if (cut == 0) return;
+    const uint64_t waves = static_cast<uint64_t>(gridDim.x) * (blockDim.x / 64);
+    const uint64_t wave = blockIdx.x * static_cast<uint64_t>(blockDim.x / 64) + (threadIdx.x >> 6);
+    for (uint64_t base = wave * 64; base < capacity + 2; base += waves * 64) {
+        const uint64_t s = base + lane_id();
+        bool ev = false;
+        if (s < capacity + 2 && live_slot(s, tlocs[s], capacity) && epochs[s] < cut) {
+            ev = true;
+            if (s < capacity) {
+                tkeys[s] = make_uint4(~0u, ~0u, ~0u, kTombW);
+                tlocs[s] = kTomb;
+            } else {
+                tlocs[s] = kEmpty;
+            }
+        }
+        const uint64_t mask = __ballot(ev);
+        if (mask && lane_id() == __builtin_ctzll(mask))
+            __hip_atomic_fetch_add(n_evicted, static_cast<uint64_t>(__popcll(mask)), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -448,28 +637,41 @@ int launch_sum_hits(const int32_t* hits, uint32_t n_req, const int64_t* group_of
     return check_launch("pkv_sum_hits");
 }
 
+int launch_evict(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint32_t* epochs, uint64_t budget,
+                 uint32_t* work, uint64_t* n_evicted, hipStream_t s) {
+    const unsigned g = grid_for(capacity + 2, 256, 16384);
+    hipLaunchKernelGGL(k_evict_clear, dim3(grid_for(2 * kHistBins, 256, 512)), dim3(256), 0, s, work, n_evicted);
+    for (int digit = 0; digit < 2; ++digit) {
+        hipLaunchKernelGGL(k_evict_hist, dim3(g), dim3(256), 0, s, tlocs, capacity, epochs, work, digit);
+        hipLaunchKernelGGL(k_evict_select, dim3(1), dim3(kSelectThreads), 0, s, work, budget, digit);
+    }
+    hipLaunchKernelGGL(k_evict_apply, dim3(g), dim3(256), 0, s, reinterpret_cast<uint4*>(tkeys), tlocs, capacity,
+                       epochs, work, n_evicted);
+    return check_launch("pkv_table_evict");
+}
+
 int launch_table_init(uint8_t* keys, uint64_t* locs, uint64_t capacity, hipStream_t s) {
-    hipLaunchKernelGGL(k_init, dim3(grid_for(capacity + 1, 256, 16384)), dim3(256), 0, s,
+    hipLaunchKernelGGL(k_init, dim3(grid_for(capacity + 2, 256, 16384)), dim3(256), 0, s,
                        reinterpret_cast<uint4*>(keys), locs, capacity);
     return check_launch("pkv_table_init");
 }
 
 int launch_lookup(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity, const uint8_t* keys,
-                  const int64_t* key_off, uint32_t n_req, uint64_t n_keys, int32_t* hits, int32_t* status,
-                  hipStream_t s) {
+                  const int64_t* key_off, uint32_t n_req, uint64_t n_keys, int32_t* hits, uint32_t* epochs,
+                  uint32_t epoch, int32_t* status, hipStream_t s) {
     if (n_req == 0) return PKV_OK;
     hipLaunchKernelGGL(k_lookup, dim3((n_req + kLookupWaves - 1) / kLookupWaves), dim3(64 * kLookupWaves), 0, s,
                        reinterpret_cast<const uint4*>(tkeys), tlocs, capacity, reinterpret_cast<const uint4*>(keys),
-                       key_off, n_req, n_keys, hits, status);
+                       key_off, n_req, n_keys, hits, epochs, epoch, status);
     return check_launch("pkv_lookup_prefix");
 }
 
 int launch_store(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint8_t* keys, const int64_t* key_off,
                  uint32_t n_req, uint64_t n_keys, const int32_t* hits, const uint64_t* locs, uint64_t* new_slots,
-                 uint64_t* n_new, int32_t* status, hipStream_t s) {
+                 uint64_t* n_new, uint32_t* epochs, uint32_t epoch, int32_t* status, hipStream_t s) {
     if (n_req == 0 || n_keys == 0) return PKV_OK;
     StoreArgs a{reinterpret_cast<uint4*>(tkeys), tlocs, capacity, reinterpret_cast<const uint4*>(keys),
-                key_off, n_req, n_keys, hits, locs, new_slots, n_new, status};
+                key_off, n_req, n_keys, hits, locs, new_slots, n_new, epochs, epoch, status};
     const uint64_t blocks = (n_keys + kStoreThreads - 1) / kStoreThreads;
     if (blocks > 0x7fffffffull) return set_error(PKV_EINVAL, "pkv_store: too many keys (%llu)",
                                                  static_cast<unsigned long long>(n_keys));
@@ -498,7 +700,7 @@ int launch_export(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity
     hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(1), 0, s, count);
     int rc = check_launch("pkv_table_export (zero)");
     if (rc) return rc;
-    hipLaunchKernelGGL(k_export, dim3(grid_for(capacity + 1, 256, 8192)), dim3(256), 0, s,
+    hipLaunchKernelGGL(k_export, dim3(grid_for(capacity + 2, 256, 8192)), dim3(256), 0, s,
                        reinterpret_cast<const uint4*>(tkeys), tlocs, capacity, reinterpret_cast<uint4*>(out_keys),
                        out_locs, count);
     return check_launch("pkv_table_export");

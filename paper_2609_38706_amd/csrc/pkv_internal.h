@@ -23,14 +23,21 @@ static constexpr uint32_t kInitH[8] = {0x6a09e667u, 0xbb67ae85u, 0x3c6ef372u, 0x
                                       0x510e527fu, 0x9b05688cu, 0x1f83d9abu, 0x5be0cd19u};
 
 // Index slot encoding.  A slot's location word is the state of the slot:
-//   kEmpty    -- free (its key bytes are all 0xFF);
+//   kEmpty    -- never used (its key bytes are all 0xFF); ends every probe path through it;
+//   kTomb     -- removed by eviction (its key bytes are the removed-entry pattern): free for a
+//                new key, but probe paths continue through it;
 //   kPending  -- claimed by an inserting lane that has not yet published the key;
 //   other     -- occupied; bit 63 (kFresh) marks an entry inserted by the running store batch,
 //                whose location may still be lowered to the batch minimum.
-// Valid caller locations are < 2^62, so no occupied value collides with the two markers.
+// Valid caller locations are < 2^62, so no occupied value collides with the markers.  Two key
+// byte patterns are reserved (all 0xFF: empty; all 0xFF with a last byte 0xFE: removed); keys
+// equal to them live in the location words at [capacity] and [capacity + 1].
 static constexpr uint64_t kEmpty = ~0ull;
 static constexpr uint64_t kPending = ~0ull - 1;
+static constexpr uint64_t kTomb = ~0ull - 2;
 static constexpr uint64_t kFresh = 1ull << 63;
+static constexpr uint64_t kFromTomb = 1ull << 63;   // slot-log flag: the claimed slot was a removed entry
+static constexpr uint32_t kTombW = 0xFEFFFFFFu;     // last 32-bit word of the removed-entry pattern
 static constexpr uint32_t kSlotsPerBucket = 4;   // 4 x 16-byte keys = one 64-byte segment
 
 namespace dev {
@@ -90,6 +97,13 @@ __device__ __forceinline__ bool eq4(const uint4& a, const uint4& b) {
     return ((a.x ^ b.x) | (a.y ^ b.y) | (a.z ^ b.z) | (a.w ^ b.w)) == 0;
 }
 __device__ __forceinline__ bool is_marker(const uint4& a) { return (a.x & a.y & a.z & a.w) == 0xFFFFFFFFu; }
+__device__ __forceinline__ bool is_tomb_key(const uint4& a) { return (a.x & a.y & a.z) == 0xFFFFFFFFu && a.w == kTombW; }
+// Location word of a reserved key (capacity for the empty pattern, capacity + 1 for the removed
+// pattern), or 0 for an ordinary key.
+__device__ __forceinline__ uint64_t reserved_slot(const uint4& a, uint64_t capacity) {
+    if ((a.x & a.y & a.z) != 0xFFFFFFFFu) return 0;
+    return a.w == 0xFFFFFFFFu ? capacity : (a.w == kTombW ? capacity + 1 : 0);
+}
 
 // Home bucket: the key is a SHA-256 output, so its first eight bytes are already uniform.
 __device__ __forceinline__ uint64_t home_bucket(const uint4& k, uint64_t bucket_mask) {
@@ -107,11 +121,14 @@ int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_o
                   uint8_t* keys, int32_t* status, hipStream_t s);
 int launch_table_init(uint8_t* keys, uint64_t* locs, uint64_t capacity, hipStream_t s);
 int launch_lookup(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity, const uint8_t* keys,
-                  const int64_t* key_off, uint32_t n_req, uint64_t n_keys, int32_t* hits, int32_t* status,
-                  hipStream_t s);
+                  const int64_t* key_off, uint32_t n_req, uint64_t n_keys, int32_t* hits, uint32_t* epochs,
+                  uint32_t epoch, int32_t* status, hipStream_t s);
 int launch_store(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint8_t* keys, const int64_t* key_off,
                  uint32_t n_req, uint64_t n_keys, const int32_t* hits, const uint64_t* locs,
-                 uint64_t* new_slots, uint64_t* n_new, int32_t* status, hipStream_t s);
+                 uint64_t* new_slots, uint64_t* n_new, uint32_t* epochs, uint32_t epoch, int32_t* status,
+                 hipStream_t s);
+int launch_evict(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint32_t* epochs, uint64_t budget,
+                 uint32_t* work, uint64_t* n_evicted, hipStream_t s);
 int launch_rollback(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint64_t* slots,
                     const uint64_t* n_slots, uint64_t max_slots, hipStream_t s);
 int launch_sum_hits(const int32_t* hits, uint32_t n_req, const int64_t* group_off, uint32_t n_groups, uint64_t* sums,

@@ -66,40 +66,44 @@ def raw_table(table):
 
 EMPTY = np.uint64(0xFFFFFFFFFFFFFFFF)
 PENDING = np.uint64(0xFFFFFFFFFFFFFFFE)
+TOMB = np.uint64(0xFFFFFFFFFFFFFFFD)
 FRESH = np.uint64(1 << 63)
+TOMB_KEY = np.array([0xFF] * 15 + [0xFE], np.uint8)
 
 
 def check_structure(table):
-    """Index invariants: every occupied slot is reachable from its home bucket with no empty slot
-    in between; no claimed-but-unpublished or batch-marked slot survives a store; empty slots hold
-    the all-0xFF key; the all-0xFF key never occupies an ordinary slot; no key is stored twice."""
+    """Index invariants: every live slot is reachable from its home bucket with no empty slot in
+    between (removed slots do not break paths); no claimed-but-unpublished or batch-marked slot
+    survives a store; empty slots hold the all-0xFF key and removed slots the removed pattern; no
+    reserved pattern occupies an ordinary live slot; no key is stored twice.  Returns the number of
+    entries (live slots plus occupied reserved-key words)."""
     keys, locs = raw_table(table)
     cap = table.capacity
+    assert locs.shape[0] == cap + 2
     main = locs[:cap]
-    occ = main != EMPTY
+    occ = main != EMPTY                      # on some probe path: live or removed
+    tomb = main == TOMB
+    live = occ & ~tomb
     assert not (main == PENDING).any(), "pending slot left behind"
-    assert not (main[occ] & FRESH).any(), "fresh bit left behind"
+    assert not (main[live] & FRESH).any(), "fresh bit left behind"
     assert (keys[~occ] == 0xFF).all(), "empty slot with key bytes"
-    marker = (keys == 0xFF).all(axis=1)
-    assert not (occ & marker).any(), "marker key stored in an ordinary slot"
-    if not occ.any():
-        return int(occ.sum())
-    assert not occ.all() or True
-    # home slot of each occupied key
-    lo = keys[:, :8].copy().view("<u8").reshape(-1)
-    home = (lo & np.uint64(cap // 4 - 1)).astype(np.int64) * 4
-    idx = np.arange(cap, dtype=np.int64)
-    # last empty position at or before each index, cyclically
-    last = np.where(~occ, idx, -1)
-    last = np.maximum.accumulate(last)
-    if (~occ).any():
-        wrap_last = int(idx[~occ][-1]) - cap
-        last = np.where(last < 0, wrap_last, last)
-        s = idx[occ]
-        dist_home = (s - home[occ]) % cap
-        dist_empty = s - last[occ]
-        assert (dist_home < dist_empty).all(), "occupied slot not reachable from its home bucket"
-    # no duplicate keys
-    ok = keys[occ]
-    assert np.unique(ok.view("V16").reshape(-1)).shape[0] == ok.shape[0], "duplicate key stored"
-    return int(occ.sum()) + int(locs[cap] != EMPTY)
+    assert (keys[tomb] == TOMB_KEY[None, :]).all(), "removed slot without the removed pattern"
+    marker = (keys == 0xFF).all(axis=1) | (keys == TOMB_KEY[None, :]).all(axis=1)
+    assert not (live & marker).any(), "reserved pattern stored in an ordinary slot"
+    if live.any():
+        lo = keys[:, :8].copy().view("<u8").reshape(-1)
+        home = (lo & np.uint64(cap // 4 - 1)).astype(np.int64) * 4
+        idx = np.arange(cap, dtype=np.int64)
+        # last empty position at or before each index, cyclically
+        last = np.where(~occ, idx, -1)
+        last = np.maximum.accumulate(last)
+        if (~occ).any():
+            wrap_last = int(idx[~occ][-1]) - cap
+            last = np.where(last < 0, wrap_last, last)
+            s = idx[live]
+            dist_home = (s - home[live]) % cap
+            dist_empty = s - last[live]
+            assert (dist_home < dist_empty).all(), "live slot not reachable from its home bucket"
+        lk = keys[live]
+        assert np.unique(lk.view("V16").reshape(-1)).shape[0] == lk.shape[0], "duplicate key stored"
+    return int(live.sum()) + int(locs[cap] != EMPTY) + int(locs[cap + 1] != EMPTY)
