@@ -41,6 +41,9 @@ WORKLOAD_TEXT = {
     "c5": "256 req x 131072 tok, block 16, groups of 4 with uniform fork points, 4M-slot index",
     "omission": "differential omission test (Eq. 4): 512 req x 1024 tok, block 16, 20 registered dimensions, "
                 "22 bindings (complete, 20 leave-one-out, token-only) x (base + 20 one-dimension variants)",
+    "budget": "fixed-budget tier: stream of 1024 req x 2048 tok batches (64 shared prefixes, fresh suffixes), "
+              "block 16, provenance classes drawn uniformly, 1M-slot index with a 2^18-entry budget; each step "
+              "touching lookup, touching store, generational eviction",
 }
 
 
@@ -86,6 +89,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_TEXT))
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--classes", type=int, default=8, help="provenance classes of the budget workload")
     p.add_argument("--no-saturation", action="store_true", help="skip the derive-at-full-occupancy diagnostic")
     p.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (0 = host cores, at most 16)")
     p.add_argument("--calib-copy", action="store_true", help="run only a plain 1 GiB device copy (counter calibration)")
@@ -266,6 +270,102 @@ def omission_leg(args):
             "omissions": int(res["omission"].sum())}
 
 
+def budget_leg(args):
+    """Steps of a fixed-budget tier over a cyclic stream of batches: derive, touching lookup,
+    touching store, eviction to the budget.  Retention = hit blocks / prefix blocks requested."""
+    import torch
+    import paper_2609_38706_amd as pkv
+    from paper_2609_38706_amd.pipeline import DeviceBatch
+    from workloads import locations, make_budget
+    batches, cap, budget = make_budget(classes=args.classes)
+    table = pkv.Table(cap, epochs=True)
+    dbs = []
+    for b in batches:
+        db = DeviceBatch.from_batch(b)
+        db.set_locations(locations(db.key_off.cpu().numpy(), b.tag))
+        dbs.append(db)
+    n_ev = torch.zeros(1, dtype=torch.int64, device="cuda")
+    stream = torch.cuda.current_stream()
+    state = {"epoch": 0}
+
+    def step(i, ev=None, hits_out=None, ev_out=None):
+        db = dbs[i % len(dbs)]
+        state["epoch"] += 1
+        e = state["epoch"]
+        db.n_new.zero_()
+        db.key_offsets()
+        db.digest()
+        if ev is not None:
+            ev[0].record(stream)
+        db.derive()
+        if ev is not None:
+            ev[1].record(stream)
+        pkv.pkv_lookup_prefix_touch(table, db.keys, db.key_off, e, db.hits[: db.n_req], db.status)
+        pkv.pkv_store_touch(table, db.keys, db.key_off, db.hits[: db.n_req], db.locs, db.n_new, db.status, e)
+        if ev is not None:
+            ev[2].record(stream)
+        pkv.pkv_table_evict(table, budget, n_ev)
+        if ev is not None:
+            ev[3].record(stream)
+        if hits_out is not None:
+            hits_out.copy_(db.hits[: db.n_req])
+            ev_out.copy_(n_ev)
+
+    for i in range(max(args.warmup, 2 * len(dbs))):
+        step(i)
+    torch.cuda.synchronize()
+    first = max(args.warmup, 2 * len(dbs))
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    hits = torch.zeros((args.steps, dbs[0].n_req), dtype=torch.int32, device="cuda")
+    evicted = torch.zeros(args.steps, dtype=torch.int64, device="cuda")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(first + k, evs[k], hits[k], evicted[k:k + 1])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for db in dbs:
+        if db.host_status() != 0:
+            raise RuntimeError(f"budget step failed: status {db.host_status()}")
+    h = hits.cpu().numpy()
+    pre = np.stack([batches[(first + k) % len(batches)].meta["prefix_blocks"] for k in range(args.steps)])
+    if (h > pre).any():
+        raise RuntimeError("budget tier: a request hit beyond its shared prefix")
+    n_keys = sum(dbs[(first + k) % len(dbs)].n_keys for k in range(args.steps))
+    return {"ms": (t1 - t0) * 1e3 / args.steps, "n_keys_per_step": n_keys // args.steps,
+            "derive_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evs])),
+            "index_ms": float(np.mean([e[1].elapsed_time(e[2]) for e in evs])),
+            "evict_ms": float(np.mean([e[2].elapsed_time(e[3]) for e in evs])),
+            "retention": float(h.sum() / pre.sum()), "evicted_per_step": float(evicted.float().mean().item()),
+            "n_req": dbs[0].n_req, "capacity": cap, "budget": budget, "batches": batches, "first": first}
+
+
+def budget_cpu_leg(args, g, target_s=10.0):
+    """The oracle on the same step sequence (touching lookup, touching store, eviction), from an
+    empty index, until about `target_s` seconds; rate in keys per second."""
+    import oracle
+    from workloads import locations
+    threads = args.cpu_threads or max(1, min(16, len(os.sched_getaffinity(0))))
+    batches = g["batches"]
+    idx = oracle.Index(g["capacity"])
+    total, keys_done, i = 0.0, 0, 0
+    while total < target_s:
+        b = batches[i % len(batches)]
+        i += 1
+        t0 = time.perf_counter()
+        ko = oracle.key_offsets(b.tok_off, b.block)
+        keys = oracle.derive(b.tokens, b.tok_off, oracle.batch_digests(b), b.block, threads)
+        hits = idx.lookup_touch(keys, ko, i)
+        assert idx.store_touch(keys, ko, hits, locations(ko, b.tag), i) == 0
+        idx.evict(g["budget"])
+        total += time.perf_counter() - t0
+        keys_done += int(ko[-1])
+    return {"value": round(keys_done / total / 1e9, 6), "unit": "Gkeys/s", "cores": threads, "kind": "oracle",
+            "sample": f"{i} steps of the same batch stream from an empty index (digests, derive on {threads} threads, "
+                      f"touching lookup and store and eviction single-threaded); {total:.2f} s",
+            "seconds": round(total, 3), "steps": i}
+
+
 def omission_cpu_leg(args, case, n_keys, target_s=10.0):
     """The oracle's omission matrix on the same case, repeated until about `target_s` seconds."""
     from oracle.omission import omission_matrix
@@ -335,6 +435,31 @@ def main():
     torch.cuda.set_device(0)
     if args.calib_copy:
         calib_copy()
+        return
+    if args.workload == "budget":
+        log(args, "budget tier")
+        g = budget_leg(args)
+        ops = g["n_keys_per_step"] * compressions_per_key(16) * OPS_PER_COMPRESSION
+        achieved = ops / (g["derive_ms"] * 1e-3)
+        cpu = None if args.no_cpu_baseline else budget_cpu_leg(args, g)
+        out = {
+            "metric": "provenance-bound block keys derived+probed per second (Gkeys/s); % of roofline",
+            "value": round(g["n_keys_per_step"] / (g["ms"] * 1e-3) / 1e9, 6), "unit": "Gkeys/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": max(args.warmup, 16), "ms_per_step": round(g["ms"], 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32", "data": "synthetic",
+            "config": {"workload": WORKLOAD_TEXT["budget"], "name": "budget", "classes": args.classes,
+                       "requests": g["n_req"], "keys": g["n_keys_per_step"], "block": 16, "capacity": g["capacity"],
+                       "budget": g["budget"], "parallelism": "1 GPU"},
+            "kernels_ms": {"derive": round(g["derive_ms"], 4), "lookup+store": round(g["index_ms"], 4),
+                           "evict": round(g["evict_ms"], 4)},
+            "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 4), "peak": round(INT_PEAK / 1e12, 4),
+                         "unit": "Tops/s", "frac": round(achieved / INT_PEAK, 5), "traffic": None, "kernel": "derive",
+                         "ops_per_key": compressions_per_key(16) * OPS_PER_COMPRESSION,
+                         "chain_ceiling_frac": round(chain_ceiling_frac(g["n_req"]), 5)},
+            "retention": round(g["retention"], 5), "evicted_per_step": g["evicted_per_step"],
+            "cpu_baseline": cpu,
+        }
+        print(json.dumps(out), flush=True)
         return
     if args.workload == "omission":
         log(args, "omission test")

@@ -186,7 +186,7 @@ int pkv_store_touch(const pkv_table* table, const uint8_t* d_keys, const int64_t
  * stay intact: its slot is marked removed, not empty).  d_work: PKV_EVICT_WORK_BYTES of device
  * memory (8-byte aligned, contents overwritten); *d_n_evicted receives the number removed.  The
  * index must not be accessed by other calls while this runs (stream order suffices). */
-#define PKV_EVICT_WORK_BYTES ((size_t)(2 * 65536 * 4 + 64))
+#define PKV_EVICT_WORK_BYTES ((size_t)(3 * 2048 * 4 + 64))
 int pkv_table_evict(const pkv_table* table, const uint32_t* d_epochs, uint64_t budget, void* d_work,
                     uint64_t* d_n_evicted, hipStream_t stream);
 

@@ -22,7 +22,7 @@ EXPORTED = ["pkv_descriptor_encode", "pkv_descriptor_digest", "pkv_digest_batch"
             "pkv_table_export", "pkv_sum_hits", "pkv_lookup_prefix_touch", "pkv_store_touch",
             "pkv_table_evict", "pkv_last_error", "pkv_version"]
 
-EVICT_WORK_BYTES = 2 * 65536 * 4 + 64   # PKV_EVICT_WORK_BYTES
+EVICT_WORK_BYTES = 3 * 2048 * 4 + 64   # PKV_EVICT_WORK_BYTES
 
 
 class PkvError(RuntimeError):

@@ -450,56 +450,71 @@ __global__ __launch_bounds__(256) void k_export(const uint4* tkeys, const uint64
 // Generational: with E* the smallest epoch such that at most `budget` live entries were last used
 // at or after E*, every live entry used before E* is removed (its key slot becomes a removed
 // slot; a reserved key's location word becomes empty).  E* is found by a radix select over the
-// 32-bit epochs in two 16-bit digits: a histogram pass over the index and a one-workgroup scan per
-// digit.  The work area holds the two histograms and a small control block.
-constexpr uint32_t kHistBins = 65536;
+// 32-bit epochs in three digits (bits 21-31, 10-20, 0-9): per digit, a histogram pass over the
+// index and a one-workgroup scan.  Histograms are kept per workgroup in LDS and flushed with one
+// global atomic per non-empty bin, so entries that share an epoch do not contend on one address.
+// The work area holds the three histograms and a small control block.
+constexpr uint32_t kDigitBins = 2048;
 constexpr uint32_t kSelectThreads = 1024;
+constexpr uint32_t kHistThreads = 1024;
+constexpr uint32_t kHistBlocks = 256;      // one workgroup per CU: one global atomic per hot bin each
+__host__ __device__ constexpr int digit_shift(int d) { return d == 0 ? 21 : (d == 1 ? 10 : 0); }
+__host__ __device__ constexpr uint32_t digit_bins(int d) { return d == 2 ? 1024u : 2048u; }
+
 struct EvictCtl {
-    uint64_t cut;      // E*: entries with epoch < cut are removed
-    uint64_t above;    // live entries whose high digit exceeds h0
-    uint32_t h0;       // high digit of E* - 1
+    uint64_t cut;      // E*: entries with epoch < cut are removed (0: none)
+    uint64_t above;    // live entries whose selected leading digits exceed the prefix so far
+    uint64_t live;     // live entries before the eviction
+    uint32_t prefix;   // leading digits selected so far (epoch >> digit_shift of the next digit)
     uint32_t done;     // 1 when nothing has to be removed, or the selection is complete
 };
+
+__device__ __forceinline__ EvictCtl* evict_ctl(uint32_t* work) {
+    return reinterpret_cast<EvictCtl*>(work + 3 * kDigitBins);
+}
 
 __device__ __forceinline__ bool live_slot(uint64_t s, uint64_t l, uint64_t capacity) {
     return l != kEmpty && !(s < capacity && (l == kTomb || l == kPending));
 }
 
-// Histogram increment aggregated over the wavefront: lanes with equal bins share one atomic.
-// Every lane of the wavefront must call it (the loop is wavefront-uniform).
-__device__ __forceinline__ void hist_add(uint32_t* hist, bool act, uint32_t bin) {
-    uint64_t todo = __ballot(act);
-    while (todo) {
-        const uint32_t leader = __builtin_ctzll(todo);
-        const uint32_t b = __shfl(bin, leader, 64);
-        const uint64_t same = __ballot(act && bin == b) & todo;
-        if (lane_id() == leader) atomicAdd(hist + b, static_cast<uint32_t>(__popcll(same)));
-        todo &= ~same;
-    }
-}
-
 __global__ __launch_bounds__(256) void k_evict_clear(uint32_t* work, uint64_t* n_evicted) {
-    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
-    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < 2 * kHistBins; i += stride)
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < 3 * kDigitBins; i += gridDim.x * blockDim.x)
         work[i] = 0;
     if (blockIdx.x == 0 && threadIdx.x == 0) {
-        EvictCtl* c = reinterpret_cast<EvictCtl*>(work + 2 * kHistBins);
+        EvictCtl* c = evict_ctl(work);
         c->cut = 0;
         c->above = 0;
-        c->h0 = 0;
+        c->live = 0;
+        c->prefix = 0;
         c->done = 0;
         *n_evicted = 0;
     }
 }
 
-// digit 0: high 16 bits of every live entry's epoch; digit 1: low 16 bits of the entries whose high
-// digit is h0.
-__global__ __launch_bounds__(256) void k_evict_hist(const uint64_t* tlocs, uint64_t capacity, const uint32_t* epochs,
-                                                    uint32_t* work, int digit) {
-    const EvictCtl* c = reinterpret_cast<const EvictCtl*>(work + 2 * kHistBins);
-    if (digit == 1 && c->done) return;
-    uint32_t* hist = work + digit * kHistBins;
-    const uint32_t h0 = c->h0;
+// Increment of an LDS histogram aggregated over the wavefront: lanes with equal bins share one
+// atomic.  Every lane of the wavefront must call it (the loop is wavefront-uniform).
+__device__ __forceinline__ void lds_hist_add(uint32_t* h, bool act, uint32_t bin) {
+    uint64_t todo = __ballot(act);
+    while (todo) {
+        const uint32_t leader = __builtin_ctzll(todo);
+        const uint32_t b = __shfl(bin, leader, 64);
+        const uint64_t same = __ballot(act && bin == b) & todo;
+        if (lane_id() == leader) atomicAdd(h + b, static_cast<uint32_t>(__popcll(same)));
+        todo &= ~same;
+    }
+}
+
+// Histogram of digit d over the live entries whose higher digits equal the selected prefix.
+__global__ __launch_bounds__(kHistThreads) void k_evict_hist(const uint64_t* tlocs, uint64_t capacity,
+                                                             const uint32_t* epochs, uint32_t* work, int d) {
+    __shared__ uint32_t h[kDigitBins];
+    const EvictCtl* c = evict_ctl(work);
+    if (c->done) return;                       // uniform: the control block is read-only here
+    const uint32_t prefix = c->prefix;
+    const int shift = digit_shift(d);
+    const uint32_t bins = digit_bins(d);
+    for (uint32_t i = threadIdx.x; i < kDigitBins; i += blockDim.x) h[i] = 0;
+    __syncthreads();
     const uint64_t waves = static_cast<uint64_t>(gridDim.x) * (blockDim.x / 64);
     const uint64_t wave = blockIdx.x * static_cast<uint64_t>(blockDim.x / 64) + (threadIdx.x >> 6);
     for (uint64_t base = wave * 64; base < capacity + 2; base += waves * 64) {
@@ -508,44 +523,54 @@ __global__ __launch_bounds__(256) void k_evict_hist(const uint64_t* tlocs, uint6
         uint32_t bin = 0;
         if (s < capacity + 2 && live_slot(s, tlocs[s], capacity)) {
             const uint32_t e = epochs[s];
-            act = digit == 0 || (e >> 16) == h0;
-            bin = digit == 0 ? (e >> 16) : (e & 0xFFFFu);
+            const uint32_t high = d == 0 ? 0u : (e >> (shift + (d == 1 ? 11 : 10)));
+            act = high == prefix;
+            bin = (e >> shift) & (bins - 1);
         }
-        hist_add(hist, act, bin);
+        lds_hist_add(h, act, bin);
     }
+    __syncthreads();
+    uint32_t* g = work + d * kDigitBins;
+    for (uint32_t i = threadIdx.x; i < bins; i += blockDim.x)
+        if (h[i]) atomicAdd(g + i, h[i]);
 }
 
-// One workgroup.  With G(b) = base + sum of hist[b'] over b' >= b, finds the largest b with
-// G(b) > budget (it exists whenever G(0) > budget).
-__global__ __launch_bounds__(kSelectThreads) void k_evict_select(uint32_t* work, uint64_t budget, int digit) {
+// One workgroup.  With G(b) = above + sum of hist[b'] over b' >= b, finds the largest b with
+// G(b) > budget (it exists whenever G(0) > budget) and extends the selected prefix by b.
+__global__ __launch_bounds__(kSelectThreads) void k_evict_select(uint32_t* work, uint64_t budget, int d,
+                                                                 uint64_t* n_evicted) {
     __shared__ uint64_t part[kSelectThreads];
     __shared__ uint32_t best;
     __shared__ uint64_t total;
-    EvictCtl* c = reinterpret_cast<EvictCtl*>(work + 2 * kHistBins);
-    if (digit == 1 && c->done) return;
-    const uint32_t* hist = work + digit * kHistBins;
+    EvictCtl* c = evict_ctl(work);
+    if (c->done) return;
+    const uint32_t* hist = work + d * kDigitBins;
+    const uint32_t bins = digit_bins(d);
+    const uint32_t per = bins / kSelectThreads;          // 2 or 1 bins per thread
     const uint32_t t = threadIdx.x;
-    constexpr uint32_t per = kHistBins / kSelectThreads;
     uint64_t mine = 0;
     for (uint32_t i = 0; i < per; ++i) mine += hist[t * per + i];
     part[t] = mine;
     if (t == 0) best = 0;          // raised by atomicMax; some thread always finds a bin when not done
     __syncthreads();
-    // exclusive suffix sum over threads: the live entries in bins above this thread's range
-    uint64_t above_t = digit == 0 ? 0 : c->above;
-    for (uint32_t u = t + 1; u < kSelectThreads; ++u) above_t += part[u];
-    if (t == 0) total = above_t + mine;
+    // inclusive suffix sum over threads (log steps): part[t] = sum over u >= t
+    for (uint32_t off = 1; off < kSelectThreads; off <<= 1) {
+        const uint64_t add = t + off < kSelectThreads ? part[t + off] : 0;
+        __syncthreads();
+        part[t] += add;
+        __syncthreads();
+    }
+    // the live entries in bins above this thread's range
+    const uint64_t above_t = c->above + part[t] - mine;
+    if (t == 0) total = c->above + part[0];
     __syncthreads();
-    if (digit == 0 && total <= budget) {          // everything fits: nothing to remove
-        if (t == 0) {
-            c->cut = 0;
-            c->done = 1;
-        }
+    if (d == 0 && t == 0) c->live = total;
+    if (d == 0 && total <= budget) {          // everything fits: nothing to remove
+        if (t == 0) c->done = 1;
         return;
     }
-    uint64_t acc = above_t;
+    uint64_t acc = above_t, before = 0;
     uint32_t found = 0xFFFFFFFFu;
-    uint64_t before = 0;
     for (int i = static_cast<int>(per) - 1; i >= 0; --i) {
         const uint64_t prev = acc;
         acc += hist[t * per + i];
@@ -554,40 +579,31 @@ __global__ __launch_bounds__(kSelectThreads) void k_evict_select(uint32_t* work,
     if (found != 0xFFFFFFFFu) atomicMax(&best, found);
     __syncthreads();
     if (found != 0xFFFFFFFFu && found == best) {
-        if (digit == 0) {
-            c->h0 = found;
-            c->above = before;                // G(h0 + 1)
+        const uint32_t prefix = (c->prefix << (d == 2 ? 10 : 11)) | found;
+        if (d < 2) {
+            c->prefix = prefix;
+            c->above = before;                    // entries above the selected bin
         } else {
-            c->cut = (static_cast<uint64_t>(c->h0) << 16) + found + 1;
+            c->cut = static_cast<uint64_t>(prefix) + 1;
             c->done = 1;
+            *n_evicted = c->live - before;        // every live entry below the cut
         }
     }
 }
 
 __global__ __launch_bounds__(256) void k_evict_apply(uint4* tkeys, uint64_t* tlocs, uint64_t capacity,
-                                                     const uint32_t* epochs, const uint32_t* work,
-                                                     uint64_t* n_evicted) {
-    const EvictCtl* c = reinterpret_cast<const EvictCtl*>(work + 2 * kHistBins);
-    const uint64_t cut = c->cut;
+                                                     const uint32_t* epochs, uint32_t* work) {
+    const uint64_t cut = evict_ctl(work)->cut;
     if (cut == 0) return;
-    const uint64_t waves = static_cast<uint64_t>(gridDim.x) * (blockDim.x / 64);
-    const uint64_t wave = blockIdx.x * static_cast<uint64_t>(blockDim.x / 64) + (threadIdx.x >> 6);
-    for (uint64_t base = wave * 64; base < capacity + 2; base += waves * 64) {
-        const uint64_t s = base + lane_id();
-        bool ev = false;
-        if (s < capacity + 2 && live_slot(s, tlocs[s], capacity) && epochs[s] < cut) {
-            ev = true;
-            if (s < capacity) {
-                tkeys[s] = make_uint4(~0u, ~0u, ~0u, kTombW);
-                tlocs[s] = kTomb;
-            } else {
-                tlocs[s] = kEmpty;
-            }
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+    for (uint64_t s = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; s < capacity + 2; s += stride) {
+        if (!live_slot(s, tlocs[s], capacity) || epochs[s] >= cut) continue;
+        if (s < capacity) {
+            tkeys[s] = make_uint4(~0u, ~0u, ~0u, kTombW);
+            tlocs[s] = kTomb;
+        } else {
+            tlocs[s] = kEmpty;
         }
-        const uint64_t mask = __ballot(ev);
-        if (mask && lane_id() == __builtin_ctzll(mask))
-            __hip_atomic_fetch_add(n_evicted, static_cast<uint64_t>(__popcll(mask)), __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -639,14 +655,14 @@ int launch_sum_hits(const int32_t* hits, uint32_t n_req, const int64_t* group_of
 
 int launch_evict(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint32_t* epochs, uint64_t budget,
                  uint32_t* work, uint64_t* n_evicted, hipStream_t s) {
-    const unsigned g = grid_for(capacity + 2, 256, 16384);
-    hipLaunchKernelGGL(k_evict_clear, dim3(grid_for(2 * kHistBins, 256, 512)), dim3(256), 0, s, work, n_evicted);
-    for (int digit = 0; digit < 2; ++digit) {
-        hipLaunchKernelGGL(k_evict_hist, dim3(g), dim3(256), 0, s, tlocs, capacity, epochs, work, digit);
-        hipLaunchKernelGGL(k_evict_select, dim3(1), dim3(kSelectThreads), 0, s, work, budget, digit);
+    const unsigned g = grid_for(capacity + 2, kHistThreads, kHistBlocks);
+    hipLaunchKernelGGL(k_evict_clear, dim3(8), dim3(256), 0, s, work, n_evicted);
+    for (int d = 0; d < 3; ++d) {
+        hipLaunchKernelGGL(k_evict_hist, dim3(g), dim3(kHistThreads), 0, s, tlocs, capacity, epochs, work, d);
+        hipLaunchKernelGGL(k_evict_select, dim3(1), dim3(kSelectThreads), 0, s, work, budget, d, n_evicted);
     }
-    hipLaunchKernelGGL(k_evict_apply, dim3(g), dim3(256), 0, s, reinterpret_cast<uint4*>(tkeys), tlocs, capacity,
-                       epochs, work, n_evicted);
+    hipLaunchKernelGGL(k_evict_apply, dim3(grid_for(capacity + 2, 256, 16384)), dim3(256), 0, s,
+                       reinterpret_cast<uint4*>(tkeys), tlocs, capacity, epochs, work);
     return check_launch("pkv_table_evict");
 }
 

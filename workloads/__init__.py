@@ -17,4 +17,5 @@ from .recipes import (  # noqa: F401
     OMISSION_CASES,
     make_omission,
     make_omission_tiny,
+    make_budget,
 )

@@ -437,5 +437,35 @@ def make_omission_tiny(seed=SEEDS["omission-tiny"]) -> OmissionCase:
 OMISSION_CASES = {"omission": make_omission, "omission-tiny": make_omission_tiny}
 
 
+# ---- fixed-budget tier inputs (section 6.5: retention against provenance diversity) -------------
+
+SEEDS["budget"] = 0x5EED0009
+
+
+def make_budget(classes=8, n_batches=8, seed=SEEDS["budget"], n_req=1024, length=2048, n_prefix=64):
+    """A stream of request batches for a fixed-budget tier: every batch has ``n_req`` requests of
+    ``length`` tokens, each one of ``n_prefix`` shared prefixes (512-1536 tokens, shared by all
+    batches) plus a fresh random suffix, under one of ``classes`` provenance classes (adapter
+    identities) drawn uniformly.  Returns (batches, capacity, budget): a 1M-slot index with a
+    budget of 2^18 entries."""
+    g_pre, g_req, g_desc, g_ord = _streams(seed, 4)
+    block, vocab = 16, 128256
+    pre_len = g_pre.integers(512, 1536, size=n_prefix, endpoint=True)
+    prefixes = [g_pre.integers(0, vocab, size=int(n), dtype=np.int32) for n in pre_len]
+    descs = [_shuffled([(b"model_id", b"synthetic-8b"), (b"adapter_id", b"lora-" + g_desc.bytes(6).hex().encode()),
+                        (b"weight_dtype", b"bfloat16"), (b"weight_version", _u64(3)), (b"kv_format", b"bfloat16"),
+                        (b"salt", b"tenant-shared")], g_ord) for _ in range(classes)]
+    batches = []
+    for t in range(n_batches):
+        pid = g_req.integers(0, n_prefix, size=n_req)
+        tok = g_req.integers(0, vocab, size=(n_req, length), dtype=np.int32)
+        for r in range(n_req):
+            tok[r, : pre_len[pid[r]]] = prefixes[pid[r]]
+        cls = g_req.integers(0, classes, size=n_req).astype(np.int32)
+        batches.append(Batch(tok.reshape(-1), np.arange(n_req + 1, dtype=np.int64) * length, block, descs, cls,
+                             TAG_STEP + 8 + t, {"prefix_blocks": _full_blocks(pre_len[pid], block)}))
+    return batches, 1 << 20, 1 << 18
+
+
 def make_workload(name: str, **kw) -> Workload:
     return WORKLOADS[name](**kw)
