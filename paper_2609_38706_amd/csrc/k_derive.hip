@@ -908,53 +908,94 @@ __global__ __launch_bounds__(64) void k_digest(const uint8_t* bytes, uint64_t n_
     reinterpret_cast<uint4*>(out)[i] = make_uint4(bswap(s[0]), bswap(s[1]), bswap(s[2]), bswap(s[3]));
 }
 
-// ---- key offsets: one workgroup scans floor(len / B) over all requests ------------------------
+// ---- key offsets: floor(len / B) scanned over the requests ------------------------------------
+// One workgroup scans a chunk of kScanChunk requests.  A batch of one chunk is done in one launch;
+// a larger batch scans every chunk locally (the last entry of each chunk then holds the chunk's
+// total), one workgroup turns the chunk ends into global prefix sums, and a last pass adds each
+// chunk's offset (the final value at its start) to the rest of the chunk.  The chunk ends double as
+// the scratch, so the call needs no memory beyond its output.
 constexpr int kScanThreads = 1024;
 constexpr int kScanPerThread = 8;
+constexpr uint32_t kScanChunk = kScanThreads * kScanPerThread;
 
+// Inclusive scan of per-thread sums across the workgroup: returns this thread's exclusive prefix;
+// *total receives the workgroup total.
+__device__ __forceinline__ int64_t block_exclusive(int64_t mine, int64_t* wave_sum, int64_t* total) {
+    const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int64_t incl = mine;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int64_t y = __shfl_up(incl, d, 64);
+        if (lane >= static_cast<uint32_t>(d)) incl += y;
+    }
+    if (lane == 63) wave_sum[wave] = incl;
+    __syncthreads();
+    int64_t wave_base = 0, t = 0;
+    for (uint32_t q = 0; q < kScanThreads / 64; ++q) {
+        if (q < wave) wave_base += wave_sum[q];
+        t += wave_sum[q];
+    }
+    *total = t;
+    return wave_base + incl - mine;
+}
+
+// Chunk blockIdx.x: key_off[r + 1] = sum of floor(len_q / B) over the chunk's requests q <= r.
 __global__ __launch_bounds__(kScanThreads) void k_key_offsets(const int64_t* tok_off, uint32_t n_req, uint32_t block,
                                                              int64_t* key_off) {
     __shared__ int64_t wave_sum[kScanThreads / 64];
-    __shared__ int64_t carry_sh;
-    const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    if (tid == 0) { carry_sh = 0; key_off[0] = 0; }
+    const uint32_t tid = threadIdx.x;
+    if (blockIdx.x == 0 && tid == 0) key_off[0] = 0;
+    const uint64_t base = static_cast<uint64_t>(blockIdx.x) * kScanChunk;
+    int64_t v[kScanPerThread];
+    int64_t mine = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPerThread; ++j) {
+        const uint64_t r = base + static_cast<uint64_t>(tid) * kScanPerThread + j;
+        int64_t c = 0;
+        if (r < n_req) c = (tok_off[r + 1] - tok_off[r]) / block;
+        v[j] = c;
+        mine += c;
+    }
+    int64_t total;
+    int64_t run = block_exclusive(mine, wave_sum, &total);
+#pragma unroll
+    for (int j = 0; j < kScanPerThread; ++j) {
+        const uint64_t r = base + static_cast<uint64_t>(tid) * kScanPerThread + j;
+        run += v[j];
+        if (r < n_req) key_off[r + 1] = run;
+    }
+}
+
+__device__ __forceinline__ uint64_t chunk_end(uint64_t c, uint32_t n_req) {
+    const uint64_t e = (c + 1) * kScanChunk;
+    return e < n_req ? e : n_req;
+}
+
+// One workgroup: the chunk totals at the chunk ends become global prefix sums.
+__global__ __launch_bounds__(kScanThreads) void k_key_offsets_carry(uint32_t n_req, int64_t* key_off) {
+    __shared__ int64_t wave_sum[kScanThreads / 64];
+    __shared__ int64_t carry;
+    const uint64_t n_chunks = (static_cast<uint64_t>(n_req) + kScanChunk - 1) / kScanChunk;
+    if (threadIdx.x == 0) carry = 0;
     __syncthreads();
-    for (uint64_t base = 0; base < n_req; base += static_cast<uint64_t>(kScanThreads) * kScanPerThread) {
-        int64_t v[kScanPerThread];
-        int64_t mine = 0;
-#pragma unroll
-        for (int j = 0; j < kScanPerThread; ++j) {
-            const uint64_t r = base + static_cast<uint64_t>(tid) * kScanPerThread + j;
-            int64_t c = 0;
-            if (r < n_req) c = (tok_off[r + 1] - tok_off[r]) / block;
-            v[j] = c;
-            mine += c;
-        }
-        // inclusive scan of `mine` across the wave
-        int64_t incl = mine;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int64_t y = __shfl_up(incl, d, 64);
-            if (lane >= static_cast<uint32_t>(d)) incl += y;
-        }
-        if (lane == 63) wave_sum[wave] = incl;
+    for (uint64_t t0 = 0; t0 < n_chunks; t0 += kScanThreads) {
+        const uint64_t c = t0 + threadIdx.x;
+        const int64_t mine = c < n_chunks ? key_off[chunk_end(c, n_req)] : 0;
+        int64_t total;
+        const int64_t ex = block_exclusive(mine, wave_sum, &total);
+        if (c < n_chunks) key_off[chunk_end(c, n_req)] = carry + ex + mine;
         __syncthreads();
-        int64_t wave_base = 0, total = 0;
-        for (uint32_t q = 0; q < kScanThreads / 64; ++q) {
-            if (q < wave) wave_base += wave_sum[q];
-            total += wave_sum[q];
-        }
-        int64_t run = carry_sh + wave_base + incl - mine;
-#pragma unroll
-        for (int j = 0; j < kScanPerThread; ++j) {
-            const uint64_t r = base + static_cast<uint64_t>(tid) * kScanPerThread + j;
-            run += v[j];
-            if (r < n_req) key_off[r + 1] = run;
-        }
-        __syncthreads();
-        if (tid == 0) carry_sh += total;
+        if (threadIdx.x == 0) carry += total;
         __syncthreads();
     }
+}
+
+// Chunk blockIdx.x + 1: adds the final value at its start to every entry but its (final) end.
+__global__ __launch_bounds__(256) void k_key_offsets_add(uint32_t n_req, int64_t* key_off) {
+    const uint64_t c = blockIdx.x + 1ull;
+    const uint64_t start = c * kScanChunk, end = chunk_end(c, n_req);
+    const int64_t off = key_off[start];
+    for (uint64_t i = start + 1 + threadIdx.x; i < end; i += blockDim.x) key_off[i] += off;
 }
 
 }  // namespace
@@ -1003,7 +1044,14 @@ int launch_digest_batch(const uint8_t* bytes, uint64_t n_bytes, const int64_t* o
 }
 
 int launch_key_offsets(const int64_t* tok_off, uint32_t n_req, uint32_t block, int64_t* key_off, hipStream_t s) {
-    hipLaunchKernelGGL(k_key_offsets, dim3(1), dim3(kScanThreads), 0, s, tok_off, n_req, block, key_off);
+    const uint64_t n_chunks = (static_cast<uint64_t>(n_req) + kScanChunk - 1) / kScanChunk;
+    hipLaunchKernelGGL(k_key_offsets, dim3(n_chunks ? static_cast<unsigned>(n_chunks) : 1u), dim3(kScanThreads), 0, s,
+                       tok_off, n_req, block, key_off);
+    if (n_chunks > 1) {
+        hipLaunchKernelGGL(k_key_offsets_carry, dim3(1), dim3(kScanThreads), 0, s, n_req, key_off);
+        hipLaunchKernelGGL(k_key_offsets_add, dim3(static_cast<unsigned>(n_chunks - 1)), dim3(256), 0, s, n_req,
+                           key_off);
+    }
     return check_launch("pkv_key_offsets");
 }
 

@@ -98,7 +98,7 @@ class OmissionRun:
             db.hits[: nb * n].zero_()
             self.n_new.zero_()
         pkv_store(self.table, db.keys, db.key_off[: nb * n + 1], db.hits[: nb * n], db.locs, self.n_new, db.status,
-                  None, stream)
+                  db.new_slots, stream)
         pkv_lookup_prefix(self.table, db.keys, db.key_off[nb * n:], db.hits[nb * n:], db.status, stream)
         pkv_sum_hits(db.hits[nb * n:], self.group_off, self.sums, db.status, stream)
 

@@ -452,3 +452,20 @@ def _sub_batch(batch, rows):
     off = np.zeros(len(rows) + 1, np.int64)
     off[1:] = np.cumsum([c.shape[0] for c in chunks])
     return Batch(np.concatenate(chunks), off, batch.block, batch.descs, batch.desc_idx[rows], batch.tag)
+
+
+@pytest.mark.parametrize("n_req", [1, 8191, 8192, 8193, 3 * 8192 + 5, 100000])
+def test_key_offsets_across_scan_chunks(pkv, n_req):
+    """The key-offset scan works in chunks of 8192 requests; sizes around and across chunk ends must
+    give the oracle's prefix sums of floor(len / B)."""
+    import torch
+    rng = np.random.default_rng(n_req)
+    lens = rng.integers(0, 80, size=n_req)
+    lens[rng.random(n_req) < 0.2] = 0
+    off = np.zeros(n_req + 1, np.int64)
+    off[1:] = np.cumsum(lens)
+    for block in (16, 7):
+        tok_off = torch.from_numpy(off).cuda()
+        key_off = torch.full((n_req + 1,), -5, dtype=torch.int64, device="cuda")
+        pkv.pkv_key_offsets(tok_off, block, key_off)
+        assert (key_off.cpu().numpy() == oracle.key_offsets(off, block)).all(), block
