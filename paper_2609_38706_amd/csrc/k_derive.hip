@@ -582,7 +582,8 @@ __device__ __forceinline__ void load_production(const int32_t* tp, uint32_t B, u
     }
 }
 
-__device__ __forceinline__ void produce_comp(PcmShared& sh, uint32_t lane, uint32_t m, uint32_t bitlen, int64_t g,
+template <typename Shared>
+__device__ __forceinline__ void produce_comp(Shared& sh, uint32_t lane, uint32_t m, uint32_t bitlen, int64_t g,
                                              const Production& pr) {
     const int64_t key = g / m;
     const uint32_t c = static_cast<uint32_t>(g - key * m) + 1;
@@ -721,6 +722,171 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pc(ChainArgs a) {
                 load_production(tp, B, m, n, g + 2, p1);
                 if (g < total) produce_comp(sh, lane, m, bitlen, g, p2);
                 __syncthreads();                               // end of token compression c
+            }
+        }
+    }
+}
+
+// ---- B = 16m (m >= 2), each chain on a lane pair (used while chains are very scarce) -----------
+// The consumer of k_derive_m16_pc with the lane-pair rounds of k_derive_b16_pp: compression 1 of a
+// key runs in four barrier phases while the helper's lane pairs compute its schedule; each of the
+// m token-only compressions reads its 64 K + W words from a ring of three LDS slots that one
+// helper lane per chain fills two compressions ahead.
+struct PpmShared {
+    uint4 kwt[3][16][kPpChains];      // K_t + W_t of token-only compressions, three slots
+    uint4 w1tok[2][2][kPpChains];     // W8..W15 of compression 1, two keys
+    uint4 kw1tok[2][2][kPpChains];    // K_t + W_t, t = 8..15 of compression 1, two keys
+    uint4 kw1hi[12][kPpChains];       // K_t + W_t, t = 16..63 of compression 1 (current key)
+    uint4 prev[kPpChains];            // previous key words
+};
+
+__global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
+    __shared__ PpmShared sh;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t c = lane >> 1;                  // chain of this lane pair
+    const bool odd = (lane & 1) != 0;
+    const uint32_t r = blockIdx.x * kPpChains + c;
+    const uint32_t B = a.block, m = B / 16;
+    const uint32_t bitlen = (32u + 4u * B) * 8u;
+    int64_t t0 = 0, k0 = 0, n = 0;
+    bool valid = r < a.n_req;
+    if (valid && !chain_bounds(a, r, t0, k0, n)) valid = false;
+    if (!valid) n = 0;
+    const int64_t nmax = wave_max(n);           // identical in both wavefronts
+    uint32_t dg[4] = {0u, 0u, 0u, 0u};
+    if (valid) load_digest(a, r, dg);
+
+    if (wave == 0) {
+        // ---------------- consumer: lane pair per chain ----------------
+        PairLane pl;
+        pl.m = odd ? ~0u : 0u;
+        pl.nm = ~pl.m;
+        pl.r1 = odd ? 2u : 6u;
+        pl.r2 = odd ? 13u : 11u;
+        pl.r3 = odd ? 22u : 25u;
+        uint32_t iv[4], dgk[4], kwp[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            iv[q] = odd ? kInitH[q] : kInitH[4 + q];
+            dgk[q] = dg[q] + kRoundK[4 + q];
+            kwp[q] = kRoundK[q];
+        }
+        if (odd) sh.prev[c] = make_uint4(0u, 0u, 0u, 0u);
+        __syncthreads();                                       // prologue
+        // K + W of a token compression stream through two 16-word register sets, each block read
+        // one block (16 rounds) ahead; the first block of compression g + 1 is read during the last
+        // block of compression g (production g + 1 was made during compression g - 1).
+        uint32_t kwa[16], kwb[16];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) get4(&sh.kwt[0][j][c], kwa + 4 * j);
+        for (int64_t i = 0; i < nmax; ++i) {
+            const int kb = static_cast<int>(i & 1);
+            uint32_t x[4], h[4], kw[16], q;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) { kw[j] = kwp[j]; kw[4 + j] = dgk[j]; }
+            get4(&sh.kw1tok[kb][0][c], kw + 8);
+            get4(&sh.kw1tok[kb][1][c], kw + 12);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) x[j] = iv[j];
+            q = (x[3] + kw[0]) & pl.nm;
+            pair_rounds16(x, q, pl, kw, 0u);                   // rounds 0..15
+            __syncthreads();
+#pragma unroll
+            for (int ph = 0; ph < 3; ++ph) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) get4(&sh.kw1hi[4 * ph + j][c], kw + 4 * j);
+                q = (x[3] + kw[0]) & pl.nm;
+                pair_rounds16(x, q, pl, kw, 0u);
+                if (ph < 2) __syncthreads();
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) h[j] = x[j] + iv[j];
+            __syncthreads();                                   // end of compression 1
+            for (uint32_t cc = 1; cc <= m; ++cc) {
+                const int64_t g = i * m + (cc - 1);            // produced two compressions ago
+                const int slot = static_cast<int>(g % 3), nslot = static_cast<int>((g + 1) % 3);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) x[j] = h[j];
+                q = (x[3] + kwa[0]) & pl.nm;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) get4(&sh.kwt[slot][4 + j][c], kwb + 4 * j);
+                pair_rounds16(x, q, pl, kwa, kwb[0]);          // rounds 0..15
+#pragma unroll
+                for (int j = 0; j < 4; ++j) get4(&sh.kwt[slot][8 + j][c], kwa + 4 * j);
+                pair_rounds16(x, q, pl, kwb, kwa[0]);          // rounds 16..31
+#pragma unroll
+                for (int j = 0; j < 4; ++j) get4(&sh.kwt[slot][12 + j][c], kwb + 4 * j);
+                pair_rounds16(x, q, pl, kwa, kwb[0]);          // rounds 32..47
+#pragma unroll
+                for (int j = 0; j < 4; ++j) get4(&sh.kwt[nslot][j][c], kwa + 4 * j);
+                pair_rounds16(x, q, pl, kwb, 0u);              // rounds 48..63
+#pragma unroll
+                for (int j = 0; j < 4; ++j) h[j] += x[j];
+                if (cc == m) {                                 // h on the odd lane is the key
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) kwp[j] = lane_swap(h[j]) + kRoundK[j];
+                    if (odd) {
+                        if (i < n)
+                            reinterpret_cast<uint4*>(a.keys)[k0 + i] =
+                                make_uint4(bswap(h[0]), bswap(h[1]), bswap(h[2]), bswap(h[3]));
+                        put4(&sh.prev[c], h);
+                    }
+                }
+                __syncthreads();                               // end of token compression cc
+            }
+        }
+    } else {
+        // ---------------- helper ----------------
+        const bool producer = lane < kPpChains;               // lanes 0..31 own chain `lane`
+        const uint32_t rp = blockIdx.x * kPpChains + lane;
+        int64_t pt0 = 0, pk0 = 0, pn = 0;
+        if (producer && rp < a.n_req && !chain_bounds(a, rp, pt0, pk0, pn)) pn = 0;
+        if (!(producer && rp < a.n_req)) pn = 0;
+        const int32_t* tp = a.tokens + pt0;
+        uint32_t dsel[2];
+        dsel[0] = odd ? dg[1] : dg[0];
+        dsel[1] = odd ? dg[3] : dg[2];
+        uint32_t* kw1hi_col = reinterpret_cast<uint32_t*>(&sh.kw1hi[0][c]) + (odd ? 1 : 0);
+        const int64_t total = nmax * m;                        // token compressions of the workgroup
+        Production p0, p1, p2;
+        if (producer) {
+            load_production(tp, B, m, pn, 0, p0);
+            load_production(tp, B, m, pn, 1, p1);
+            produce_comp(sh, lane, m, bitlen, 0, p0);
+            produce_comp(sh, lane, m, bitlen, 1, p1);
+            load_production(tp, B, m, pn, 2, p0);              // p0, p1 = productions g + 2, g + 3
+            load_production(tp, B, m, pn, 3, p1);
+        }
+        __syncthreads();                                       // prologue
+        for (int64_t i = 0; i < nmax; ++i) {
+            const int kb = static_cast<int>(i & 1);
+            uint32_t pv[4], tw[8], v[8];
+            get4(&sh.prev[c], pv);
+            get4(&sh.w1tok[kb][0][c], tw);
+            get4(&sh.w1tok[kb][1][c], tw + 4);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = odd ? tw[7 - 2 * k] : tw[6 - 2 * k];
+            v[4] = dsel[1];
+            v[5] = dsel[0];
+            v[6] = odd ? pv[3] : pv[2];
+            v[7] = odd ? pv[1] : pv[0];
+            pair_schedule8<8>(v, odd, kw1hi_col);
+            __syncthreads();
+            pair_schedule8<16>(v, odd, kw1hi_col);
+            __syncthreads();
+            pair_schedule8<24>(v, odd, kw1hi_col);
+            __syncthreads();
+            __syncthreads();                                   // end of compression 1
+            for (uint32_t cc = 1; cc <= m; ++cc) {
+                const int64_t g = i * m + (cc - 1) + 2;        // production made during compression (i, cc)
+                if (producer) {
+                    p2 = p0;
+                    p0 = p1;
+                    load_production(tp, B, m, pn, g + 2, p1);
+                    if (g < total) produce_comp(sh, lane, m, bitlen, g, p2);
+                }
+                __syncthreads();                               // end of token compression cc
             }
         }
     }
@@ -1026,6 +1192,8 @@ int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_o
         hipLaunchKernelGGL(k_derive_b16_pc, grid, dim3(kPcThreads), 0, s, a);
     } else if (block == 16) {
         hipLaunchKernelGGL(k_derive_b16, grid, dim3(kDeriveThreads), 0, s, a);
+    } else if (block % 16 == 0 && pp_grid <= static_cast<unsigned>(compute_units())) {
+        hipLaunchKernelGGL(k_derive_m16_pp, dim3(pp_grid), dim3(kPcThreads), 0, s, a);
     } else if (block % 16 == 0 && grid.x <= static_cast<unsigned>(compute_units())) {
         hipLaunchKernelGGL(k_derive_m16_pc, grid, dim3(kPcThreads), 0, s, a);
     } else if (block % 16 == 0) {

@@ -78,18 +78,19 @@ def test_ragged_with_empty_requests_in_between(pkv):
     assert [k.shape[0] for k in ks] == [n // 16 for n in lens]
 
 
-@pytest.mark.parametrize("n_req", [8192, 8193, 16384, 16385])
-def test_derive_kernels_agree_at_the_switches(pkv, n_req):
-    """8192 requests = 256 workgroups of 32 lane-pair chains (the last size of the lane-pair kernel);
-    8193..16384 run the two-wavefront kernel with one lane per chain; from 16385 on the
-    one-wavefront kernel.  Every kernel must give the oracle's keys."""
-    rng = np.random.default_rng(n_req)
-    lens = rng.integers(0, 64, size=n_req)
+@pytest.mark.parametrize("n_req,block", [(8192, 16), (8193, 16), (16384, 16), (16385, 16), (8192, 32), (8193, 32),
+                                         (16385, 48)])
+def test_derive_kernels_agree_at_the_switches(pkv, n_req, block):
+    """8192 requests = 256 workgroups of 32 lane-pair chains (the last size of the lane-pair kernels);
+    8193..16384 run the two-wavefront kernels with one lane per chain; from 16385 on the
+    one-wavefront kernels.  Every kernel, for B = 16 and for B = 16m, must give the oracle's keys."""
+    rng = np.random.default_rng(n_req + block)
+    lens = rng.integers(0, 4 * block, size=n_req)
     off = np.zeros(n_req + 1, np.int64)
     off[1:] = np.cumsum(lens)
     toks = rng.integers(0, 128256, size=int(off[-1]), dtype=np.int32)
     descs = [_with(BASE, b"salt", b"%d" % i) for i in range(7)]
-    b = Batch(toks, off, 16, descs, rng.integers(0, 7, size=n_req).astype(np.int32))
+    b = Batch(toks, off, block, descs, rng.integers(0, 7, size=n_req).astype(np.int32))
     db = gpu_batch(b)
     db.digest()
     db.derive()
