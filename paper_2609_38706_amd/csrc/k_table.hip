@@ -51,17 +51,17 @@ __global__ __launch_bounds__(256) void k_init(uint4* keys, uint64_t* locs, uint6
 }
 
 // ---- lookup: one wavefront per request --------------------------------------------------------
-// A request's keys are probed in windows of 64 x CHUNKS keys, one lane per key; a lane loads its
-// key's whole 64-byte bucket with four 16-byte loads issued together, and the next window's keys
-// are fetched while the current window's buckets are in flight.  A ballot over each 64-key chunk
-// finds the first absent key, which ends the request.  The first window is a single chunk; later
-// windows grow to LOOKUP_CHUNKS chunks.  Probes past the first miss are wasted bandwidth, traded
-// for fewer serial round trips per request.
-#ifndef PKV_LOOKUP_CHUNKS
-#define PKV_LOOKUP_CHUNKS 1
+// A request's keys are probed in windows, one lane per key; a lane loads its key's whole 64-byte
+// bucket with four 16-byte loads issued together, and the next window's keys are fetched while
+// the current window's buckets are in flight.  A ballot finds the first absent key, which ends the
+// request.  The first window holds LOOKUP_FIRST keys and each later window twice as many, up to
+// 64: probes past a request's first miss are wasted bandwidth, so short prefixes (and misses on
+// the first key) probe few keys, while long prefixes soon reach full 64-key windows.
+#ifndef PKV_LOOKUP_FIRST
+#define PKV_LOOKUP_FIRST 16
 #endif
 constexpr int kLookupWaves = 4;
-constexpr int kChunks = PKV_LOOKUP_CHUNKS;
+constexpr uint32_t kFirstWindow = PKV_LOOKUP_FIRST;
 
 // Probe of one key (lane-private): bucket slots already loaded in sl[0..3].  Returns the slot
 // holding the key, or -1 when it is absent; continues to later buckets while a full bucket
@@ -121,57 +121,33 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
         return;
     }
     int64_t base = 0;
-    int chunks = 1;
-    uint4 nk[kChunks];
-#pragma unroll
-    for (int c = 0; c < kChunks; ++c) nk[c] = key_at(base + 64 * c + lane, c < chunks);
+    uint32_t width = kFirstWindow;
+    uint4 nk = key_at(base + lane, lane < width);
     int64_t h = n;
     while (base < n) {
-        uint4 ck[kChunks], sl[kChunks][4];
-        bool v[kChunks];
-        uint64_t bk[kChunks];
+        const uint4 ck = nk;
+        const bool v = lane < width && base + lane < n;
+        const uint64_t bk = home_bucket(ck, bmask);
+        uint4 sl[4];
+        if (v) {
 #pragma unroll
-        for (int c = 0; c < kChunks; ++c) {
-            ck[c] = nk[c];
-            v[c] = c < chunks && base + 64 * c + lane < n;
-            bk[c] = home_bucket(ck[c], bmask);
-            if (v[c]) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) sl[c][j] = tkeys[bk[c] * kSlotsPerBucket + j];
-            }
+            for (int j = 0; j < 4; ++j) sl[j] = tkeys[bk * kSlotsPerBucket + j];
         }
-        // next window: twice as many chunks, up to kChunks
-        const int next_chunks = chunks * 2 < kChunks ? chunks * 2 : kChunks;
-        const int64_t next_base = base + 64 * chunks;
-#pragma unroll
-        for (int c = 0; c < kChunks; ++c) nk[c] = key_at(next_base + 64 * c + lane, c < next_chunks);
-        int64_t stop = -1;
-        int64_t fslot[kChunks];
-#pragma unroll
-        for (int c = 0; c < kChunks; ++c) fslot[c] = -1;
-#pragma unroll
-        for (int c = 0; c < kChunks; ++c) {
-            if (c >= chunks) break;
-            fslot[c] = v[c] ? probe_key(tkeys, tlocs, capacity, bmask, ck[c], bk[c], sl[c]) : -1;
-            const uint64_t miss = __ballot(v[c] && fslot[c] < 0);
-            if (miss) {
-                stop = base + 64 * c + __builtin_ctzll(miss);
-                break;
-            }
-        }
-        if (epochs) {                           // a touching lookup refreshes every hit key
-#pragma unroll
-            for (int c = 0; c < kChunks; ++c) {
-                const int64_t idx = base + 64 * c + lane;
-                if (c < chunks && fslot[c] >= 0 && (stop < 0 || idx < stop)) epochs[fslot[c]] = epoch;
-            }
-        }
+        // next window: twice as wide, up to the wavefront
+        const uint32_t next_width = width * 2 < 64 ? width * 2 : 64;
+        const int64_t next_base = base + width;
+        nk = key_at(next_base + lane, lane < next_width);
+        const int64_t fslot = v ? probe_key(tkeys, tlocs, capacity, bmask, ck, bk, sl) : -1;
+        const uint64_t miss = __ballot(v && fslot < 0);
+        const int64_t stop = miss ? base + __builtin_ctzll(miss) : -1;
+        if (epochs && fslot >= 0 && (stop < 0 || base + lane < stop))   // a touching lookup refreshes hits
+            epochs[fslot] = epoch;
         if (stop >= 0) {
             h = stop;
             break;
         }
         base = next_base;
-        chunks = next_chunks;
+        width = next_width;
     }
     if (lane == 0) hits[r] = static_cast<int32_t>(h < n ? h : n);
 }
