@@ -41,6 +41,10 @@ WORKLOAD_TEXT = {
     "c5": "256 req x 131072 tok, block 16, groups of 4 with uniform fork points, 4M-slot index",
     "omission": "differential omission test (Eq. 4): 512 req x 1024 tok, block 16, 20 registered dimensions, "
                 "22 bindings (complete, 20 leave-one-out, token-only) x (base + 20 one-dimension variants)",
+    "identity-adapter": "content identity of a LoRA adapter: 392 bfloat16 tensors (rank 8, 28 layers x 7 "
+                        "projections of a 7B-class model), 36.7 MB",
+    "identity-checkpoint": "content identity of a 0.5 B-parameter checkpoint: 290 bfloat16 tensors (24 layers, "
+                           "hidden 896, vocabulary 151936), 988 MB",
     "budget": "fixed-budget tier: stream of 1024 req x 2048 tok batches (64 shared prefixes, fresh suffixes), "
               "block 16, provenance classes drawn uniformly, 1M-slot index with a 2^18-entry budget; each step "
               "touching lookup, touching store, generational eviction",
@@ -270,6 +274,71 @@ def omission_leg(args):
             "omissions": int(res["omission"].sum())}
 
 
+def tree_compressions(nbytes):
+    """SHA-256 compressions of one tensor's tree (leaves of 1024 bytes with a prefix byte, nodes of up
+    to 16 digests with a prefix byte)."""
+    blocks = lambda m: (m + 9 + 63) // 64
+    if nbytes == 0:
+        return 1
+    full, last = divmod(nbytes, 1024)
+    counts = [1024] * full + ([last] if last else [])
+    total = sum(blocks(1 + c) for c in counts)
+    n = len(counts)
+    while n > 1:
+        groups = [min(16, n - i) for i in range(0, n, 16)]
+        total += sum(blocks(1 + 32 * k) for k in groups)
+        n = len(groups)
+    return total
+
+
+def identity_leg(args, kind):
+    import torch
+    from paper_2609_38706_amd.identity import TensorPool, content_identity
+    from workloads import identity_shapes
+    shapes = identity_shapes(kind)
+    g = torch.Generator(device="cuda").manual_seed(0x5EED000A)
+    tensors = [torch.randn(shape, generator=g, device="cuda").to(torch.bfloat16) for _, _, shape in shapes]
+    pool = TensorPool(tensors)
+    nbytes = sum(pool.nbytes)
+    comps = sum(tree_compressions(n) for n in pool.nbytes)
+    for _ in range(args.warmup):
+        pool.compute_roots()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for e in evs:
+        e[0].record()
+        pool.compute_roots()
+        e[1].record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    pool.host_roots()
+    t2 = time.perf_counter()
+    ident = content_identity([(n, t) for (n, _, _), t in zip(shapes, tensors)])
+    t3 = time.perf_counter()
+    return {"ms": (t1 - t0) * 1e3 / args.steps, "pass_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evs])),
+            "identity_ms": (t3 - t2) * 1e3, "nbytes": nbytes, "compressions": comps, "identity": ident.hex(),
+            "tensors": [(n, dt, sh, t) for (n, dt, sh), t in zip(shapes, tensors)]}
+
+
+def identity_cpu_leg(args, g, target_s=10.0):
+    """The oracle's identity of the same bytes, repeated until about `target_s` seconds."""
+    from oracle.identity import identity as oracle_identity
+    ts = [(n, dt, sh, t.contiguous().view(-1).view(__import__("torch").uint8).cpu().numpy().tobytes())
+          for n, dt, sh, t in g["tensors"]]
+    total, reps, ident = 0.0, 0, None
+    while total < target_s:
+        t0 = time.perf_counter()
+        ident = oracle_identity(ts)
+        total += time.perf_counter() - t0
+        reps += 1
+    if ident.hex() != g["identity"]:
+        raise RuntimeError("identity: GPU and oracle disagree")
+    return {"value": round(reps * g["nbytes"] / total / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{reps} identities of the same {g['nbytes'] / 1e6:.1f} MB (plain tree walk, one SHA-256 per "
+                      f"leaf and node, single thread); {total:.2f} s", "seconds": round(total, 3), "steps": reps}
+
+
 def budget_leg(args):
     """Steps of a fixed-budget tier over a cyclic stream of batches: derive, touching lookup,
     touching store, eviction to the budget.  Retention = hit blocks / prefix blocks requested."""
@@ -435,6 +504,28 @@ def main():
     torch.cuda.set_device(0)
     if args.calib_copy:
         calib_copy()
+        return
+    if args.workload.startswith("identity-"):
+        kind = args.workload.split("-", 1)[1]
+        log(args, "content identity", kind)
+        g = identity_leg(args, kind)
+        ops = g["compressions"] * OPS_PER_COMPRESSION
+        achieved = ops / (g["pass_ms"] * 1e-3)
+        cpu = None if args.no_cpu_baseline else identity_cpu_leg(args, g)
+        out = {
+            "metric": "content identity throughput (GB/s of tensor bytes); % of roofline",
+            "value": round(g["nbytes"] / (g["ms"] * 1e-3) / 1e9, 4), "unit": "GB/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(g["ms"], 4), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "u32", "data": "synthetic",
+            "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload, "bytes": g["nbytes"],
+                       "tensors": len(g["tensors"]), "parallelism": "1 GPU"},
+            "kernels_ms": {"roots": round(g["pass_ms"], 4), "identity_total_host": round(g["identity_ms"], 3)},
+            "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 4), "peak": round(INT_PEAK / 1e12, 4),
+                         "unit": "Tops/s", "frac": round(achieved / INT_PEAK, 5), "traffic": None,
+                         "kernel": "tree roots", "compressions": g["compressions"]},
+            "cpu_baseline": cpu,
+        }
+        print(json.dumps(out), flush=True)
         return
     if args.workload == "budget":
         log(args, "budget tier")

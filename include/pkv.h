@@ -201,6 +201,41 @@ int pkv_table_evict(const pkv_table* table, const uint32_t* d_epochs, uint64_t b
 int pkv_sum_hits(const int32_t* d_hit_blocks, uint32_t n_req, const int64_t* d_group_off, uint32_t n_groups,
                  uint64_t* d_sums, int32_t* d_status, hipStream_t stream);
 
+/* Content identity of an adapter or checkpoint (section 5.3: the adapter is bound by an identity
+ * of its contents, every tensor's name, dtype, shape and bytes with the meaningful configuration
+ * fields; section 6.5: its cost).  The paper fixes no hash; this library defines:
+ *   tensor root : Merkle tree over the tensor's bytes; leaves of 1024 bytes, leaf = SHA-256(0x00 |
+ *                 bytes) (an empty tensor has one empty leaf); node = SHA-256(0x01 | up to 16
+ *                 consecutive child digests); the first level with one digest holds the root;
+ *   record      : "PKVT" | u32(|name|) name | u32(|dtype|) dtype | u32(ndim) u64(dim)... |
+ *                 u64(byte length) | root                      (integers little-endian);
+ *   identity    : SHA-256("PKVA" | u32(#tensors) | records in name order | u32(#fields) |
+ *                 (u32(|key|) key u32(|value|) value)... in key order)       (32 bytes).
+ *
+ * pkv_tensor_roots (device): the roots of n_tensors tensors whose bytes lie in d_data (n_bytes, a
+ * multiple of 4, 4-byte aligned); tensor t occupies [d_tensor_off[t], d_tensor_off[t] +
+ * d_tensor_len[t]) (int64; every start a multiple of 4; tensors may leave gaps and may overlap).
+ * d_work: pkv_tree_work_bytes(n_bytes, n_tensors) bytes, 256-byte aligned; d_roots: n_tensors x 32
+ * bytes.  A tensor outside the data sets PKV_ELAYOUT.
+ * pkv_content_identity (host, pure): the identity from the tensors' metadata and roots;
+ * duplicate tensor names or configuration keys are PKV_EDUPDIM. */
+typedef struct {
+    const uint8_t* name;
+    uint32_t name_len;
+    const uint8_t* dtype;
+    uint32_t dtype_len;
+    const uint64_t* shape;
+    uint32_t ndim;
+    uint64_t nbytes;
+    const uint8_t* root;       /* 32 bytes */
+} pkv_tensor;
+uint64_t pkv_tree_work_bytes(uint64_t n_bytes, uint32_t n_tensors);
+int pkv_tensor_roots(const uint8_t* d_data, uint64_t n_bytes, const int64_t* d_tensor_off, const int64_t* d_tensor_len,
+                     uint32_t n_tensors, void* d_work, uint64_t work_bytes, uint8_t* d_roots, int32_t* d_status,
+                     hipStream_t stream);
+int pkv_content_identity(const pkv_tensor* tensors, uint32_t n_tensors, const pkv_field* config, size_t n_config,
+                         uint8_t out[32]);
+
 /* Text describing the last non-OK return on this thread. */
 const char* pkv_last_error(void);
 

@@ -20,7 +20,8 @@ ERROR_NAMES = {0: "PKV_OK", -1: "PKV_EINVAL", -2: "PKV_EDUPDIM", -3: "PKV_ERESER
 EXPORTED = ["pkv_descriptor_encode", "pkv_descriptor_digest", "pkv_digest_batch", "pkv_key_offsets",
             "pkv_derive_keys", "pkv_table_init", "pkv_lookup_prefix", "pkv_store", "pkv_table_rollback",
             "pkv_table_export", "pkv_sum_hits", "pkv_lookup_prefix_touch", "pkv_store_touch",
-            "pkv_table_evict", "pkv_last_error", "pkv_version"]
+            "pkv_table_evict", "pkv_tree_work_bytes", "pkv_tensor_roots", "pkv_content_identity",
+            "pkv_last_error", "pkv_version"]
 
 EVICT_WORK_BYTES = 3 * 2048 * 4 + 64   # PKV_EVICT_WORK_BYTES
 
@@ -66,11 +67,15 @@ def lib() -> ctypes.CDLL:
             "pkv_lookup_prefix_touch": [P, P, P, U32, U64, P, U32, P, P, P],
             "pkv_store_touch": [P, P, P, U32, U64, P, P, P, P, P, U32, P, P],
             "pkv_table_evict": [P, P, U64, P, P, P],
+            "pkv_tensor_roots": [P, U64, P, P, U32, P, U64, P, P, P],
+            "pkv_content_identity": [P, U32, P, ctypes.c_size_t, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
             f.argtypes = args
             f.restype = I32
+        L.pkv_tree_work_bytes.argtypes = [U64, U32]
+        L.pkv_tree_work_bytes.restype = U64
         L.pkv_last_error.restype = ctypes.c_char_p
         L.pkv_version.restype = ctypes.c_char_p
         _lib = L
@@ -239,6 +244,39 @@ def pkv_table_evict(table: Table, budget: int, n_evicted, stream=None):
     t = table.struct()
     _check(lib().pkv_table_evict(ctypes.byref(t), _ptr(table.epochs, torch.int32), budget,
                                  _ptr(table.work, torch.int64), _ptr(n_evicted, torch.int64), _stream(stream)))
+
+
+class pkv_tensor(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char_p), ("name_len", ctypes.c_uint32), ("dtype", ctypes.c_char_p),
+                ("dtype_len", ctypes.c_uint32), ("shape", ctypes.POINTER(ctypes.c_uint64)), ("ndim", ctypes.c_uint32),
+                ("nbytes", ctypes.c_uint64), ("root", ctypes.c_char_p)]
+
+
+def pkv_tree_work_bytes(n_bytes: int, n_tensors: int) -> int:
+    return int(lib().pkv_tree_work_bytes(n_bytes, n_tensors))
+
+
+def pkv_tensor_roots(data, tensor_off, tensor_len, work, roots, status, stream=None):
+    import torch
+    _check(lib().pkv_tensor_roots(_ptr(data, torch.uint8), data.numel(), _ptr(tensor_off, torch.int64),
+                                  _ptr(tensor_len, torch.int64), tensor_off.numel(), _ptr(work),
+                                  work.numel() * work.element_size(), _ptr(roots, torch.uint8),
+                                  _ptr(status, torch.int32), _stream(stream)))
+
+
+def pkv_content_identity(tensors, config=()) -> bytes:
+    """tensors: (name, dtype, shape, nbytes, root) tuples (bytes, bytes, ints, int, 32 bytes)."""
+    arr = (pkv_tensor * max(1, len(tensors)))()
+    keep = []
+    for i, (name, dtype, shape, nbytes, root) in enumerate(tensors):
+        name, dtype, root = bytes(name), bytes(dtype), bytes(root)
+        shp = (ctypes.c_uint64 * max(1, len(shape)))(*[int(d) for d in shape])
+        keep += [name, dtype, root, shp]
+        arr[i] = pkv_tensor(name, len(name), dtype, len(dtype), shp, len(shape), int(nbytes), root)
+    cfg, keep2 = _fields(config)
+    out = (ctypes.c_uint8 * 32)()
+    _check(lib().pkv_content_identity(arr, len(tensors), cfg, len(config), out))
+    return bytes(out)
 
 
 def pkv_sum_hits(hits, group_off, sums, status, stream=None):

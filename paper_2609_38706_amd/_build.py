@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_DIR = os.path.join(PKG, "lib")
 LIB_PATH = os.path.join(LIB_DIR, "libpkv.so")
-SOURCES = ["api.hip", "k_derive.hip", "k_table.hip"]
+SOURCES = ["api.hip", "k_derive.hip", "k_table.hip", "k_tree.hip"]
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",

@@ -97,7 +97,7 @@ void host_block(uint32_t st[8], const uint8_t* p) {
     for (int i = 0; i < 8; ++i) st[i] += v[i];
 }
 
-void host_digest16(const uint8_t* m, size_t len, uint8_t out[16]) {
+void host_sha256(const uint8_t* m, size_t len, uint8_t out[32]) {
     uint32_t st[8];
     std::memcpy(st, kInitH, sizeof st);
     size_t done = 0;
@@ -111,12 +111,30 @@ void host_digest16(const uint8_t* m, size_t len, uint8_t out[16]) {
     for (int i = 0; i < 8; ++i) tail[tl - 8 + i] = static_cast<uint8_t>(bits >> (56 - 8 * i));
     host_block(st, tail);
     if (tl == 128) host_block(st, tail + 64);
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 8; ++i) {
         out[4 * i] = static_cast<uint8_t>(st[i] >> 24);
         out[4 * i + 1] = static_cast<uint8_t>(st[i] >> 16);
         out[4 * i + 2] = static_cast<uint8_t>(st[i] >> 8);
         out[4 * i + 3] = static_cast<uint8_t>(st[i]);
     }
+}
+
+void host_digest16(const uint8_t* m, size_t len, uint8_t out[16]) {
+    uint8_t full[32];
+    host_sha256(m, len, full);
+    std::memcpy(out, full, 16);
+}
+
+void put64(std::vector<uint8_t>& v, uint64_t x) {
+    for (int i = 0; i < 8; ++i) v.push_back(static_cast<uint8_t>(x >> (8 * i)));
+}
+void put32v(std::vector<uint8_t>& v, uint32_t x) {
+    for (int i = 0; i < 4; ++i) v.push_back(static_cast<uint8_t>(x >> (8 * i)));
+}
+void put_bytes(std::vector<uint8_t>& v, const uint8_t* p, size_t n) { v.insert(v.end(), p, p + n); }
+
+bool bytes_less(const uint8_t* a, size_t na, const uint8_t* b, size_t nb) {
+    return std::lexicographical_compare(a, a + na, b, b + nb);
 }
 
 int check_table(const pkv_table* t, const char* what) {
@@ -316,6 +334,86 @@ int pkv_sum_hits(const int32_t* d_hit_blocks, uint32_t n_req, const int64_t* d_g
     if ((!d_hit_blocks && n_req) || !d_group_off || !d_sums || !d_status)
         return set_error(PKV_EINVAL, "pkv_sum_hits: null argument");
     return launch_sum_hits(d_hit_blocks, n_req, d_group_off, n_groups, d_sums, d_status, stream);
+}
+
+uint64_t pkv_tree_work_bytes(uint64_t n_bytes, uint32_t n_tensors) {
+    return n_tensors ? tree_layout(n_bytes, n_tensors).bytes : 0;
+}
+
+int pkv_tensor_roots(const uint8_t* d_data, uint64_t n_bytes, const int64_t* d_tensor_off, const int64_t* d_tensor_len,
+                     uint32_t n_tensors, void* d_work, uint64_t work_bytes, uint8_t* d_roots, int32_t* d_status,
+                     hipStream_t stream) {
+    if (n_tensors == 0) return PKV_OK;
+    if ((!d_data && n_bytes) || !d_tensor_off || !d_tensor_len || !d_work || !d_roots || !d_status)
+        return set_error(PKV_EINVAL, "pkv_tensor_roots: null argument");
+    if (n_bytes % 4 != 0 || !aligned(d_data, 4))
+        return set_error(PKV_EINVAL, "pkv_tensor_roots: data must be 4-byte aligned and a multiple of 4 bytes long");
+    if (!aligned(d_work, 256) || !aligned(d_roots, 16))
+        return set_error(PKV_EINVAL, "pkv_tensor_roots: work area must be 256-byte and roots 16-byte aligned");
+    if (work_bytes < tree_layout(n_bytes, n_tensors).bytes)
+        return set_error(PKV_EINVAL, "pkv_tensor_roots: work area smaller than pkv_tree_work_bytes()");
+    return launch_tensor_roots(d_data, n_bytes, d_tensor_off, d_tensor_len, n_tensors, static_cast<uint8_t*>(d_work),
+                               d_roots, d_status, stream);
+}
+
+int pkv_content_identity(const pkv_tensor* tensors, uint32_t n, const pkv_field* config, size_t n_config,
+                         uint8_t out[32]) {
+    if ((!tensors && n) || (!config && n_config) || !out) return set_error(PKV_EINVAL, "pkv_content_identity: null argument");
+    std::vector<uint32_t> order(n);
+    for (uint32_t i = 0; i < n; ++i) {
+        const pkv_tensor& t = tensors[i];
+        if ((!t.name && t.name_len) || (!t.dtype && t.dtype_len) || (!t.shape && t.ndim) || !t.root)
+            return set_error(PKV_EINVAL, "pkv_content_identity: tensor %u has a null field", i);
+        order[i] = i;
+    }
+    std::sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) {
+        return bytes_less(tensors[a].name, tensors[a].name_len, tensors[b].name, tensors[b].name_len);
+    });
+    for (uint32_t i = 1; i < n; ++i) {
+        const pkv_tensor& a = tensors[order[i - 1]];
+        const pkv_tensor& b = tensors[order[i]];
+        if (a.name_len == b.name_len && (a.name_len == 0 || std::memcmp(a.name, b.name, a.name_len) == 0))
+            return set_error(PKV_EDUPDIM, "pkv_content_identity: two tensors share a name");
+    }
+    std::vector<uint32_t> corder(n_config);
+    for (size_t i = 0; i < n_config; ++i) {
+        if ((!config[i].name && config[i].name_len) || (!config[i].value && config[i].value_len))
+            return set_error(PKV_EINVAL, "pkv_content_identity: configuration field %zu is null", i);
+        corder[i] = static_cast<uint32_t>(i);
+    }
+    std::sort(corder.begin(), corder.end(), [&](uint32_t a, uint32_t b) {
+        return bytes_less(config[a].name, config[a].name_len, config[b].name, config[b].name_len);
+    });
+    for (size_t i = 1; i < n_config; ++i) {
+        const pkv_field& a = config[corder[i - 1]];
+        const pkv_field& b = config[corder[i]];
+        if (a.name_len == b.name_len && (a.name_len == 0 || std::memcmp(a.name, b.name, a.name_len) == 0))
+            return set_error(PKV_EDUPDIM, "pkv_content_identity: two configuration fields share a name");
+    }
+    std::vector<uint8_t> m;
+    put_bytes(m, reinterpret_cast<const uint8_t*>("PKVA"), 4);
+    put32v(m, n);
+    for (uint32_t i : order) {
+        const pkv_tensor& t = tensors[i];
+        put_bytes(m, reinterpret_cast<const uint8_t*>("PKVT"), 4);
+        put32v(m, t.name_len);
+        put_bytes(m, t.name, t.name_len);
+        put32v(m, t.dtype_len);
+        put_bytes(m, t.dtype, t.dtype_len);
+        put32v(m, t.ndim);
+        for (uint32_t d = 0; d < t.ndim; ++d) put64(m, t.shape[d]);
+        put64(m, t.nbytes);
+        put_bytes(m, t.root, 32);
+    }
+    put32v(m, static_cast<uint32_t>(n_config));
+    for (uint32_t i : corder) {
+        put32v(m, config[i].name_len);
+        put_bytes(m, config[i].name, config[i].name_len);
+        put32v(m, config[i].value_len);
+        put_bytes(m, config[i].value, config[i].value_len);
+    }
+    host_sha256(m.data(), m.size(), out);
+    return PKV_OK;
 }
 
 }  // extern "C"

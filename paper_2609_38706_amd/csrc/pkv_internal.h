@@ -133,6 +133,16 @@ int launch_rollback(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const ui
                     const uint64_t* n_slots, uint64_t max_slots, hipStream_t s);
 int launch_sum_hits(const int32_t* hits, uint32_t n_req, const int64_t* group_off, uint32_t n_groups, uint64_t* sums,
                     int32_t* status, hipStream_t s);
+// Content-identity trees (k_tree.hip).
+struct TreeLayout {
+    uint32_t levels;
+    uint64_t bound[32];        // digests reserved per level
+    uint64_t digest_off[32];   // byte offset of each level's digests in the work area
+    uint64_t bytes;            // work-area size
+};
+TreeLayout tree_layout(uint64_t n_bytes, uint32_t n_tensors);
+int launch_tensor_roots(const uint8_t* data, uint64_t n_bytes, const int64_t* tensor_off, const int64_t* tensor_len,
+                        uint32_t n, uint8_t* work, uint8_t* roots, int32_t* status, hipStream_t s);
 int launch_export(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity, uint8_t* out_keys,
                   uint64_t* out_locs, uint64_t* count, hipStream_t s);
 

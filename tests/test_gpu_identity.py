@@ -1,0 +1,84 @@
+"""Content identities on the GPU (section 5.3; the tree hash defined in oracle/identity.py): tensor
+roots from the kernels must equal the oracle's for every leaf and fan-in edge, with tensors placed
+anywhere in one pool (gaps, shared bytes), and the identity of a set of torch tensors must equal
+the oracle's."""
+
+import numpy as np
+import pytest
+
+from oracle.identity import identity as oracle_identity
+from oracle.identity import tensor_root
+from tests.gpu_util import announce, gpu_available
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs an MI355X GPU")]
+
+SIZES = [0, 1, 3, 4, 1023, 1024, 1025, 16 * 1024, 16 * 1024 + 1, 17 * 1024 + 3, 256 * 1024, 256 * 1024 + 5,
+         300000, 5 * 1024 * 1024 + 7]
+
+
+@pytest.fixture(scope="module")
+def pkv():
+    import paper_2609_38706_amd as m
+    m.lib()
+    return m
+
+
+def test_roots_at_every_edge(pkv):
+    import torch
+    announce("tensor roots: 14 sizes in one pool with gaps and a shared range")
+    rng = np.random.default_rng(61)
+    datas = [rng.integers(0, 256, size=n, dtype=np.uint8).tobytes() for n in SIZES]
+    starts, pos = [], 0
+    for d in datas:
+        pos += int(rng.integers(0, 3)) * 4            # gaps between tensors
+        starts.append(pos)
+        pos += (len(d) + 3) // 4 * 4
+    pool = np.zeros(pos + 64, np.uint8)
+    for st, d in zip(starts, datas):
+        pool[st:st + len(d)] = np.frombuffer(d, np.uint8)
+    # one more tensor sharing the bytes of tensor 9
+    starts.append(starts[9])
+    datas.append(datas[9])
+    lens = [len(d) for d in datas]
+    dev = torch.from_numpy(pool).cuda()
+    off = torch.tensor(starts, dtype=torch.int64, device="cuda")
+    ln = torch.tensor(lens, dtype=torch.int64, device="cuda")
+    work = torch.empty((pkv.pkv_tree_work_bytes(dev.numel(), len(datas)) + 7) // 8, dtype=torch.int64, device="cuda")
+    roots = torch.empty((len(datas), 32), dtype=torch.uint8, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pkv.pkv_tensor_roots(dev, off, ln, work, roots, status)
+    got = [bytes(r) for r in roots.cpu().numpy()]
+    assert int(status.item()) == 0
+    assert got == [tensor_root(d) for d in datas]
+
+
+def test_misplaced_tensor_reports_elayout(pkv):
+    import torch
+    dev = torch.zeros(4096, dtype=torch.uint8, device="cuda")
+    work = torch.empty((pkv.pkv_tree_work_bytes(4096, 2) + 7) // 8, dtype=torch.int64, device="cuda")
+    roots = torch.empty((2, 32), dtype=torch.uint8, device="cuda")
+    for off, ln in [([0, 2], [10, 10]), ([0, 4000], [10, 100])]:        # unaligned start; past the end
+        status = torch.zeros(1, dtype=torch.int32, device="cuda")
+        pkv.pkv_tensor_roots(dev, torch.tensor(off, dtype=torch.int64, device="cuda"),
+                             torch.tensor(ln, dtype=torch.int64, device="cuda"), work, roots, status)
+        assert int(status.item()) == pkv.PKV_ELAYOUT
+
+
+def test_identity_of_torch_tensors_matches_oracle(pkv):
+    import torch
+    from paper_2609_38706_amd.identity import content_identity
+    g = torch.Generator(device="cpu").manual_seed(62)
+    tensors = [
+        (b"base_model.layers.0.q.lora_A", torch.randn(8, 896, generator=g).to(torch.bfloat16)),
+        (b"base_model.layers.0.q.lora_B", torch.randn(896, 8, generator=g).to(torch.bfloat16)),
+        (b"base_model.layers.0.mlp.scale", torch.randn(3, generator=g)),              # 12 bytes
+        (b"base_model.layers.0.mlp.idx", torch.randint(-128, 127, (7,), generator=g, dtype=torch.int8)),
+        (b"empty", torch.zeros(0)),
+    ]
+    config = [(b"r", b"8"), (b"lora_alpha", b"16"), (b"target_modules", b"q,v")]
+    got = content_identity([(n, t.cuda()) for n, t in tensors], config)
+    want = oracle_identity([(n, str(t.dtype).replace("torch.", "").encode(), tuple(t.shape),
+                             t.contiguous().reshape(-1).view(torch.uint8).numpy().tobytes()) for n, t in tensors],
+                           config)
+    assert got == want

@@ -28,12 +28,12 @@ def built():
 
 def declared_functions():
     text = open(os.path.join(ROOT, "include", "pkv.h")).read()
-    return sorted(set(re.findall(r"^(?:int|const char\*)\s+(pkv_\w+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^(?:int|uint64_t|const char\*)\s+(pkv_\w+)\s*\(", text, re.M)))
 
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 19
     lib = pkv.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -120,3 +120,18 @@ def test_null_arguments_rejected_on_host():
     assert L.pkv_lookup_prefix(ctypes.byref(t), None, 0x2000, 3, 5, 0x3000, 0x4000, None) == pkv.PKV_EINVAL
     assert L.pkv_store(ctypes.byref(t), 0x1000, 0x2000, 3, 5, 0x3000, 0x4000, None, None, 0x5000, None) == pkv.PKV_EINVAL
     assert L.pkv_digest_batch(0x1000, 10, None, 0x2000, 3, 0x3000, 0x4000, None) == pkv.PKV_EINVAL
+
+
+def test_host_content_identity_matches_oracle():
+    from oracle.identity import identity as oracle_identity
+    from oracle.identity import tensor_root
+    rng = np.random.default_rng(9)
+    ts = [(b"w%d" % i, b"float32", (i + 1, 3), rng.integers(0, 256, size=12 * (i + 1), dtype=np.uint8).tobytes())
+          for i in range(4)]
+    recs = [(n, dt, sh, len(d), tensor_root(d)) for n, dt, sh, d in ts]
+    cfg = [(b"b", b"2"), (b"a", b"1")]
+    assert pkv.pkv_content_identity(list(reversed(recs)), cfg) == oracle_identity(ts, cfg)
+    with pytest.raises(pkv.PkvError):
+        pkv.pkv_content_identity(recs + recs[:1], cfg)
+    with pytest.raises(pkv.PkvError):
+        pkv.pkv_content_identity(recs, cfg + cfg[:1])

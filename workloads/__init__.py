@@ -18,4 +18,5 @@ from .recipes import (  # noqa: F401
     make_omission,
     make_omission_tiny,
     make_budget,
+    identity_shapes,
 )

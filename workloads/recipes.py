@@ -469,3 +469,38 @@ def make_budget(classes=8, n_batches=8, seed=SEEDS["budget"], n_req=1024, length
 
 def make_workload(name: str, **kw) -> Workload:
     return WORKLOADS[name](**kw)
+
+
+# ---- content identities (section 5.3 adapter identity from contents; section 6.5 startup costs) ----
+
+def identity_shapes(kind="adapter"):
+    """Tensor names, dtypes and shapes of the two objects section 6.5 times: a LoRA adapter of about
+    40 MB (rank 8 on the seven projections of 28 layers of a 7B-class model, bfloat16) and a
+    checkpoint of about 0.5 B parameters (24 layers, hidden 896, MLP 4864, vocabulary 151936,
+    bfloat16).  Only shapes: the bytes are drawn from a seeded generator by the caller."""
+    out = []
+    if kind == "adapter":
+        h, f, r = 4096, 14336, 8
+        mods = {"q_proj": (h, h), "k_proj": (h, 1024), "v_proj": (h, 1024), "o_proj": (h, h),
+                "gate_proj": (h, f), "up_proj": (h, f), "down_proj": (f, h)}
+        for layer in range(28):
+            for m, (din, dout) in mods.items():
+                base = f"base_model.model.layers.{layer}.{m}"
+                out.append((f"{base}.lora_A.weight".encode(), b"bfloat16", (r, din)))
+                out.append((f"{base}.lora_B.weight".encode(), b"bfloat16", (dout, r)))
+    elif kind == "checkpoint":
+        h, f, v, kvd = 896, 4864, 151936, 128
+        out.append((b"model.embed_tokens.weight", b"bfloat16", (v, h)))
+        for layer in range(24):
+            base = f"model.layers.{layer}"
+            for name, shape in [("self_attn.q_proj.weight", (h, h)), ("self_attn.q_proj.bias", (h,)),
+                                ("self_attn.k_proj.weight", (kvd, h)), ("self_attn.k_proj.bias", (kvd,)),
+                                ("self_attn.v_proj.weight", (kvd, h)), ("self_attn.v_proj.bias", (kvd,)),
+                                ("self_attn.o_proj.weight", (h, h)), ("mlp.gate_proj.weight", (f, h)),
+                                ("mlp.up_proj.weight", (f, h)), ("mlp.down_proj.weight", (h, f)),
+                                ("input_layernorm.weight", (h,)), ("post_attention_layernorm.weight", (h,))]:
+                out.append((f"{base}.{name}".encode(), b"bfloat16", shape))
+        out.append((b"model.norm.weight", b"bfloat16", (h,)))
+    else:
+        raise ValueError(kind)
+    return out
