@@ -5,9 +5,13 @@
 // Tree of one tensor: leaves of 1024 bytes, leaf = SHA-256(0x00 | bytes); a node is
 // SHA-256(0x01 | up to 16 consecutive child digests); the first level with a single digest holds
 // the root (an empty tensor has one empty leaf).  All tensors are hashed together: level 0 has one
-// lane per leaf of every tensor, each further level one lane per node.  Per level, a
-// one-workgroup scan turns the tensors' node counts into offsets (CSR); a tensor whose tree is
+// lane per leaf of every tensor, each further level one lane per node.  One workgroup first
+// turns the tensors' node counts at every level into offsets (CSR); a tensor whose tree is
 // already a single digest carries it up unchanged.
+//
+// Data that starts 16-byte aligned and is a whole number of 16-byte units (every full leaf of an
+// aligned tensor; every node, since the work area is 256-byte aligned) is read with 16-byte loads,
+// the next block while the current one compresses; other leaves take the byte-exact path.
 //
 // Work area (see tree_layout): the CSR of every level, then the digests of every level.
 #include "pkv_internal.h"
@@ -59,6 +63,72 @@ __device__ __forceinline__ void hash_prefixed(uint32_t prefix, const uint32_t* p
     }
 }
 
+__device__ __forceinline__ void load_units(const uint4* p, uint32_t n16, uint32_t u0, uint4 v[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t u = u0 + i;
+        v[i] = p[u < n16 ? u : n16 - 1];                              // n16 > 0: clamped to the data
+    }
+}
+
+// SHA-256(prefix | data[0 .. 16 n16)) for 16-byte-aligned data.  The stream of big-endian data words
+// is followed by the padding word 0x80000000 and zeros; message word q takes the last byte of stream
+// word q - 1 (the prefix for q = 0) and the first three of stream word q.  Blocks made only of data
+// words skip the padding selects; at most two blocks follow them (the rest of the data, the padding,
+// the length), and every data unit they hold is already loaded when the loop over full blocks ends.
+__device__ __forceinline__ void hash_prefixed16(uint32_t prefix, const uint4* p, uint32_t n16, uint32_t s[8]) {
+    const uint64_t msg = 1ull + 16ull * n16;
+    const uint32_t n_full = n16 / 4;
+    const uint32_t n_blocks = static_cast<uint32_t>((msg + 9 + 63) / 64);
+    init_state(s);
+    uint32_t carry = prefix;
+    uint4 cur[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) cur[i] = make_uint4(0u, 0u, 0u, 0u);
+    if (n16 > 0) load_units(p, n16, 0, cur);
+    for (uint32_t c = 0; c < n_full; ++c) {
+        uint32_t w[16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t raw[4] = {cur[i].x, cur[i].y, cur[i].z, cur[i].w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t be = bswap(raw[k]);
+                w[4 * i + k] = __builtin_amdgcn_alignbit(carry, be, 8);
+                carry = be;
+            }
+        }
+        load_units(p, n16, 4 * (c + 1), cur);
+        __builtin_amdgcn_sched_barrier(0);                            // the loads stay ahead of the rounds
+        compress(s, w);
+    }
+    for (uint32_t c = n_full; c < n_blocks; ++c) {
+        uint32_t w[16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t u = 4 * c + i;
+            const bool in = u < n16;
+            const uint32_t raw[4] = {cur[i].x, cur[i].y, cur[i].z, cur[i].w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t pad = (k == 0 && u == n16) ? 0x80000000u : 0u;
+                const uint32_t be = in ? bswap(raw[k]) : pad;
+                w[4 * i + k] = __builtin_amdgcn_alignbit(carry, be, 8);
+                carry = be;
+            }
+        }
+        if (c + 1 == n_blocks) {
+            w[14] = static_cast<uint32_t>((msg * 8) >> 32);
+            w[15] = static_cast<uint32_t>(msg * 8);
+        }
+        compress(s, w);
+    }
+}
+
+__device__ __forceinline__ bool aligned16(const void* p, uint64_t len) {
+    return ((reinterpret_cast<uintptr_t>(p) | len) & 15) == 0;
+}
+
 __device__ __forceinline__ void store_digest(uint8_t* d, uint64_t i, const uint32_t s[8]) {
     uint4* o = reinterpret_cast<uint4*>(d + 32 * i);
     o[0] = make_uint4(bswap(s[0]), bswap(s[1]), bswap(s[2]), bswap(s[3]));
@@ -75,49 +145,63 @@ __device__ __forceinline__ uint32_t owner(const int64_t* csr, uint32_t n, int64_
     return lo;
 }
 
-// One workgroup: csr[t] = sum of count(t') over t' < t.  Level 0: count = leaves of tensor t
-// (its offsets are validated: a bad tensor counts one leaf and reports PKV_ELAYOUT); level > 0:
-// count = ceil(nodes of the level below / 16).
+constexpr uint32_t kStagedCsr = 1024;                                 // CSR entries staged in LDS (8 KB)
+
+// Tensor owning item i of a level, or n when i lies past the level.  When the level's CSR fits, it
+// is staged in LDS first, so the search reads LDS instead of making dependent global loads.  Every
+// lane of the workgroup must call it (the staging ends in a barrier).
+__device__ __forceinline__ uint32_t find_owner(const int64_t* csr, uint32_t n, int64_t i, int64_t* lcsr) {
+    if (n + 1 <= kStagedCsr) {
+        for (uint32_t k = threadIdx.x; k <= n; k += blockDim.x) lcsr[k] = csr[k];
+        __syncthreads();
+        return i >= lcsr[n] ? n : owner(lcsr, n, i);
+    }
+    return i >= csr[n] ? n : owner(csr, n, i);
+}
+
+// One workgroup: the CSR of every level, csr_l[t] = sum over t' < t of the nodes of tensor t' at
+// level l.  Level 0 counts the leaves of each tensor (its start and length are validated: a bad
+// tensor counts one leaf and reports PKV_ELAYOUT); level l + 1 counts ceil(level l / 16).
 __global__ __launch_bounds__(kCsrThreads) void k_tree_csr(const int64_t* tensor_off, const int64_t* tensor_len,
-                                                          uint64_t n_bytes, uint32_t n, const int64_t* below,
+                                                          uint64_t n_bytes, uint32_t n, uint32_t levels,
                                                           int64_t* csr, int32_t* status) {
     __shared__ int64_t wave_sum[kCsrThreads / 64];
     __shared__ int64_t carry;
     const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    if (tid == 0) { carry = 0; csr[0] = 0; }
-    __syncthreads();
-    for (uint32_t base = 0; base < n; base += kCsrThreads) {
-        const uint32_t t = base + tid;
-        int64_t cnt = 0;
-        if (t < n) {
-            if (below == nullptr) {
-                const int64_t a = tensor_off[t], l = tensor_len[t];
-                const bool ok = a >= 0 && l >= 0 && static_cast<uint64_t>(a) <= n_bytes &&
-                                static_cast<uint64_t>(l) <= n_bytes - static_cast<uint64_t>(a) && (a & 3) == 0;
-                if (!ok) dev::report(status, PKV_ELAYOUT);
-                const int64_t len = ok ? l : 0;
-                cnt = len == 0 ? 1 : (len + kLeafBytes - 1) / kLeafBytes;
-            } else {
-                cnt = (below[t + 1] - below[t] + kFanIn - 1) / kFanIn;
+    for (uint32_t l = 0; l < levels; ++l) {
+        int64_t* out = csr + static_cast<uint64_t>(l) * (n + 1ull);
+        if (tid == 0) { carry = 0; out[0] = 0; }
+        __syncthreads();
+        for (uint32_t base = 0; base < n; base += kCsrThreads) {
+            const uint32_t t = base + tid;
+            int64_t cnt = 0;
+            if (t < n) {
+                const int64_t a = tensor_off[t], len = tensor_len[t];
+                const bool ok = a >= 0 && len >= 0 && static_cast<uint64_t>(a) <= n_bytes &&
+                                static_cast<uint64_t>(len) <= n_bytes - static_cast<uint64_t>(a) && (a & 3) == 0;
+                if (!ok && l == 0) dev::report(status, PKV_ELAYOUT);
+                const int64_t bytes = ok ? len : 0;
+                cnt = bytes == 0 ? 1 : (bytes + kLeafBytes - 1) / kLeafBytes;
+                for (uint32_t k = 0; k < l; ++k) cnt = (cnt + kFanIn - 1) / kFanIn;
             }
-        }
-        int64_t incl = cnt;
+            int64_t incl = cnt;
 #pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int64_t y = __shfl_up(incl, d, 64);
-            if (lane >= static_cast<uint32_t>(d)) incl += y;
+            for (int d = 1; d < 64; d <<= 1) {
+                const int64_t y = __shfl_up(incl, d, 64);
+                if (lane >= static_cast<uint32_t>(d)) incl += y;
+            }
+            if (lane == 63) wave_sum[wave] = incl;
+            __syncthreads();
+            int64_t wave_base = 0, total = 0;
+            for (uint32_t q = 0; q < kCsrThreads / 64; ++q) {
+                if (q < wave) wave_base += wave_sum[q];
+                total += wave_sum[q];
+            }
+            if (t < n) out[t + 1] = carry + wave_base + incl;
+            __syncthreads();
+            if (tid == 0) carry += total;
+            __syncthreads();
         }
-        if (lane == 63) wave_sum[wave] = incl;
-        __syncthreads();
-        int64_t wave_base = 0, total = 0;
-        for (uint32_t q = 0; q < kCsrThreads / 64; ++q) {
-            if (q < wave) wave_base += wave_sum[q];
-            total += wave_sum[q];
-        }
-        if (t < n) csr[t + 1] = carry + wave_base + incl;
-        __syncthreads();
-        if (tid == 0) carry += total;
-        __syncthreads();
     }
 }
 
@@ -125,9 +209,10 @@ __global__ __launch_bounds__(kCsrThreads) void k_tree_csr(const int64_t* tensor_
 __global__ __launch_bounds__(64) void k_tree_leaves(const uint8_t* data, uint64_t n_bytes, const int64_t* tensor_off,
                                                     const int64_t* tensor_len, uint32_t n, const int64_t* csr,
                                                     uint8_t* out) {
+    __shared__ int64_t lcsr[kStagedCsr];
     const int64_t i = blockIdx.x * 64ll + threadIdx.x;
-    if (i >= csr[n]) return;
-    const uint32_t t = owner(csr, n, i);
+    const uint32_t t = find_owner(csr, n, i, lcsr);
+    if (t == n) return;
     const int64_t a = tensor_off[t], l = tensor_len[t];
     if (a < 0 || l < 0 || static_cast<uint64_t>(a) > n_bytes || static_cast<uint64_t>(l) > n_bytes - a || (a & 3) != 0)
         return;                                                       // reported by k_tree_csr
@@ -137,16 +222,20 @@ __global__ __launch_bounds__(64) void k_tree_leaves(const uint8_t* data, uint64_
     const int64_t rem = b - start;
     const uint32_t len = rem <= 0 ? 0u : (rem < kLeafBytes ? static_cast<uint32_t>(rem) : kLeafBytes);
     uint32_t s[8];
-    hash_prefixed(0x00u, reinterpret_cast<const uint32_t*>(data + start), len, s);
+    if (aligned16(data + start, len))
+        hash_prefixed16(0x00u, reinterpret_cast<const uint4*>(data + start), len / 16, s);
+    else
+        hash_prefixed(0x00u, reinterpret_cast<const uint32_t*>(data + start), len, s);
     store_digest(out, i, s);
 }
 
 // Level l > 0: one lane per node; children are the level below's digests of the same tensor.
 __global__ __launch_bounds__(64) void k_tree_nodes(uint32_t n, const int64_t* csr_below, const int64_t* csr,
                                                    const uint8_t* below, uint8_t* out) {
+    __shared__ int64_t lcsr[kStagedCsr];
     const int64_t i = blockIdx.x * 64ll + threadIdx.x;
-    if (i >= csr[n]) return;
-    const uint32_t t = owner(csr, n, i);
+    const uint32_t t = find_owner(csr, n, i, lcsr);
+    if (t == n) return;
     const int64_t j = i - csr[t];
     const int64_t c0 = csr_below[t] + kFanIn * j;
     const int64_t end = csr_below[t + 1];
@@ -158,8 +247,8 @@ __global__ __launch_bounds__(64) void k_tree_nodes(uint32_t n, const int64_t* cs
         dst[1] = src[1];
         return;
     }
-    uint32_t s[8];
-    hash_prefixed(0x01u, reinterpret_cast<const uint32_t*>(below + 32 * c0), static_cast<uint32_t>(32 * (c1 - c0)), s);
+    uint32_t s[8];                                                    // digests are 32-byte aligned
+    hash_prefixed16(0x01u, reinterpret_cast<const uint4*>(below + 32 * c0), static_cast<uint32_t>(2 * (c1 - c0)), s);
     store_digest(out, i, s);
 }
 
@@ -199,13 +288,11 @@ int launch_tensor_roots(const uint8_t* data, uint64_t n_bytes, const int64_t* te
     const TreeLayout L = tree_layout(n_bytes, n);
     int64_t* csr = reinterpret_cast<int64_t*>(work);
     auto csr_of = [&](uint32_t l) { return csr + static_cast<uint64_t>(l) * (n + 1ull); };
-    hipLaunchKernelGGL(k_tree_csr, dim3(1), dim3(kCsrThreads), 0, s, tensor_off, tensor_len, n_bytes, n,
-                       static_cast<const int64_t*>(nullptr), csr_of(0), status);
+    hipLaunchKernelGGL(k_tree_csr, dim3(1), dim3(kCsrThreads), 0, s, tensor_off, tensor_len, n_bytes, n, L.levels,
+                       csr, status);
     hipLaunchKernelGGL(k_tree_leaves, dim3(static_cast<unsigned>((L.bound[0] + 63) / 64)), dim3(64), 0, s, data,
                        n_bytes, tensor_off, tensor_len, n, csr_of(0), work + L.digest_off[0]);
     for (uint32_t l = 1; l < L.levels; ++l) {
-        hipLaunchKernelGGL(k_tree_csr, dim3(1), dim3(kCsrThreads), 0, s, tensor_off, tensor_len, n_bytes, n,
-                           csr_of(l - 1), csr_of(l), status);
         hipLaunchKernelGGL(k_tree_nodes, dim3(static_cast<unsigned>((L.bound[l] + 63) / 64)), dim3(64), 0, s, n,
                            csr_of(l - 1), csr_of(l), work + L.digest_off[l - 1], work + L.digest_off[l]);
     }

@@ -20,7 +20,7 @@ class TensorPool:
             starts.append(pos)
             lens.append(b.numel())
             parts.append(b)
-            pad = (-b.numel()) % 4
+            pad = (-b.numel()) % 256                                 # 256-byte aligned starts
             if pad:
                 parts.append(torch.zeros(pad, dtype=torch.uint8, device=device))
             pos += b.numel() + pad

@@ -53,6 +53,63 @@ def test_roots_at_every_edge(pkv):
     assert got == [tensor_root(d) for d in datas]
 
 
+# Sizes whose leaves take the 16-byte path when their start is 16-byte aligned: tails of a multiple
+# of 16 bytes and not, and 1..17, 31..33, 255..257 leaves, so the first node level holds every
+# child count from 1 to 16.
+ALIGNED_SIZES = [16, 48, 1008, 1024 + 16, 1024 + 20] + [k * 1024 for k in range(1, 18)] + \
+    [31 * 1024, 32 * 1024 + 32, 33 * 1024 + 1, 255 * 1024, 256 * 1024, 257 * 1024 + 496]
+
+
+def test_roots_of_aligned_tensors(pkv):
+    import torch
+    announce(f"tensor roots: {len(ALIGNED_SIZES)} sizes, starts 16-byte aligned or 4 mod 16")
+    rng = np.random.default_rng(63)
+    datas = [rng.integers(0, 256, size=n, dtype=np.uint8).tobytes() for n in ALIGNED_SIZES]
+    starts, pos = [], 0
+    for i, d in enumerate(datas):
+        pos = (pos + 15) // 16 * 16 + (4 if i % 5 == 4 else 0)      # every fifth start is 4 mod 16
+        starts.append(pos)
+        pos += (len(d) + 3) // 4 * 4
+    pool = np.zeros(pos + 64, np.uint8)
+    for st, d in zip(starts, datas):
+        pool[st:st + len(d)] = np.frombuffer(d, np.uint8)
+    dev = torch.from_numpy(pool).cuda()
+    off = torch.tensor(starts, dtype=torch.int64, device="cuda")
+    ln = torch.tensor([len(d) for d in datas], dtype=torch.int64, device="cuda")
+    work = torch.empty((pkv.pkv_tree_work_bytes(dev.numel(), len(datas)) + 7) // 8, dtype=torch.int64, device="cuda")
+    roots = torch.empty((len(datas), 32), dtype=torch.uint8, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pkv.pkv_tensor_roots(dev, off, ln, work, roots, status)
+    got = [bytes(r) for r in roots.cpu().numpy()]
+    assert int(status.item()) == 0
+    assert got == [tensor_root(d) for d in datas]
+
+
+def test_roots_of_many_tensors(pkv):
+    # more tensors than the kernels stage in LDS for their owner search (1024 CSR entries)
+    import torch
+    announce("tensor roots: 1500 tensors of 0..5000 bytes")
+    rng = np.random.default_rng(64)
+    datas = [rng.integers(0, 256, size=int(n), dtype=np.uint8).tobytes() for n in rng.integers(0, 5000, size=1500)]
+    starts, pos = [], 0
+    for d in datas:
+        starts.append(pos)
+        pos += (len(d) + 15) // 16 * 16
+    pool = np.zeros(pos + 16, np.uint8)
+    for st, d in zip(starts, datas):
+        pool[st:st + len(d)] = np.frombuffer(d, np.uint8)
+    dev = torch.from_numpy(pool).cuda()
+    off = torch.tensor(starts, dtype=torch.int64, device="cuda")
+    ln = torch.tensor([len(d) for d in datas], dtype=torch.int64, device="cuda")
+    work = torch.empty((pkv.pkv_tree_work_bytes(dev.numel(), len(datas)) + 7) // 8, dtype=torch.int64, device="cuda")
+    roots = torch.empty((len(datas), 32), dtype=torch.uint8, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pkv.pkv_tensor_roots(dev, off, ln, work, roots, status)
+    got = [bytes(r) for r in roots.cpu().numpy()]
+    assert int(status.item()) == 0
+    assert got == [tensor_root(d) for d in datas]
+
+
 def test_misplaced_tensor_reports_elayout(pkv):
     import torch
     dev = torch.zeros(4096, dtype=torch.uint8, device="cuda")
