@@ -103,27 +103,20 @@ __global__ __launch_bounds__(kDeriveThreads) void k_derive_b16(ChainArgs a) {
     }
 }
 
-// ---- B = 16, two wavefronts per 64 chains (used while chains are scarce) ----------------------
+// ---- consumer / helper split (used while chains are scarce) -----------------------------------
 // A chain's rounds are strictly serial, but much of each key's instruction stream is not on that
-// serial path.  Two wavefronts share the same 64 chains (lane = chain):
-//   consumer (wave 0): only the 2 x 64 SHA-256 rounds of every key, reading K_t + W_t from LDS;
-//   helper   (wave 1): during the first three phases of key i, compression 1's schedule
-//                      W16..W63 (it depends on key i-1), one phase ahead of the consumer; during
-//                      the long last phase, every token-only part of key i+1 (token loads two keys
-//                      ahead, byte swaps, the whole schedule of compression 2) into a double buffer.
+// serial path.  Two wavefronts share the same chains:
+//   consumer: only the SHA-256 rounds of every key, reading K_t + W_t from LDS;
+//   helper:   during the first three phases of key i, compression 1's schedule W16..W63 (it
+//             depends on key i-1), one phase ahead of the consumer; during the long last phase,
+//             every token-only part of key i+1 (token loads two keys ahead, byte swaps, the whole
+//             schedule of the token-only compressions) into a double buffer.
 // Per key there are four phases separated by workgroup barriers: phases 0-2 each hold 16 rounds
-// of compression 1, phase 3 holds its last 16 rounds and all of compression 2, whose 64 K + W
-// words the consumer already holds in registers.  The consumer issues about 1850 instructions per
-// key instead of about 2900.
+// of compression 1, phase 3 holds its last 16 rounds and the token-only compressions, whose K + W
+// words the consumer already holds in registers.  The kernels below use this split with their
+// rounds on lane pairs (B = 16: k_derive_b16_pp; B = 16m: k_derive_m16_pp) or one lane per chain
+// (B = 16m: k_derive_m16_pc).
 constexpr int kPcThreads = 128;
-
-struct PcShared {
-    uint4 kw2[2][16][64];      // K_t + W_t of compression 2, 64 words per lane, two keys
-    uint4 w1tok[2][2][64];     // W8..W15 of compression 1 (byte-swapped tokens 0..7), two keys
-    uint4 kw1tok[2][2][64];    // K_t + W_t for t = 8..15 of compression 1, two keys
-    uint4 kw1hi[12][64];       // K_t + W_t for t = 16..63 of compression 1 (current key)
-    uint4 prev[64];            // previous key words (consumer -> helper)
-};
 
 __device__ __forceinline__ void put4(uint4* p, const uint32_t* v) { *p = make_uint4(v[0], v[1], v[2], v[3]); }
 __device__ __forceinline__ void get4(const uint4* p, uint32_t* v) {
@@ -215,93 +208,6 @@ __device__ __forceinline__ void produce_key(Shared& sh, uint32_t lane, int buf, 
     lds_put16(&sh.kw2[buf][12], lane, kw);
 }
 
-__global__ __launch_bounds__(kPcThreads) void k_derive_b16_pc(ChainArgs a) {
-    __shared__ PcShared sh;
-    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint32_t lane = threadIdx.x & 63;
-    const uint32_t r = blockIdx.x * 64 + lane;
-    int64_t t0 = 0, k0 = 0, n = 0;
-    bool valid = r < a.n_req;
-    if (valid && !chain_bounds(a, r, t0, k0, n)) valid = false;
-    if (!valid) n = 0;
-    const int64_t nmax = wave_max(n);           // identical in both wavefronts
-    uint32_t dg[4] = {0u, 0u, 0u, 0u};
-    if (valid) load_digest(a, r, dg);
-    const int32_t* tp = a.tokens + t0;
-
-    if (wave == 0) {
-        // ---------------- consumer ----------------
-        uint32_t prev[4] = {0u, 0u, 0u, 0u};
-        uint32_t dgk[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) dgk[q] = dg[q] + kRoundK[4 + q];
-        put4(&sh.prev[lane], prev);
-        __syncthreads();                                       // prologue
-        for (int64_t i = 0; i < nmax; ++i) {
-            const int buf = static_cast<int>(i & 1);
-            uint32_t s[8], kw[16], kw2[64];
-            init_state(s);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) { kw[q] = prev[q] + kRoundK[q]; kw[4 + q] = dgk[q]; }
-            get4(&sh.kw1tok[buf][0][lane], kw + 8);
-            get4(&sh.kw1tok[buf][1][lane], kw + 12);
-#pragma unroll
-            for (int ph = 0; ph < 4; ++ph) lds_get16(&sh.kw2[buf][4 * ph], lane, kw2 + 16 * ph);
-            rounds16(s, kw);                                   // rounds 0..15
-            __syncthreads();
-            lds_get16(&sh.kw1hi[0], lane, kw);
-            rounds16(s, kw);                                   // rounds 16..31
-            __syncthreads();
-            lds_get16(&sh.kw1hi[4], lane, kw);
-            rounds16(s, kw);                                   // rounds 32..47
-            __syncthreads();
-            lds_get16(&sh.kw1hi[8], lane, kw);
-            rounds16(s, kw);                                   // rounds 48..63
-            uint32_t hmid[8];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) { hmid[q] = s[q] + kInitH[q]; s[q] = hmid[q]; }
-#pragma unroll
-            for (int ph = 0; ph < 4; ++ph) rounds16(s, kw2 + 16 * ph);   // compression 2
-#pragma unroll
-            for (int q = 0; q < 4; ++q) prev[q] = s[q] + hmid[q];
-            if (i < n) store_key(a.keys, k0 + i, prev);
-            put4(&sh.prev[lane], prev);
-            __syncthreads();                                   // end of key
-        }
-    } else {
-        // ---------------- helper ----------------
-        uint32_t tk[16], pre[16];
-        load_tokens16(tp, 0, n, tk);
-        load_tokens16(tp, 1, n, pre);
-        produce_key(sh, lane, 0, tk);
-        __syncthreads();                                       // prologue
-        for (int64_t i = 0; i < nmax; ++i) {
-            const int buf = static_cast<int>(i & 1);
-            uint32_t w[16], kw[16];
-            get4(&sh.prev[lane], w);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) w[4 + q] = dg[q];
-            get4(&sh.w1tok[buf][0][lane], w + 8);
-            get4(&sh.w1tok[buf][1][lane], w + 12);
-            schedule16<16>(w, kw);
-            lds_put16(&sh.kw1hi[0], lane, kw);
-            __syncthreads();
-            schedule16<32>(w, kw);
-            lds_put16(&sh.kw1hi[4], lane, kw);
-            __syncthreads();
-            schedule16<48>(w, kw);
-            lds_put16(&sh.kw1hi[8], lane, kw);
-            __syncthreads();
-            // long phase: the next key's token-only data, and the tokens two keys ahead
-#pragma unroll
-            for (int q = 0; q < 16; ++q) tk[q] = pre[q];
-            load_tokens16(tp, i + 2, n, pre);
-            produce_key(sh, lane, buf ^ 1, tk);
-            __syncthreads();                                   // end of key
-        }
-    }
-}
-
 // ---- B = 16, each chain on a lane pair (used while chains are very scarce) ---------------------
 // Within one SHA-256 round the e-half (Sigma1, Ch, h + K_t + W_t) and the a-half (Sigma0, Maj) are
 // independent until the final sums.  The consumer wavefront gives each chain two lanes: the even
@@ -319,7 +225,7 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_b16_pc(ChainArgs a) {
 // the two wait states a DPP read of a just-written register needs.  The helper wavefront splits
 // each chain's message schedule the same way (even words on the even lane, odd words on the odd
 // lane), so it keeps ahead of the faster consumer; the token-only work of the next key is done by
-// one helper lane per chain, as in the two-wavefront kernel above.
+// one helper lane per chain.
 constexpr uint32_t kPpChains = 32;
 
 struct PpShared {
@@ -406,22 +312,35 @@ __device__ __forceinline__ void pair_schedule8(uint32_t v[8], bool odd, uint32_t
     }
 }
 
-__global__ __launch_bounds__(kPcThreads) void k_derive_b16_pp(ChainArgs a) {
-    __shared__ PpShared sh;
+// P consumer/helper pairs per workgroup (P = 2 puts two consumers on one compute unit, each on its
+// own SIMD, when there are enough chains for that); every barrier is workgroup-wide, so all pairs
+// run the same number of keys.
+template <int P>
+__global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
+    __shared__ PpShared sh_pairs[P];
+    __shared__ int64_t pair_n[2 * P];
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t pair = wave % P;                // consumers are waves 0..P-1, helpers P..2P-1
+    PpShared& sh = sh_pairs[pair];
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t c = lane >> 1;                  // chain of this lane pair
     const bool odd = (lane & 1) != 0;
-    const uint32_t r = blockIdx.x * kPpChains + c;
+    const uint32_t base = (blockIdx.x * P + pair) * kPpChains;
+    const uint32_t r = base + c;
     int64_t t0 = 0, k0 = 0, n = 0;
     bool valid = r < a.n_req;
     if (valid && !chain_bounds(a, r, t0, k0, n)) valid = false;
     if (!valid) n = 0;
-    const int64_t nmax = wave_max(n);           // identical in both wavefronts
+    int64_t nmax = wave_max(n);                 // identical in both wavefronts of a pair
+    if (P > 1) {
+        if (lane == 0) pair_n[wave] = nmax;
+        __syncthreads();
+        for (int k = 0; k < 2 * P; ++k) nmax = pair_n[k] > nmax ? pair_n[k] : nmax;
+    }
     uint32_t dg[4] = {0u, 0u, 0u, 0u};
     if (valid) load_digest(a, r, dg);
 
-    if (wave == 0) {
+    if (wave < P) {
         // ---------------- consumer: lane pair per chain ----------------
         PairLane pl;
         pl.m = odd ? ~0u : 0u;
@@ -487,7 +406,7 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_b16_pp(ChainArgs a) {
         // ---------------- helper ----------------
         // producer view: lanes 0..31 own chain `lane` for the token-only work
         const bool producer = lane < kPpChains;
-        const uint32_t rp = blockIdx.x * kPpChains + lane;
+        const uint32_t rp = base + lane;
         int64_t pt0 = 0, pk0 = 0, pn = 0;
         if (producer && rp < a.n_req && !chain_bounds(a, rp, pt0, pk0, pn)) pn = 0;
         if (!(producer && rp < a.n_req)) pn = 0;
@@ -1186,10 +1105,11 @@ int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_o
     ChainArgs a{tokens, n_tokens, tok_off, n_req, digests, block, key_off, n_keys, keys, status};
     const dim3 grid((n_req + kDeriveThreads - 1) / kDeriveThreads);
     const unsigned pp_grid = (n_req + kPpChains - 1) / kPpChains;
+    const unsigned pp2_grid = (n_req + 2 * kPpChains - 1) / (2 * kPpChains);
     if (block == 16 && pp_grid <= static_cast<unsigned>(compute_units())) {
-        hipLaunchKernelGGL(k_derive_b16_pp, dim3(pp_grid), dim3(kPcThreads), 0, s, a);
-    } else if (block == 16 && grid.x <= static_cast<unsigned>(compute_units())) {
-        hipLaunchKernelGGL(k_derive_b16_pc, grid, dim3(kPcThreads), 0, s, a);
+        hipLaunchKernelGGL(k_derive_b16_pp<1>, dim3(pp_grid), dim3(kPcThreads), 0, s, a);
+    } else if (block == 16 && pp2_grid <= static_cast<unsigned>(compute_units())) {
+        hipLaunchKernelGGL(k_derive_b16_pp<2>, dim3(pp2_grid), dim3(2 * kPcThreads), 0, s, a);
     } else if (block == 16) {
         hipLaunchKernelGGL(k_derive_b16, grid, dim3(kDeriveThreads), 0, s, a);
     } else if (block % 16 == 0 && pp_grid <= static_cast<unsigned>(compute_units())) {
