@@ -52,18 +52,22 @@ WORKLOAD_TEXT = {
 
 
 DERIVE_SOURCES = ["paper_2609_38706_amd/csrc/k_derive.hip", "paper_2609_38706_amd/csrc/pkv_internal.h"]
+LOOKUP_SOURCES = ["paper_2609_38706_amd/csrc/k_table.hip", "paper_2609_38706_amd/csrc/pkv_internal.h"]
+HBM_PEAK = 8.0e12             # MI355X HBM3E, bytes/s
+BYTES_PER_PROBE = 80          # one 64-byte bucket + the 16-byte probe key
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per derive launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary, or None
-    when there is none for this workload or the derive source has changed since it was taken."""
+def measured_traffic(workload: str, kernel: str = "derive"):
+    """HBM bytes per launch of the derive (or lookup) kernel from the committed rocprofv3
+    FETCH_SIZE/WRITE_SIZE summary, or None when there is none for this workload or the kernel's
+    source has changed since it was taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"derive_traffic_{workload}.json")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
     h = hashlib.sha256()
-    for f in DERIVE_SOURCES:
+    for f in (DERIVE_SOURCES if kernel == "derive" else LOOKUP_SOURCES):
         h.update(open(os.path.join(ROOT, f), "rb").read())
     if rec.get("source_sha256") != h.hexdigest():
         return None
@@ -122,14 +126,22 @@ def setup_gpu(args, w):
     from paper_2609_38706_amd.pipeline import DeviceBatch
     from workloads import locations
 
+    import torch
     table = pkv.Table(w.capacity)
+    fill = None
     for pre in (w.fill, w.warmup):
         if pre is None:
             continue
         db = DeviceBatch.from_batch(pre)
         db.set_locations(locations(db.key_off.cpu().numpy(), pre.tag))
         db.digest()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
         db.derive()
+        ev[1].record()
+        if pre is w.fill:
+            torch.cuda.synchronize()
+            fill = {"chains": db.n_req, "keys": db.n_keys, "block": db.block, "ms": ev[0].elapsed_time(ev[1])}
         if pre is w.warmup:
             db.lookup(table)
         else:
@@ -144,7 +156,7 @@ def setup_gpu(args, w):
         run = DeviceBatch.from_batch(w.batch)
         run.set_locations(locations(run.key_off.cpu().numpy(), w.batch.tag))
         runs.append(run)
-    return pkv, table, runs
+    return pkv, table, runs, fill
 
 
 def serial_leg(args, table, run):
@@ -192,7 +204,7 @@ def gpu_leg(args, w):
     on the stream it is launched on."""
     import torch
     from paper_2609_38706_amd.pipeline import TwoStreamRunner
-    pkv, table, runs = setup_gpu(args, w)
+    pkv, table, runs, fill = setup_gpu(args, w)
     serial = serial_leg(args, table, runs[0])
     runner = TwoStreamRunner(table)
     order = [runs[i % 2] for i in range(max(args.steps, args.warmup))]
@@ -212,9 +224,11 @@ def gpu_leg(args, w):
             raise RuntimeError(f"step failed: status {r.host_status()}")
     run = runs[(args.steps - 1) % 2]
     hits = run.host_hits()
-    return {"ms": (t1 - t0) * 1e3 / args.steps, "derive_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evs])),
+    nk = np.diff(run.key_off.cpu().numpy())
+    probes = int(np.minimum(np.maximum(hits, 0) + 1, nk).sum())         # algorithmic: up to the first miss
+    return {"probes": probes, "ms": (t1 - t0) * 1e3 / args.steps, "derive_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evs])),
             "serial": serial, "n_keys": run.n_keys, "n_req": run.n_req, "hit_blocks": int(hits.sum()),
-            "new_entries": int(run.n_new.item())}
+            "new_entries": int(run.n_new.item()), "fill": fill}
 
 
 def saturation_leg(args, n_chains=131072, blocks=16, reps=5):
@@ -589,6 +603,23 @@ def main():
                 "unit": "Tops/s", "frac": round(achieved / INT_PEAK, 5), "traffic": measured_traffic(args.workload),
                 "kernel": "derive", "ops_per_key": compressions_per_key(block) * OPS_PER_COMPRESSION,
                 "chain_ceiling_frac": round(chain_ceiling_frac(n_chains), 5)}
+    ser = g["serial"]
+    lookup_bps = g["probes"] * BYTES_PER_PROBE / (ser["lookup_ms"] * 1e-3)
+    roofline_lookup = {"bound": "hbm", "achieved": round(lookup_bps / 1e9, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                       "frac": round(lookup_bps / HBM_PEAK, 5), "traffic": measured_traffic(args.workload, "lookup"),
+                       "kernel": "lookup (serial pass, events)", "probes": g["probes"],
+                       "bytes_per_probe": BYTES_PER_PROBE}
+    rates = {"derive_gkeys_per_s": round(g["n_keys"] / (g["derive_ms"] * 1e-3) / 1e9, 4),
+             "lookup_gprobes_per_s": round(g["probes"] / (ser["lookup_ms"] * 1e-3) / 1e9, 4),
+             "store_ginserts_per_s": round(g["new_entries"] / (ser["store_ms"] * 1e-3) / 1e9, 4)}
+    fill = g["fill"]
+    if fill is not None:                       # the index fill: one derive launch over many chains
+        fops = fill["keys"] * compressions_per_key(fill["block"]) * OPS_PER_COMPRESSION
+        fill = {"what": "derive of the index fill (untimed preparation, one launch)", "chains": fill["chains"],
+                "keys": fill["keys"], "ms": round(fill["ms"], 4),
+                "gkeys_per_s": round(fill["keys"] / (fill["ms"] * 1e-3) / 1e9, 4),
+                "frac": round(fops / (fill["ms"] * 1e-3) / INT_PEAK, 5),
+                "chain_ceiling_frac": round(chain_ceiling_frac(fill["chains"]), 5)}
     sat = None
     if not args.no_saturation:
         log(args, "saturation leg")
@@ -612,7 +643,10 @@ def main():
                      "serial_value": round(g["n_keys"] / (g["serial"]["ms"] * 1e-3) / 1e9, 6),
                      "hit_blocks": g["hit_blocks"], "new_entries": g["new_entries"]},
         "roofline": roofline,
+        "roofline_lookup": roofline_lookup,
+        "rates": rates,
         "cpu_baseline": cpu,
+        "derive_fill": fill,
         "derive_saturated": sat,
     }
     print(json.dumps(out), flush=True)
