@@ -145,10 +145,12 @@ class TwoStreamRunner:
         self.s_derive = torch.cuda.Stream()
         self.s_index = torch.cuda.Stream()
 
-    def run(self, batches, rollback: bool = False, derive_events=None):
+    def run(self, batches, rollback: bool = False, derive_events=None, index_work=None):
         """Enqueue one pass per entry of ``batches``; returns without synchronizing.
         ``derive_events[k]`` (a pair of timing events), when given, brackets the derive of pass k on
-        the derive stream."""
+        the derive stream.  ``index_work(k, batch, stream)``, when given, enqueues pass k's index
+        operations on ``stream`` in place of the default (lookup, store, optional rollback); it is
+        called in pass order."""
         import torch
         batches = list(batches)
         for a, b in zip(batches, batches[1:]):
@@ -179,6 +181,9 @@ class TwoStreamRunner:
             if k + 1 < len(batches):
                 ready = prepare(batches[k + 1])     # after the index work of its previous pass
             self.s_index.wait_event(done)
+            if index_work is not None:
+                index_work(k, db, self.s_index)
+                continue
             with torch.cuda.stream(self.s_index):
                 db.n_new.zero_()
             db.lookup(self.table, self.s_index)
