@@ -319,21 +319,26 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
             }
         }
     }
-    // one counter update per wavefront; slot log in lane order
+    // one counter update per workgroup (every lane of the workgroup gets here); slot log in lane order
+    __shared__ uint32_t wave_claims[kStoreThreads / 64];
+    __shared__ uint64_t group_base;
     const uint64_t mask = __ballot(claimed);
-    if (mask) {
-        const uint32_t lane = lane_id();
-        const uint32_t leader = __builtin_ctzll(mask);
-        uint64_t base = 0;
-        if (lane == leader)
-            base = __hip_atomic_fetch_add(a.n_new, static_cast<uint64_t>(__popcll(mask)), __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT);
-        base = __shfl(base, leader, 64);
-        if (claimed && a.new_slots) {
-            const uint64_t pos = base + __popcll(mask & ((1ull << lane) - 1));
-            if (pos < a.n_keys) a.new_slots[pos] = my_slot;
-            else report(a.status, PKV_ELAYOUT);
-        }
+    const uint32_t lane = lane_id(), wave = threadIdx.x >> 6;
+    if (lane == 0) wave_claims[wave] = static_cast<uint32_t>(__popcll(mask));
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t total_claims = 0;
+        for (uint32_t w = 0; w < kStoreThreads / 64; ++w) total_claims += wave_claims[w];
+        group_base = total_claims ? __hip_atomic_fetch_add(a.n_new, total_claims, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT)
+                                  : 0;
+    }
+    __syncthreads();
+    if (claimed && a.new_slots) {
+        uint64_t pos = group_base + __popcll(mask & ((1ull << lane) - 1));
+        for (uint32_t w = 0; w < wave; ++w) pos += wave_claims[w];
+        if (pos < a.n_keys) a.new_slots[pos] = my_slot;
+        else report(a.status, PKV_ELAYOUT);
     }
 }
 
