@@ -93,7 +93,7 @@ def chain_ceiling_frac(n_chains: int) -> float:
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_TEXT))
     p.add_argument("--no-cpu-baseline", action="store_true")
