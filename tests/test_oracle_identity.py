@@ -69,3 +69,14 @@ def test_identity_definition_and_sensitivity():
         assert identity(v, cfg) != base
     assert identity(ts, cfg[:1]) != base
     assert identity(ts, [(b"r", b"16"), (b"alpha", b"33")]) != base
+
+
+def test_record_layout_written_out():
+    # the record of one small tensor, byte by byte (little-endian integers; the root from hashlib)
+    data = bytes(range(12))
+    root = _h(b"\x00" + data)
+    want = (b"PKVT" + b"\x01\x00\x00\x00" + b"w" + b"\x04\x00\x00\x00" + b"bf16" + b"\x02\x00\x00\x00"
+            + b"\x02\x00\x00\x00\x00\x00\x00\x00" + b"\x03\x00\x00\x00\x00\x00\x00\x00"
+            + b"\x0c\x00\x00\x00\x00\x00\x00\x00" + root)
+    assert record(b"w", b"bf16", (2, 3), data) == want
+    assert len(want) == 4 + 4 + 1 + 4 + 4 + 4 + 16 + 8 + 32
