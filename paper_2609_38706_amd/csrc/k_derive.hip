@@ -169,45 +169,6 @@ __device__ __forceinline__ int64_t wave_max(int64_t v) {
     return v;
 }
 
-__device__ __forceinline__ void load_tokens16(const int32_t* tp, int64_t key, int64_t n, uint32_t out[16]) {
-    if (key < n) {
-        const int32_t* p = tp + key * 16;
-#pragma unroll
-        for (int q = 0; q < 16; ++q) out[q] = static_cast<uint32_t>(p[q]);
-    } else {
-#pragma unroll
-        for (int q = 0; q < 16; ++q) out[q] = 0u;
-    }
-}
-
-// Token-only data of one key (16 tokens tk) into buffer `buf` of column `lane`.
-template <typename Shared>
-__device__ __forceinline__ void produce_key(Shared& sh, uint32_t lane, int buf, const uint32_t tk[16]) {
-    uint32_t v[8], kv[8], w[16], kw[16];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) { v[q] = bswap(tk[q]); kv[q] = v[q] + kRoundK[8 + q]; }
-    put4(&sh.w1tok[buf][0][lane], v);
-    put4(&sh.w1tok[buf][1][lane], v + 4);
-    put4(&sh.kw1tok[buf][0][lane], kv);
-    put4(&sh.kw1tok[buf][1][lane], kv + 4);
-    // compression 2: tokens 8..15, then the padding of a 96-byte message
-#pragma unroll
-    for (int q = 0; q < 8; ++q) w[q] = bswap(tk[8 + q]);
-    w[8] = 0x80000000u;
-#pragma unroll
-    for (int q = 9; q < 15; ++q) w[q] = 0u;
-    w[15] = (32u + 4u * 16u) * 8u;
-#pragma unroll
-    for (int q = 0; q < 16; ++q) kw[q] = w[q] + kRoundK[q];
-    lds_put16(&sh.kw2[buf][0], lane, kw);
-    schedule16<16>(w, kw);
-    lds_put16(&sh.kw2[buf][4], lane, kw);
-    schedule16<32>(w, kw);
-    lds_put16(&sh.kw2[buf][8], lane, kw);
-    schedule16<48>(w, kw);
-    lds_put16(&sh.kw2[buf][12], lane, kw);
-}
-
 // ---- B = 16, each chain on a lane pair (used while chains are very scarce) ---------------------
 // Within one SHA-256 round the e-half (Sigma1, Ch, h + K_t + W_t) and the a-half (Sigma0, Maj) are
 // independent until the final sums.  The consumer wavefront gives each chain two lanes: the even
@@ -224,8 +185,8 @@ __device__ __forceinline__ void produce_key(Shared& sh, uint32_t lane, int buf, 
 // next round's Q sits between the producer of the swapped value and the DPP read, which covers
 // the two wait states a DPP read of a just-written register needs.  The helper wavefront splits
 // each chain's message schedule the same way (even words on the even lane, odd words on the odd
-// lane), so it keeps ahead of the faster consumer; the token-only work of the next key is done by
-// one helper lane per chain.
+// lane), so it keeps ahead of the faster consumer; the token-only work of the next key is split the
+// same way.
 constexpr uint32_t kPpChains = 32;
 
 struct PpShared {
@@ -299,17 +260,66 @@ __device__ __forceinline__ uint32_t pair_schedule_step(uint32_t v[8], bool odd) 
     return w;
 }
 
-// Steps j = J0 .. J0+7 of the paired schedule; each lane writes K + W of its word into kw1hi.
-template <int J0>
-__device__ __forceinline__ void pair_schedule8(uint32_t v[8], bool odd, uint32_t* kw1hi_col) {
+// Steps j = J0 .. J0+7 of the paired schedule; each lane writes K + W of its word into a column of
+// uint4 rows whose first row holds words T0 .. T0+3 (kw1hi: T0 = 16; a token slot: T0 = 0).
+template <int J0, int T0 = 16>
+__device__ __forceinline__ void pair_schedule8(uint32_t v[8], bool odd, uint32_t* col) {
 #pragma unroll
     for (int j = J0; j < J0 + 8; ++j) {
         const uint32_t w = pair_schedule_step(v, odd);
         const uint32_t k = odd ? kRoundK[2 * j + 1] : kRoundK[2 * j];
-        // word t = 2j + odd lives at [(t - 16) / 4][chain].component(t % 4); the lane's column
+        // word t = 2j + odd lives at [(t - T0) / 4][chain].component(t % 4); the lane's column
         // pointer already includes its chain and parity
-        kw1hi_col[((2 * j - 16) >> 2) * (kPpChains * 4) + ((2 * j) & 3)] = w + k;
+        col[((2 * j - T0) >> 2) * (kPpChains * 4) + ((2 * j) & 3)] = w + k;
     }
+}
+
+// This lane's parity of a key's 16 tokens (out[k] = token 2k + odd), zeros past the chain.
+__device__ __forceinline__ void load_tokens_pair(const int32_t* tp, int64_t key, int64_t n, bool odd, uint32_t out[8]) {
+    if (key < n) {
+        const int32_t* p = tp + key * 16 + (odd ? 1 : 0);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) out[k] = static_cast<uint32_t>(p[2 * k]);
+    } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) out[k] = 0u;
+    }
+}
+
+// Token-only data of one key (B = 16) by a lane pair: each lane writes its parity of compression
+// 1's words 8..15 (and their K + W) and of compression 2's K + W words, computing its parity of
+// compression 2's schedule with pair_schedule8.
+__device__ __forceinline__ void produce_key_pair(PpShared& sh, uint32_t chain, bool odd, int buf, const uint32_t tk[8]) {
+    const uint32_t o = odd ? 1u : 0u;
+    uint32_t* wcol = reinterpret_cast<uint32_t*>(&sh.w1tok[buf][0][chain]) + o;
+    uint32_t* kcol = reinterpret_cast<uint32_t*>(&sh.kw1tok[buf][0][chain]) + o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {                      // compression 1, word 8 + 2k + odd = token 2k + odd
+        const uint32_t x = bswap(tk[k]);
+        const uint32_t kk = odd ? kRoundK[8 + 2 * k + 1] : kRoundK[8 + 2 * k];
+        wcol[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = x;
+        kcol[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = x + kk;
+    }
+    // compression 2: words 0..7 = tokens 8..15, then the padding of a 96-byte message
+    uint32_t own[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) own[k] = bswap(tk[4 + k]);
+    own[4] = odd ? 0u : 0x80000000u;
+    own[5] = 0u;
+    own[6] = 0u;
+    own[7] = odd ? (32u + 4u * 16u) * 8u : 0u;
+    uint32_t* col = reinterpret_cast<uint32_t*>(&sh.kw2[buf][0][chain]) + o;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const uint32_t kk = odd ? kRoundK[2 * k + 1] : kRoundK[2 * k];
+        col[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = own[k] + kk;
+    }
+    uint32_t v[8];                                     // own words, newest first
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = own[7 - k];
+    pair_schedule8<8, 0>(v, odd, col);
+    pair_schedule8<16, 0>(v, odd, col);
+    pair_schedule8<24, 0>(v, odd, col);
 }
 
 // P consumer/helper pairs per workgroup (P = 2 puts two consumers on one compute unit, each on its
@@ -403,25 +413,16 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             __syncthreads();                                   // end of key
         }
     } else {
-        // ---------------- helper ----------------
-        // producer view: lanes 0..31 own chain `lane` for the token-only work
-        const bool producer = lane < kPpChains;
-        const uint32_t rp = base + lane;
-        int64_t pt0 = 0, pk0 = 0, pn = 0;
-        if (producer && rp < a.n_req && !chain_bounds(a, rp, pt0, pk0, pn)) pn = 0;
-        if (!(producer && rp < a.n_req)) pn = 0;
-        const int32_t* tp = a.tokens + pt0;
-        // schedule view: the lane pair of chain c; odd lanes take odd message words
+        // ---------------- helper: lane pair per chain ----------------
+        const int32_t* tp = a.tokens + t0;
         uint32_t dsel[2];
         dsel[0] = odd ? dg[1] : dg[0];     // W4 / W5
         dsel[1] = odd ? dg[3] : dg[2];     // W6 / W7
         uint32_t* kw1hi_col = reinterpret_cast<uint32_t*>(&sh.kw1hi[0][c]) + (odd ? 1 : 0);
-        uint32_t tk[16], pre[16];
-        if (producer) {
-            load_tokens16(tp, 0, pn, tk);
-            load_tokens16(tp, 1, pn, pre);
-            produce_key(sh, lane, 0, tk);
-        }
+        uint32_t tk[8], pre[8];
+        load_tokens_pair(tp, 0, n, odd, tk);
+        load_tokens_pair(tp, 1, n, odd, pre);
+        produce_key_pair(sh, c, odd, 0, tk);
         __syncthreads();                                       // prologue
         for (int64_t i = 0; i < nmax; ++i) {
             const int buf = static_cast<int>(i & 1);
@@ -442,12 +443,10 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             __syncthreads();
             pair_schedule8<24>(v, odd, kw1hi_col);
             __syncthreads();
-            if (producer) {                                    // the next key's token-only data
 #pragma unroll
-                for (int q = 0; q < 16; ++q) tk[q] = pre[q];
-                load_tokens16(tp, i + 2, pn, pre);
-                produce_key(sh, lane, buf ^ 1, tk);
-            }
+            for (int q = 0; q < 8; ++q) tk[q] = pre[q];        // the next key's token-only data
+            load_tokens_pair(tp, i + 2, n, odd, pre);
+            produce_key_pair(sh, c, odd, buf ^ 1, tk);
             __syncthreads();                                   // end of key
         }
     }
@@ -651,6 +650,88 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pc(ChainArgs a) {
 // key runs in four barrier phases while the helper's lane pairs compute its schedule; each of the
 // m token-only compressions reads its 64 K + W words from a ring of three LDS slots that one
 // helper lane per chain fills two compressions ahead.
+// Token words of one production for a lane pair: this lane's parity of the 16 words of token
+// compression (key, c) (for the last compression only its 8 token words; the padding is added when
+// the words are produced), and for c == 1 its parity of tokens 0..7 (compression 1's words).
+// w[k] = word 2k + odd, head[k] = token 2k + odd, not yet byte-swapped; zeros past the chain.
+struct PairProduction {
+    uint32_t head[4];
+    uint32_t w[8];
+};
+
+__device__ __forceinline__ void load_production_pair(const int32_t* tp, uint32_t B, uint32_t m, int64_t n, int64_t g,
+                                                     bool odd, PairProduction& pr) {
+    const int64_t key = g / m;
+    const uint32_t c = static_cast<uint32_t>(g - key * m) + 1;
+    const uint32_t o = odd ? 1u : 0u;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pr.head[k] = 0u;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) pr.w[k] = 0u;
+    if (key < n) {
+        const int32_t* kp = tp + key * static_cast<int64_t>(B);
+        if (c == 1) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) pr.head[k] = static_cast<uint32_t>(kp[2 * k + o]);
+        }
+        const int32_t* src = kp + 16 * c - 8;
+        if (c < m) {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) pr.w[k] = static_cast<uint32_t>(src[2 * k + o]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) pr.w[k] = static_cast<uint32_t>(src[2 * k + o]);
+        }
+    }
+}
+
+// Production g by a lane pair: each lane byte-swaps its parity of the message words, computes its
+// parity of the schedule (pair_schedule8) and writes its K + W words into the slot; for c == 1
+// also its parity of compression 1's token words.
+template <typename Shared>
+__device__ __forceinline__ void produce_comp_pair(Shared& sh, uint32_t chain, bool odd, uint32_t m, uint32_t bitlen,
+                                                  int64_t g, const PairProduction& pr) {
+    const int64_t key = g / m;
+    const uint32_t c = static_cast<uint32_t>(g - key * m) + 1;
+    const uint32_t o = odd ? 1u : 0u;
+    if (c == 1) {
+        const int kb = static_cast<int>(key & 1);
+        uint32_t* wcol = reinterpret_cast<uint32_t*>(&sh.w1tok[kb][0][chain]) + o;
+        uint32_t* kcol = reinterpret_cast<uint32_t*>(&sh.kw1tok[kb][0][chain]) + o;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {                  // message word 8 + 2k + odd of compression 1
+            const uint32_t x = bswap(pr.head[k]);
+            const uint32_t kk = odd ? kRoundK[8 + 2 * k + 1] : kRoundK[8 + 2 * k];
+            wcol[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = x;
+            kcol[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = x + kk;
+        }
+    }
+    uint32_t own[8];
+    if (c < m) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) own[k] = bswap(pr.w[k]);
+    } else {                                           // words 8..15: 0x80000000, zeros, the bit length
+#pragma unroll
+        for (int k = 0; k < 4; ++k) own[k] = bswap(pr.w[k]);
+        own[4] = odd ? 0u : 0x80000000u;
+        own[5] = 0u;
+        own[6] = 0u;
+        own[7] = odd ? bitlen : 0u;
+    }
+    uint32_t* col = reinterpret_cast<uint32_t*>(&sh.kwt[static_cast<int>(g % 3)][0][chain]) + o;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const uint32_t kk = odd ? kRoundK[2 * k + 1] : kRoundK[2 * k];
+        col[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = own[k] + kk;
+    }
+    uint32_t v[8];                                     // own words, newest first
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = own[7 - k];
+    pair_schedule8<8, 0>(v, odd, col);
+    pair_schedule8<16, 0>(v, odd, col);
+    pair_schedule8<24, 0>(v, odd, col);
+}
+
 struct PpmShared {
     uint4 kwt[3][16][kPpChains];      // K_t + W_t of token-only compressions, three slots
     uint4 w1tok[2][2][kPpChains];     // W8..W15 of compression 1, two keys
@@ -756,27 +837,20 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
             }
         }
     } else {
-        // ---------------- helper ----------------
-        const bool producer = lane < kPpChains;               // lanes 0..31 own chain `lane`
-        const uint32_t rp = blockIdx.x * kPpChains + lane;
-        int64_t pt0 = 0, pk0 = 0, pn = 0;
-        if (producer && rp < a.n_req && !chain_bounds(a, rp, pt0, pk0, pn)) pn = 0;
-        if (!(producer && rp < a.n_req)) pn = 0;
-        const int32_t* tp = a.tokens + pt0;
+        // ---------------- helper: lane pair per chain ----------------
+        const int32_t* tp = a.tokens + t0;
         uint32_t dsel[2];
         dsel[0] = odd ? dg[1] : dg[0];
         dsel[1] = odd ? dg[3] : dg[2];
         uint32_t* kw1hi_col = reinterpret_cast<uint32_t*>(&sh.kw1hi[0][c]) + (odd ? 1 : 0);
         const int64_t total = nmax * m;                        // token compressions of the workgroup
-        Production p0, p1, p2;
-        if (producer) {
-            load_production(tp, B, m, pn, 0, p0);
-            load_production(tp, B, m, pn, 1, p1);
-            produce_comp(sh, lane, m, bitlen, 0, p0);
-            produce_comp(sh, lane, m, bitlen, 1, p1);
-            load_production(tp, B, m, pn, 2, p0);              // p0, p1 = productions g + 2, g + 3
-            load_production(tp, B, m, pn, 3, p1);
-        }
+        PairProduction p0, p1, p2;
+        load_production_pair(tp, B, m, n, 0, odd, p0);
+        load_production_pair(tp, B, m, n, 1, odd, p1);
+        produce_comp_pair(sh, c, odd, m, bitlen, 0, p0);
+        produce_comp_pair(sh, c, odd, m, bitlen, 1, p1);
+        load_production_pair(tp, B, m, n, 2, odd, p0);         // p0, p1 = productions g + 2, g + 3
+        load_production_pair(tp, B, m, n, 3, odd, p1);
         __syncthreads();                                       // prologue
         for (int64_t i = 0; i < nmax; ++i) {
             const int kb = static_cast<int>(i & 1);
@@ -799,12 +873,10 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
             __syncthreads();                                   // end of compression 1
             for (uint32_t cc = 1; cc <= m; ++cc) {
                 const int64_t g = i * m + (cc - 1) + 2;        // production made during compression (i, cc)
-                if (producer) {
-                    p2 = p0;
-                    p0 = p1;
-                    load_production(tp, B, m, pn, g + 2, p1);
-                    if (g < total) produce_comp(sh, lane, m, bitlen, g, p2);
-                }
+                p2 = p0;
+                p0 = p1;
+                load_production_pair(tp, B, m, n, g + 2, odd, p1);
+                if (g < total) produce_comp_pair(sh, c, odd, m, bitlen, g, p2);
                 __syncthreads();                               // end of token compression cc
             }
         }
