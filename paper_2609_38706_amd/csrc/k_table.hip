@@ -193,37 +193,48 @@ __device__ __forceinline__ uint64_t wave_base_of(uint32_t block_threads) {
     return static_cast<uint64_t>(blockIdx.x) * block_threads + wave * 64ull;
 }
 
-// Key bytes of a slot whose location word was seen published, read as two relaxed 64-bit
-// atomics.  During one store launch a key slot only ever holds a marker pattern (empty or removed)
-// or its final key, so a half that matches neither marker's half is final.  A half that does is
-// re-read after an acquire fence: either it really has that value, or the read was stale.
+// Device-coherent 16-byte accesses to one key slot.  The sc1 bit gives the same agent-scope
+// coherence that the compiler uses for relaxed agent-scope atomics (the access bypasses the
+// non-coherent part of the XCD's L2), for all 16 bytes in one memory operation instead of two
+// 8-byte ones.  Each statement waits for its own access (vmcnt 0), so the result is in place when
+// it returns and the compiler need not track the access.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 load_key_coherent(const uint4* p) {
+    u32x4 v;
+    asm volatile("global_load_dwordx4 %0, %1, off sc1\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(p) : "memory");
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void store_key_coherent(uint4* p, const uint4& k) {
+    const u32x4 v = {k.x, k.y, k.z, k.w};
+    asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_waitcnt vmcnt(0)" : : "v"(p), "v"(v) : "memory");
+}
+
+// Key bytes of a slot whose location word was seen published.  During one store launch a key
+// slot only ever holds a marker pattern (empty or removed) or its final key, so a key whose
+// 8-byte halves match neither marker's half is final.  One that does is re-read after an acquire
+// fence: either it really has that value, or the read was stale.
 constexpr uint64_t kTombHi = (static_cast<uint64_t>(kTombW) << 32) | 0xFFFFFFFFull;
 
 __device__ __forceinline__ uint4 read_slot_key(uint4* tkeys, uint64_t s) {
-    uint64_t* p = reinterpret_cast<uint64_t*>(tkeys + s);
-    uint64_t lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    uint64_t hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint4 k = load_key_coherent(tkeys + s);
+    const uint64_t lo = (static_cast<uint64_t>(k.y) << 32) | k.x, hi = (static_cast<uint64_t>(k.w) << 32) | k.z;
     if (lo == ~0ull || hi == ~0ull || hi == kTombHi) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        k = load_key_coherent(tkeys + s);
     }
-    return make_uint4(static_cast<uint32_t>(lo), static_cast<uint32_t>(lo >> 32), static_cast<uint32_t>(hi),
-                      static_cast<uint32_t>(hi >> 32));
+    return k;
 }
 
-// Writes a claimed slot's key and then publishes its location word.  The two key halves are
-// agent-scope atomic stores (write-through to the device coherence point); the lane waits until
-// both are complete (vmcnt 0) before the location store is issued, so any lane that reads the
-// published location word afterwards reads the final key.  This is the gfx950 agent-scope release
-// without its L2 writeback: that writeback exists for preceding non-atomic stores, and none precede
-// the publication here.  The asm statement's memory clobber also keeps the compiler from moving
-// the stores across the wait.
+// Writes a claimed slot's key and then publishes its location word.  The key is one 16-byte
+// device-coherent store, complete (vmcnt 0) before the location store is issued, so any lane that
+// reads the published location word afterwards reads the final key.  This is the gfx950
+// agent-scope release without its L2 writeback: that writeback exists for preceding non-atomic
+// stores, and none precede the publication here.  The asm statement's memory clobber keeps the
+// compiler from moving the stores across each other.
 __device__ __forceinline__ void publish_slot(uint4* tkeys, uint64_t* tlocs, uint64_t s, const uint4& k, uint64_t v) {
-    uint64_t* p = reinterpret_cast<uint64_t*>(tkeys + s);
-    __hip_atomic_store(p, (static_cast<uint64_t>(k.y) << 32) | k.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(p + 1, (static_cast<uint64_t>(k.w) << 32) | k.z, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    store_key_coherent(tkeys + s, k);
     __hip_atomic_store(tlocs + s, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
