@@ -231,6 +231,32 @@ __device__ __forceinline__ void pair_rounds4(uint32_t& x0, uint32_t& x1, uint32_
                  : [m] "v"(pl.m), [nm] "v"(pl.nm), [r1] "v"(pl.r1), [r2] "v"(pl.r2), [r3] "v"(pl.r3), [k1] "v"(k1),
                    [k2] "v"(k2), [k3] "v"(k3), [k4] "v"(k4));
 }
+// The same round without forming the next round's Q (the caller forms it from K + W words that
+// are still arriving); two wait states cover the DPP read of the just-written select.
+#define PKV_PAIR_ROUND_LAST(X0, X1, X2, X3)                                                        \
+    "v_alignbit_b32 %[t0], %[" #X0 "], %[" #X0 "], %[r1]\n"                                       \
+    "v_alignbit_b32 %[t1], %[" #X0 "], %[" #X0 "], %[r2]\n"                                       \
+    "v_alignbit_b32 %[t2], %[" #X0 "], %[" #X0 "], %[r3]\n"                                       \
+    "v_bitop3_b32 %[t0], %[t0], %[t1], %[t2] bitop3:0x96\n"                                       \
+    "v_bitop3_b32 %[t1], %[" #X0 "], %[" #X1 "], %[m] bitop3:0xd2\n"                              \
+    "v_bitop3_b32 %[t1], %[t1], %[" #X1 "], %[" #X2 "] bitop3:0xca\n"                             \
+    "v_add3_u32 %[t0], %[t0], %[t1], %[q]\n"                                                      \
+    "v_bitop3_b32 %[t1], %[m], %[" #X3 "], %[t0] bitop3:0xca\n"                                   \
+    "s_nop 1\n"                                                                                   \
+    "v_add_u32_dpp %[" #X3 "], %[t1], %[t0] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
+
+// Four paired rounds whose last one leaves Q of the following round to the caller.
+__device__ __forceinline__ void pair_rounds4_last(uint32_t& x0, uint32_t& x1, uint32_t& x2, uint32_t& x3, uint32_t q,
+                                                  const PairLane& pl, uint32_t k1, uint32_t k2, uint32_t k3) {
+    uint32_t t0, t1, t2;
+    asm volatile(PKV_PAIR_ROUND(a, b, c, d, k1) PKV_PAIR_ROUND(d, a, b, c, k2) PKV_PAIR_ROUND(c, d, a, b, k3)
+                     PKV_PAIR_ROUND_LAST(b, c, d, a)
+                 : [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [q] "+v"(q), [a] "+v"(x0), [b] "+v"(x1),
+                   [c] "+v"(x2), [d] "+v"(x3)
+                 : [m] "v"(pl.m), [nm] "v"(pl.nm), [r1] "v"(pl.r1), [r2] "v"(pl.r2), [r3] "v"(pl.r3), [k1] "v"(k1),
+                   [k2] "v"(k2), [k3] "v"(k3));
+}
+#undef PKV_PAIR_ROUND_LAST
 #undef PKV_PAIR_ROUND
 
 // 16 paired rounds; kw[j] = K + W of round t0 + j, `after` = K + W of round t0 + 16 (any value
@@ -243,17 +269,83 @@ __device__ __forceinline__ void pair_rounds16(uint32_t x[4], uint32_t& q, const 
     pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[13], kw[14], kw[15], after);
 }
 
+// Compression 1 of a key on the consumer: rounds 0..15 take K + W from kw (registers), the other
+// 48 rounds from the helper's rows (rows[4p + j][c] holds rounds 16 + 16p + 4j .. + 3).  The
+// barrier that makes a phase's rows visible sits four rounds before the phase starts, and the rows
+// are read right after it, so the last four rounds of the previous phase cover their LDS latency;
+// those four rounds leave Q of the phase's first round to be formed from the new words.
+__device__ __forceinline__ void pair_comp1(uint32_t x[4], const PairLane& pl, const uint32_t kw[16],
+                                           const uint4 (*rows)[kPpChains], uint32_t c) {
+    uint32_t ka[16], kb[16];
+    uint32_t q = (x[3] + kw[0]) & pl.nm;
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[1], kw[2], kw[3], kw[4]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[5], kw[6], kw[7], kw[8]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[9], kw[10], kw[11], kw[12]);      // rounds 0..11
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) get4(&rows[j][c], ka + 4 * j);
+    pair_rounds4_last(x[0], x[1], x[2], x[3], q, pl, kw[13], kw[14], kw[15]);         // rounds 12..15
+    q = (x[3] + ka[0]) & pl.nm;
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, ka[1], ka[2], ka[3], ka[4]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, ka[5], ka[6], ka[7], ka[8]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, ka[9], ka[10], ka[11], ka[12]);      // rounds 16..27
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) get4(&rows[4 + j][c], kb + 4 * j);
+    pair_rounds4_last(x[0], x[1], x[2], x[3], q, pl, ka[13], ka[14], ka[15]);         // rounds 28..31
+    q = (x[3] + kb[0]) & pl.nm;
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kb[1], kb[2], kb[3], kb[4]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kb[5], kb[6], kb[7], kb[8]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kb[9], kb[10], kb[11], kb[12]);      // rounds 32..43
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) get4(&rows[8 + j][c], ka + 4 * j);
+    pair_rounds4_last(x[0], x[1], x[2], x[3], q, pl, kb[13], kb[14], kb[15]);         // rounds 44..47
+    q = (x[3] + ka[0]) & pl.nm;
+    pair_rounds16(x, q, pl, ka, 0u);                                                   // rounds 48..63
+}
+
 __device__ __forceinline__ uint32_t lane_swap(uint32_t v) {
     return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0xB1, 0xF, 0xF, false));
+}
+
+// a + (b of the partner lane), one instruction; two wait states cover a just-written b.
+__device__ __forceinline__ uint32_t add_swapped(uint32_t a, uint32_t b) {
+    uint32_t r;
+    asm("s_nop 1\n\tv_add_u32_dpp %0, %1, %2 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf" : "=v"(r) : "v"(b), "v"(a));
+    return r;
+}
+
+// Bitwise select m ? a : b in one instruction (v_bfi_b32), with the lane's parity mask m as an
+// ordinary register: no condition register to rebuild around each use.
+__device__ __forceinline__ uint32_t bsel(uint32_t m, uint32_t a, uint32_t b) {
+    uint32_t r;
+    asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(a), "v"(b));
+    return r;
+}
+
+// What a lane of a pair needs for its parity of a message schedule: its parity mask and
+// k[j] = K_{2j + odd} for j = 0..31, held in registers for the whole kernel.
+struct PairK {
+    uint32_t m;
+    uint32_t k[32];
+};
+
+__device__ __forceinline__ PairK make_pair_k(bool odd) {
+    PairK pk;
+    pk.m = odd ? ~0u : 0u;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) pk.k[j] = odd ? kRoundK[2 * j + 1] : kRoundK[2 * j];
+    return pk;
 }
 
 // One step of a message schedule split over a lane pair: the even lane computes W_{2j}, the odd
 // lane W_{2j+1}.  v[k] is the lane's own word k+1 steps back.  The even lane needs its partner's
 // W_{2j-7} and W_{2j-15}, the odd lane its partner's W_{2j-6} and W_{2j-14}; each lane sends
 // sigma0 of the older one plus the newer one.
-__device__ __forceinline__ uint32_t pair_schedule_step(uint32_t v[8], bool odd) {
-    const uint32_t z = dev::ssig0(odd ? v[7] : v[6]) + (odd ? v[3] : v[2]);
-    const uint32_t w = dev::ssig1(v[0]) + v[7] + lane_swap(z);
+__device__ __forceinline__ uint32_t pair_schedule_step(uint32_t v[8], uint32_t m) {
+    const uint32_t z = dev::ssig0(bsel(m, v[7], v[6])) + bsel(m, v[3], v[2]);
+    const uint32_t w = dev::ssig1(v[0]) + add_swapped(v[7], z);
 #pragma unroll
     for (int k = 7; k > 0; --k) v[k] = v[k - 1];
     v[0] = w;
@@ -263,11 +355,11 @@ __device__ __forceinline__ uint32_t pair_schedule_step(uint32_t v[8], bool odd) 
 // Steps j = J0 .. J0+7 of the paired schedule; each lane writes K + W of its word into a column of
 // uint4 rows whose first row holds words T0 .. T0+3 (kw1hi: T0 = 16; a token slot: T0 = 0).
 template <int J0, int T0 = 16>
-__device__ __forceinline__ void pair_schedule8(uint32_t v[8], bool odd, uint32_t* col) {
+__device__ __forceinline__ void pair_schedule8(uint32_t v[8], const PairK& pk, uint32_t* col) {
 #pragma unroll
     for (int j = J0; j < J0 + 8; ++j) {
-        const uint32_t w = pair_schedule_step(v, odd);
-        const uint32_t k = odd ? kRoundK[2 * j + 1] : kRoundK[2 * j];
+        const uint32_t w = pair_schedule_step(v, pk.m);
+        const uint32_t k = pk.k[j];
         // word t = 2j + odd lives at [(t - T0) / 4][chain].component(t % 4); the lane's column
         // pointer already includes its chain and parity
         col[((2 * j - T0) >> 2) * (kPpChains * 4) + ((2 * j) & 3)] = w + k;
@@ -289,14 +381,15 @@ __device__ __forceinline__ void load_tokens_pair(const int32_t* tp, int64_t key,
 // Token-only data of one key (B = 16) by a lane pair: each lane writes its parity of compression
 // 1's words 8..15 (and their K + W) and of compression 2's K + W words, computing its parity of
 // compression 2's schedule with pair_schedule8.
-__device__ __forceinline__ void produce_key_pair(PpShared& sh, uint32_t chain, bool odd, int buf, const uint32_t tk[8]) {
+__device__ __forceinline__ void produce_key_pair(PpShared& sh, uint32_t chain, bool odd, const PairK& pk, int buf,
+                                                 const uint32_t tk[8]) {
     const uint32_t o = odd ? 1u : 0u;
     uint32_t* wcol = reinterpret_cast<uint32_t*>(&sh.w1tok[buf][0][chain]) + o;
     uint32_t* kcol = reinterpret_cast<uint32_t*>(&sh.kw1tok[buf][0][chain]) + o;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {                      // compression 1, word 8 + 2k + odd = token 2k + odd
         const uint32_t x = bswap(tk[k]);
-        const uint32_t kk = odd ? kRoundK[8 + 2 * k + 1] : kRoundK[8 + 2 * k];
+        const uint32_t kk = pk.k[4 + k];
         wcol[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = x;
         kcol[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = x + kk;
     }
@@ -304,22 +397,19 @@ __device__ __forceinline__ void produce_key_pair(PpShared& sh, uint32_t chain, b
     uint32_t own[8];
 #pragma unroll
     for (int k = 0; k < 4; ++k) own[k] = bswap(tk[4 + k]);
-    own[4] = odd ? 0u : 0x80000000u;
+    own[4] = ~pk.m & 0x80000000u;
     own[5] = 0u;
     own[6] = 0u;
-    own[7] = odd ? (32u + 4u * 16u) * 8u : 0u;
+    own[7] = pk.m & ((32u + 4u * 16u) * 8u);
     uint32_t* col = reinterpret_cast<uint32_t*>(&sh.kw2[buf][0][chain]) + o;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-        const uint32_t kk = odd ? kRoundK[2 * k + 1] : kRoundK[2 * k];
-        col[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = own[k] + kk;
-    }
+    for (int k = 0; k < 8; ++k) col[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = own[k] + pk.k[k];
     uint32_t v[8];                                     // own words, newest first
 #pragma unroll
     for (int k = 0; k < 8; ++k) v[k] = own[7 - k];
-    pair_schedule8<8, 0>(v, odd, col);
-    pair_schedule8<16, 0>(v, odd, col);
-    pair_schedule8<24, 0>(v, odd, col);
+    pair_schedule8<8, 0>(v, pk, col);
+    pair_schedule8<16, 0>(v, pk, col);
+    pair_schedule8<24, 0>(v, pk, col);
 }
 
 // P consumer/helper pairs per workgroup (P = 2 puts two consumers on one compute unit, each on its
@@ -382,17 +472,7 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             for (int ph = 0; ph < 16; ++ph) get4(&sh.kw2[buf][ph][c], kw2 + 4 * ph);
 #pragma unroll
             for (int j = 0; j < 4; ++j) x[j] = iv[j];
-            q = (x[3] + kw[0]) & pl.nm;
-            pair_rounds16(x, q, pl, kw, 0u);                   // rounds 0..15
-            __syncthreads();
-#pragma unroll
-            for (int ph = 0; ph < 3; ++ph) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) get4(&sh.kw1hi[4 * ph + j][c], kw + 4 * j);
-                q = (x[3] + kw[0]) & pl.nm;
-                pair_rounds16(x, q, pl, kw, 0u);               // rounds 16(ph+1) .. 16(ph+1)+15
-                if (ph < 2) __syncthreads();
-            }
+            pair_comp1(x, pl, kw, sh.kw1hi, c);                // three barriers inside
 #pragma unroll
             for (int j = 0; j < 4; ++j) { hmid[j] = x[j] + iv[j]; x[j] = hmid[j]; }
             q = (x[3] + kw2[0]) & pl.nm;
@@ -419,10 +499,11 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
         dsel[0] = odd ? dg[1] : dg[0];     // W4 / W5
         dsel[1] = odd ? dg[3] : dg[2];     // W6 / W7
         uint32_t* kw1hi_col = reinterpret_cast<uint32_t*>(&sh.kw1hi[0][c]) + (odd ? 1 : 0);
+        const PairK pk = make_pair_k(odd);
         uint32_t tk[8], pre[8];
         load_tokens_pair(tp, 0, n, odd, tk);
         load_tokens_pair(tp, 1, n, odd, pre);
-        produce_key_pair(sh, c, odd, 0, tk);
+        produce_key_pair(sh, c, odd, pk, 0, tk);
         __syncthreads();                                       // prologue
         for (int64_t i = 0; i < nmax; ++i) {
             const int buf = static_cast<int>(i & 1);
@@ -432,21 +513,21 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             get4(&sh.w1tok[buf][1][c], tw + 4);
             // own words, newest first: W14 W12 .. W0 (even lane) or W15 W13 .. W1 (odd lane)
 #pragma unroll
-            for (int k = 0; k < 4; ++k) v[k] = odd ? tw[7 - 2 * k] : tw[6 - 2 * k];
+            for (int k = 0; k < 4; ++k) v[k] = bsel(pk.m, tw[7 - 2 * k], tw[6 - 2 * k]);
             v[4] = dsel[1];
             v[5] = dsel[0];
-            v[6] = odd ? pv[3] : pv[2];
-            v[7] = odd ? pv[1] : pv[0];
-            pair_schedule8<8>(v, odd, kw1hi_col);
+            v[6] = bsel(pk.m, pv[3], pv[2]);
+            v[7] = bsel(pk.m, pv[1], pv[0]);
+            pair_schedule8<8>(v, pk, kw1hi_col);
             __syncthreads();
-            pair_schedule8<16>(v, odd, kw1hi_col);
+            pair_schedule8<16>(v, pk, kw1hi_col);
             __syncthreads();
-            pair_schedule8<24>(v, odd, kw1hi_col);
+            pair_schedule8<24>(v, pk, kw1hi_col);
             __syncthreads();
 #pragma unroll
             for (int q = 0; q < 8; ++q) tk[q] = pre[q];        // the next key's token-only data
             load_tokens_pair(tp, i + 2, n, odd, pre);
-            produce_key_pair(sh, c, odd, buf ^ 1, tk);
+            produce_key_pair(sh, c, odd, pk, buf ^ 1, tk);
             __syncthreads();                                   // end of key
         }
     }
@@ -689,8 +770,8 @@ __device__ __forceinline__ void load_production_pair(const int32_t* tp, uint32_t
 // parity of the schedule (pair_schedule8) and writes its K + W words into the slot; for c == 1
 // also its parity of compression 1's token words.
 template <typename Shared>
-__device__ __forceinline__ void produce_comp_pair(Shared& sh, uint32_t chain, bool odd, uint32_t m, uint32_t bitlen,
-                                                  int64_t g, const PairProduction& pr) {
+__device__ __forceinline__ void produce_comp_pair(Shared& sh, uint32_t chain, bool odd, const PairK& pk, uint32_t m,
+                                                  uint32_t bitlen, int64_t g, const PairProduction& pr) {
     const int64_t key = g / m;
     const uint32_t c = static_cast<uint32_t>(g - key * m) + 1;
     const uint32_t o = odd ? 1u : 0u;
@@ -701,7 +782,7 @@ __device__ __forceinline__ void produce_comp_pair(Shared& sh, uint32_t chain, bo
 #pragma unroll
         for (int k = 0; k < 4; ++k) {                  // message word 8 + 2k + odd of compression 1
             const uint32_t x = bswap(pr.head[k]);
-            const uint32_t kk = odd ? kRoundK[8 + 2 * k + 1] : kRoundK[8 + 2 * k];
+            const uint32_t kk = pk.k[4 + k];
             wcol[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = x;
             kcol[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = x + kk;
         }
@@ -713,23 +794,20 @@ __device__ __forceinline__ void produce_comp_pair(Shared& sh, uint32_t chain, bo
     } else {                                           // words 8..15: 0x80000000, zeros, the bit length
 #pragma unroll
         for (int k = 0; k < 4; ++k) own[k] = bswap(pr.w[k]);
-        own[4] = odd ? 0u : 0x80000000u;
+        own[4] = ~pk.m & 0x80000000u;
         own[5] = 0u;
         own[6] = 0u;
-        own[7] = odd ? bitlen : 0u;
+        own[7] = pk.m & bitlen;
     }
     uint32_t* col = reinterpret_cast<uint32_t*>(&sh.kwt[static_cast<int>(g % 3)][0][chain]) + o;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-        const uint32_t kk = odd ? kRoundK[2 * k + 1] : kRoundK[2 * k];
-        col[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = own[k] + kk;
-    }
+    for (int k = 0; k < 8; ++k) col[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = own[k] + pk.k[k];
     uint32_t v[8];                                     // own words, newest first
 #pragma unroll
     for (int k = 0; k < 8; ++k) v[k] = own[7 - k];
-    pair_schedule8<8, 0>(v, odd, col);
-    pair_schedule8<16, 0>(v, odd, col);
-    pair_schedule8<24, 0>(v, odd, col);
+    pair_schedule8<8, 0>(v, pk, col);
+    pair_schedule8<16, 0>(v, pk, col);
+    pair_schedule8<24, 0>(v, pk, col);
 }
 
 struct PpmShared {
@@ -843,12 +921,13 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
         dsel[0] = odd ? dg[1] : dg[0];
         dsel[1] = odd ? dg[3] : dg[2];
         uint32_t* kw1hi_col = reinterpret_cast<uint32_t*>(&sh.kw1hi[0][c]) + (odd ? 1 : 0);
+        const PairK pk = make_pair_k(odd);
         const int64_t total = nmax * m;                        // token compressions of the workgroup
         PairProduction p0, p1, p2;
         load_production_pair(tp, B, m, n, 0, odd, p0);
         load_production_pair(tp, B, m, n, 1, odd, p1);
-        produce_comp_pair(sh, c, odd, m, bitlen, 0, p0);
-        produce_comp_pair(sh, c, odd, m, bitlen, 1, p1);
+        produce_comp_pair(sh, c, odd, pk, m, bitlen, 0, p0);
+        produce_comp_pair(sh, c, odd, pk, m, bitlen, 1, p1);
         load_production_pair(tp, B, m, n, 2, odd, p0);         // p0, p1 = productions g + 2, g + 3
         load_production_pair(tp, B, m, n, 3, odd, p1);
         __syncthreads();                                       // prologue
@@ -859,16 +938,16 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
             get4(&sh.w1tok[kb][0][c], tw);
             get4(&sh.w1tok[kb][1][c], tw + 4);
 #pragma unroll
-            for (int k = 0; k < 4; ++k) v[k] = odd ? tw[7 - 2 * k] : tw[6 - 2 * k];
+            for (int k = 0; k < 4; ++k) v[k] = bsel(pk.m, tw[7 - 2 * k], tw[6 - 2 * k]);
             v[4] = dsel[1];
             v[5] = dsel[0];
-            v[6] = odd ? pv[3] : pv[2];
-            v[7] = odd ? pv[1] : pv[0];
-            pair_schedule8<8>(v, odd, kw1hi_col);
+            v[6] = bsel(pk.m, pv[3], pv[2]);
+            v[7] = bsel(pk.m, pv[1], pv[0]);
+            pair_schedule8<8>(v, pk, kw1hi_col);
             __syncthreads();
-            pair_schedule8<16>(v, odd, kw1hi_col);
+            pair_schedule8<16>(v, pk, kw1hi_col);
             __syncthreads();
-            pair_schedule8<24>(v, odd, kw1hi_col);
+            pair_schedule8<24>(v, pk, kw1hi_col);
             __syncthreads();
             __syncthreads();                                   // end of compression 1
             for (uint32_t cc = 1; cc <= m; ++cc) {
@@ -876,7 +955,7 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
                 p2 = p0;
                 p0 = p1;
                 load_production_pair(tp, B, m, n, g + 2, odd, p1);
-                if (g < total) produce_comp_pair(sh, c, odd, m, bitlen, g, p2);
+                if (g < total) produce_comp_pair(sh, c, odd, pk, m, bitlen, g, p2);
                 __syncthreads();                               // end of token compression cc
             }
         }
