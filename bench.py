@@ -55,7 +55,7 @@ DERIVE_SOURCES = ["paper_2609_38706_amd/csrc/k_derive.hip", "paper_2609_38706_am
 LOOKUP_SOURCES = ["paper_2609_38706_amd/csrc/k_table.hip", "paper_2609_38706_amd/csrc/pkv_internal.h"]
 HBM_PEAK = 8.0e12             # MI355X HBM3E, bytes/s
 EVENT_STRIDE = 10             # derive launches of the timed region between two timed ones
-BYTES_PER_PROBE = 80          # one 64-byte bucket + the 16-byte probe key
+BYTES_PER_PROBE = 80          # the key bytes of one 4-slot bucket (64) + the 16-byte probe key
 
 
 def measured_traffic(workload: str, kernel: str = "derive"):

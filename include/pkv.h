@@ -37,10 +37,10 @@
  *   - Locations are caller-defined 64-bit values below PKV_LOC_LIMIT (the top two bits are
  *     reserved for the insert protocol).
  *   - Device errors leave the index contents unspecified.
- *   - Index layout (pkv_table): keys = capacity x 16 bytes (64-byte aligned, capacity a power of
- *     two >= 4), locs = capacity + 2 uint64 words.  Two key byte patterns are reserved to mark free
- *     key slots (all 0xFF: never used; all 0xFF with a last byte 0xFE: removed by eviction); a key
- *     equal to either keeps its location in locs[capacity] / locs[capacity + 1] and does not count
+ *   - Index layout (pkv_table): one device buffer of pkv_table_bytes(capacity) bytes, 128-byte
+ *     aligned, capacity a power of two in [4, 2^56].  Slots are indexed 0 .. capacity - 1; two more
+ *     slot indices, capacity and capacity + 1, belong to the two reserved key byte patterns (all
+ *     0xFF; all 0xFF with a last byte 0xFE), which keep their locations apart and do not count
  *     against the capacity.  A fixed-budget tier adds an epochs array of capacity + 2 uint32.
  */
 #ifndef PKV_H
@@ -78,18 +78,22 @@ typedef struct {
     uint32_t value_len;
 } pkv_field;
 
-/* The shared-tier index (section 2.1 shared KV-cache tier): open addressing over 4-slot
- * buckets of 64 bytes, struct-of-arrays in HBM.
- *   keys     : capacity x 16 bytes, 64-byte aligned.
- *   locs     : capacity + 2 words (the two extra words serve the keys that equal the two
- *              reserved patterns: all 0xFF, and all 0xFF with a last byte 0xFE).
- *   capacity : a power of two, >= 4.
- * The struct itself is host memory; the arrays are device memory owned by the caller. */
+/* The shared-tier index (section 2.1 shared KV-cache tier): open addressing over buckets of four
+ * slots, one 128-byte bucket per HBM line.  Bucket b covers slots 4b .. 4b + 3 and holds, in order:
+ * the four slots' claim words (the first 8 key bytes, or a free-slot marker), four flag words, and
+ * four 16-byte pairs {key bytes 8..15, location}.  A 64-byte tail after the last bucket holds the
+ * locations of the two reserved keys.  A key's home bucket is its first 8 bytes (little-endian)
+ * modulo the bucket count; probing is linear over slots.
+ *   slots    : pkv_table_bytes(capacity) bytes of device memory, 128-byte aligned.
+ *   capacity : a power of two in [4, 2^56].
+ * The struct itself is host memory; the buffer is device memory owned by the caller. */
 typedef struct {
-    uint8_t* keys;
-    uint64_t* locs;
+    uint8_t* slots;
     uint64_t capacity;
 } pkv_table;
+/* Bytes of index memory for `capacity` slots (32 per slot plus the 64-byte tail), or 0 when the
+ * capacity is not a power of two in [4, 2^56]. */
+uint64_t pkv_table_bytes(uint64_t capacity);
 
 /* ---- host, pure, thread-safe ------------------------------------------------------------- */
 

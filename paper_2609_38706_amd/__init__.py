@@ -18,7 +18,7 @@ ERROR_NAMES = {0: "PKV_OK", -1: "PKV_EINVAL", -2: "PKV_EDUPDIM", -3: "PKV_ERESER
                -5: "PKV_EHIP", -6: "PKV_ELAYOUT", -7: "PKV_ESTALL"}
 
 EXPORTED = ["pkv_descriptor_encode", "pkv_descriptor_digest", "pkv_digest_batch", "pkv_key_offsets",
-            "pkv_derive_keys", "pkv_table_init", "pkv_lookup_prefix", "pkv_store", "pkv_table_rollback",
+            "pkv_derive_keys", "pkv_table_bytes", "pkv_table_init", "pkv_lookup_prefix", "pkv_store", "pkv_table_rollback",
             "pkv_table_export", "pkv_sum_hits", "pkv_lookup_prefix_touch", "pkv_store_touch",
             "pkv_table_evict", "pkv_tree_work_bytes", "pkv_tensor_roots", "pkv_content_identity",
             "pkv_last_error", "pkv_version"]
@@ -38,7 +38,7 @@ class pkv_field(ctypes.Structure):
 
 
 class pkv_table(ctypes.Structure):
-    _fields_ = [("keys", ctypes.c_void_p), ("locs", ctypes.c_void_p), ("capacity", ctypes.c_uint64)]
+    _fields_ = [("slots", ctypes.c_void_p), ("capacity", ctypes.c_uint64)]
 
 
 _lib = None
@@ -76,6 +76,8 @@ def lib() -> ctypes.CDLL:
             f.restype = I32
         L.pkv_tree_work_bytes.argtypes = [U64, U32]
         L.pkv_tree_work_bytes.restype = U64
+        L.pkv_table_bytes.argtypes = [U64]
+        L.pkv_table_bytes.restype = U64
         L.pkv_last_error.restype = ctypes.c_char_p
         L.pkv_version.restype = ctypes.c_char_p
         _lib = L
@@ -158,28 +160,30 @@ def pkv_derive_keys(tokens, tok_off, digests, block, key_off, keys, status, stre
 
 
 class Table:
-    """Device arrays of one index: ``keys`` uint8 [capacity, 16], ``locs`` int64 [capacity + 2];
-    with ``epochs=True`` also ``epochs`` int32 [capacity + 2] (the fixed-budget tier) and the
-    eviction work area."""
+    """Device memory of one index: ``slots`` uint8 [pkv_table_bytes(capacity)] (128-byte buckets of
+    four slots and a 64-byte tail, see include/pkv.h); with ``epochs=True`` also ``epochs`` int32
+    [capacity + 2] (the fixed-budget tier) and the eviction work area."""
 
     def __init__(self, capacity: int, device="cuda", init=True, stream=None, epochs=False):
         import torch
-        if capacity < 4 or capacity & (capacity - 1):
-            raise ValueError("capacity must be a power of two >= 4")
+        nbytes = int(lib().pkv_table_bytes(capacity))
+        if nbytes == 0:
+            raise ValueError("capacity must be a power of two in [4, 2^56]")
         self.capacity = capacity
-        self.keys = torch.empty((capacity, 16), dtype=torch.uint8, device=device)
-        self.locs = torch.empty(capacity + 2, dtype=torch.int64, device=device)
+        # torch's caching allocator hands out blocks aligned to at least 512 bytes
+        self.slots = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        if self.slots.data_ptr() % 128:
+            raise RuntimeError("index memory is not 128-byte aligned")
         self.epochs = torch.zeros(capacity + 2, dtype=torch.int32, device=device) if epochs else None
         self.work = torch.empty(EVICT_WORK_BYTES // 8, dtype=torch.int64, device=device) if epochs else None
         if init:
             pkv_table_init(self, stream)
 
     def struct(self) -> pkv_table:
-        return pkv_table(self.keys.data_ptr(), self.locs.data_ptr(), self.capacity)
+        return pkv_table(self.slots.data_ptr(), self.capacity)
 
     def copy_from(self, other: "Table"):
-        self.keys.copy_(other.keys)
-        self.locs.copy_(other.locs)
+        self.slots.copy_(other.slots)
         if self.epochs is not None and other.epochs is not None:
             self.epochs.copy_(other.epochs)
 

@@ -139,14 +139,14 @@ bool bytes_less(const uint8_t* a, size_t na, const uint8_t* b, size_t nb) {
 
 int check_table(const pkv_table* t, const char* what) {
     if (!t) return set_error(PKV_EINVAL, "%s: null table", what);
-    if (!t->keys || !t->locs) return set_error(PKV_EINVAL, "%s: null table arrays", what);
-    if (!pow2(t->capacity) || t->capacity < kSlotsPerBucket)
-        return set_error(PKV_EINVAL, "%s: capacity %llu is not a power of two >= 4", what,
+    if (!t->slots) return set_error(PKV_EINVAL, "%s: null table memory", what);
+    if (!pow2(t->capacity) || t->capacity < kSlotsPerBucket || t->capacity > (1ull << 56))
+        return set_error(PKV_EINVAL, "%s: capacity %llu is not a power of two in [4, 2^56]", what,
                          static_cast<unsigned long long>(t->capacity));
-    if (!aligned(t->keys, 64)) return set_error(PKV_EINVAL, "%s: table keys not 64-byte aligned", what);
-    if (!aligned(t->locs, 8)) return set_error(PKV_EINVAL, "%s: table locations not 8-byte aligned", what);
+    if (!aligned(t->slots, 128)) return set_error(PKV_EINVAL, "%s: table memory not 128-byte aligned", what);
     return PKV_OK;
 }
+uint64_t* table_words(const pkv_table* t) { return reinterpret_cast<uint64_t*>(t->slots); }
 }  // namespace
 
 int set_error(int code, const char* fmt, ...) {
@@ -243,10 +243,15 @@ int pkv_derive_keys(const int32_t* d_tokens, uint64_t n_tokens, const int64_t* d
                          stream);
 }
 
+uint64_t pkv_table_bytes(uint64_t capacity) {
+    if (!pow2(capacity) || capacity < kSlotsPerBucket || capacity > (1ull << 56)) return 0;
+    return capacity * 32 + 64;
+}
+
 int pkv_table_init(const pkv_table* table, hipStream_t stream) {
     int rc = check_table(table, "pkv_table_init");
     if (rc) return rc;
-    return launch_table_init(table->keys, table->locs, table->capacity, stream);
+    return launch_table_init(table_words(table), table->capacity, stream);
 }
 
 int pkv_lookup_prefix(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off, uint32_t n_req,
@@ -257,7 +262,7 @@ int pkv_lookup_prefix(const pkv_table* table, const uint8_t* d_keys, const int64
     if ((!d_keys && n_keys) || !d_key_off || !d_hit_blocks || !d_status)
         return set_error(PKV_EINVAL, "pkv_lookup_prefix: null argument");
     if (!aligned(d_keys, 16)) return set_error(PKV_EINVAL, "pkv_lookup_prefix: keys not 16-byte aligned");
-    return launch_lookup(table->keys, table->locs, table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
+    return launch_lookup(table_words(table), table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
                          nullptr, 0, d_status, stream);
 }
 
@@ -270,7 +275,7 @@ int pkv_lookup_prefix_touch(const pkv_table* table, const uint8_t* d_keys, const
     if ((!d_keys && n_keys) || !d_key_off || !d_hit_blocks || !d_status || !d_epochs)
         return set_error(PKV_EINVAL, "pkv_lookup_prefix_touch: null argument");
     if (!aligned(d_keys, 16)) return set_error(PKV_EINVAL, "pkv_lookup_prefix_touch: keys not 16-byte aligned");
-    return launch_lookup(table->keys, table->locs, table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
+    return launch_lookup(table_words(table), table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
                          d_epochs, epoch, d_status, stream);
 }
 
@@ -283,7 +288,7 @@ int pkv_store(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_ke
     if ((!d_keys && n_keys) || !d_key_off || !d_hit_blocks || (!d_locs && n_keys) || !d_n_new || !d_status)
         return set_error(PKV_EINVAL, "pkv_store: null argument");
     if (!aligned(d_keys, 16)) return set_error(PKV_EINVAL, "pkv_store: keys not 16-byte aligned");
-    return launch_store(table->keys, table->locs, table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
+    return launch_store(table_words(table), table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
                         d_locs, d_new_slots, d_n_new, nullptr, 0, d_status, stream);
 }
 
@@ -297,7 +302,7 @@ int pkv_store_touch(const pkv_table* table, const uint8_t* d_keys, const int64_t
         !d_epochs)
         return set_error(PKV_EINVAL, "pkv_store_touch: null argument");
     if (!aligned(d_keys, 16)) return set_error(PKV_EINVAL, "pkv_store_touch: keys not 16-byte aligned");
-    return launch_store(table->keys, table->locs, table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
+    return launch_store(table_words(table), table->capacity, d_keys, d_key_off, n_req, n_keys, d_hit_blocks,
                         d_locs, d_new_slots, d_n_new, d_epochs, epoch, d_status, stream);
 }
 
@@ -307,7 +312,7 @@ int pkv_table_evict(const pkv_table* table, const uint32_t* d_epochs, uint64_t b
     if (rc) return rc;
     if (!d_epochs || !d_work || !d_n_evicted) return set_error(PKV_EINVAL, "pkv_table_evict: null argument");
     if (!aligned(d_work, 8)) return set_error(PKV_EINVAL, "pkv_table_evict: work area not 8-byte aligned");
-    return launch_evict(table->keys, table->locs, table->capacity, d_epochs, budget, static_cast<uint32_t*>(d_work),
+    return launch_evict(table_words(table), table->capacity, d_epochs, budget, static_cast<uint32_t*>(d_work),
                         d_n_evicted, stream);
 }
 
@@ -316,7 +321,7 @@ int pkv_table_rollback(const pkv_table* table, const uint64_t* d_new_slots, cons
     int rc = check_table(table, "pkv_table_rollback");
     if (rc) return rc;
     if (max_slots && (!d_new_slots || !d_n_new)) return set_error(PKV_EINVAL, "pkv_table_rollback: null argument");
-    return launch_rollback(table->keys, table->locs, table->capacity, d_new_slots, d_n_new, max_slots, stream);
+    return launch_rollback(table_words(table), table->capacity, d_new_slots, d_n_new, max_slots, stream);
 }
 
 int pkv_table_export(const pkv_table* table, uint8_t* d_keys_out, uint64_t* d_locs_out, uint64_t* d_count,
@@ -325,7 +330,7 @@ int pkv_table_export(const pkv_table* table, uint8_t* d_keys_out, uint64_t* d_lo
     if (rc) return rc;
     if (!d_keys_out || !d_locs_out || !d_count) return set_error(PKV_EINVAL, "pkv_table_export: null argument");
     if (!aligned(d_keys_out, 16)) return set_error(PKV_EINVAL, "pkv_table_export: output keys not 16-byte aligned");
-    return launch_export(table->keys, table->locs, table->capacity, d_keys_out, d_locs_out, d_count, stream);
+    return launch_export(table_words(table), table->capacity, d_keys_out, d_locs_out, d_count, stream);
 }
 
 int pkv_sum_hits(const int32_t* d_hit_blocks, uint32_t n_req, const int64_t* d_group_off, uint32_t n_groups,

@@ -1,23 +1,25 @@
 // k_table.hip -- the shared-tier index in HBM: init, longest-prefix lookup, store of misses,
 // rollback, export and eviction to a budget, on gfx950.
 //
-// Layout: struct of arrays.  keys[capacity] (16 bytes each) grouped in 4-slot buckets, so one
-// bucket is one 64-byte segment; locs[capacity + 2] (8 bytes each), the two extra words holding
-// the locations of the two reserved key patterns (all 0xFF marks an empty key slot, all 0xFF with
-// a last byte 0xFE a removed one).  A key's home bucket is its first eight bytes masked to the
-// bucket count; probing is linear over slots, wrapping.  A fixed-budget tier adds epochs[capacity
-// + 2] (uint32): the epoch of each entry's last use.
+// Layout (pkv_internal.h): 128-byte buckets of 4 slots.  A bucket holds the four slots' claim words
+// (each the first 8 bytes of the slot's key, or a marker), their flag words, and for each slot one
+// 16-byte pair {key bytes 8..15, location word}; a 64-byte tail holds the location words of the
+// two reserved keys.  A key's home bucket is its first eight bytes masked to the bucket count;
+// probing is linear over slots, wrapping.  A fixed-budget tier adds epochs[capacity + 2] (uint32):
+// the epoch of each entry's last use.
 //
-// Lookup reads only key slots: a key is present iff some slot on its probe path holds it, and
-// absent once the path meets an empty slot (removed slots carry a pattern no probe key equals,
-// so paths run through them).  Store drives a per-slot state machine in the location word with
-// 64-bit atomics (gfx950 has no 128-bit compare-and-swap):
-//   empty or removed --CAS--> pending --(write key, wait, publish)--> location | fresh
-// A lane first scans its key's path up to the first empty slot, remembering the first removed
-// slot; it then claims that slot (or the empty one).  A lane that meets a pending slot re-reads it
-// until it is published, then compares keys, so two lanes inserting one key always meet in the
-// same slot.  A later equal key lowers a fresh entry's location with atomic min; entries older
-// than the batch carry no fresh bit and are left untouched.  A final pass clears the fresh bits.
+// Lookup reads whole buckets: a key is present iff some slot on its probe path holds it, and absent
+// once the path meets a never-used slot (removed slots have their own claim marker, so paths run
+// through them).  Store claims a slot with one 64-bit compare-and-swap on its claim word and then
+// writes the slot's {key bytes 8..15, location} pair with one 16-byte store, inside the same
+// 128-byte bucket (gfx950 has no 128-bit compare-and-swap):
+//   never used or removed --CAS claim word--> claimed, location kEmpty --16-byte store--> published
+// A lane first scans its key's path up to the first never-used slot, remembering the first removed
+// slot; it then claims that slot (or the never-used one).  A lane that meets a slot claimed with
+// its own claim word but not yet published re-reads it until it is, then compares the rest of the
+// key, so two lanes inserting one key always meet in the same slot.  A later equal key lowers a
+// fresh entry's location with atomic min; entries older than the batch carry no fresh bit and are
+// left untouched.  A final pass clears the fresh bits.
 #include "pkv_internal.h"
 
 namespace pkv {
@@ -25,10 +27,9 @@ namespace {
 
 using dev::eq4;
 using dev::home_bucket;
-using dev::is_marker;
 using dev::report;
 
-constexpr uint32_t kWaitLimit = 1u << 20;      // re-reads of one pending slot before giving up
+constexpr uint32_t kWaitLimit = 1u << 20;      // re-reads of one claimed slot before giving up
 
 __device__ __forceinline__ bool cas_relaxed(uint64_t* p, uint64_t expected, uint64_t desired) {
     return __hip_atomic_compare_exchange_strong(p, &expected, desired, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
@@ -37,63 +38,124 @@ __device__ __forceinline__ bool cas_relaxed(uint64_t* p, uint64_t expected, uint
 __device__ __forceinline__ void min_relaxed(uint64_t* p, uint64_t v) {
     __hip_atomic_fetch_min(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ uint64_t load_relaxed(uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_relaxed(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 __device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
 
+// The two 8-byte halves of a key as little-endian words, and the claim and flag words that stand
+// for its first half in a slot.
+struct KeyWords {
+    uint64_t lo, hi;
+    uint64_t claim, flag;
+};
+__device__ __forceinline__ KeyWords key_words(const uint4& k) {
+    KeyWords w;
+    w.lo = (static_cast<uint64_t>(k.y) << 32) | k.x;
+    w.hi = (static_cast<uint64_t>(k.w) << 32) | k.z;
+    w.flag = w.lo == kLoEmpty ? 1u : (w.lo == kLoRemoved ? 2u : 0u);
+    w.claim = w.flag ? kLoSub : w.lo;
+    return w;
+}
+
+// Device-coherent 16-byte access to a slot's {key bytes 8..15, location} pair.  The sc1 bit gives
+// the same agent-scope coherence that the compiler uses for relaxed agent-scope atomics (the
+// access bypasses the non-coherent part of the XCD's L2), for both words in one memory operation.
+// Each statement waits for its own access (vmcnt 0), so the compiler need not track it.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void load_pair_coherent(const uint64_t* p, uint64_t& hi, uint64_t& loc) {
+    u32x4 v;
+    asm volatile("global_load_dwordx4 %0, %1, off sc1\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(p) : "memory");
+    hi = (static_cast<uint64_t>(v.y) << 32) | v.x;
+    loc = (static_cast<uint64_t>(v.w) << 32) | v.z;
+}
+
+__device__ __forceinline__ void store_pair_coherent(uint64_t* p, uint64_t hi, uint64_t loc) {
+    const u32x4 v = {static_cast<uint32_t>(hi), static_cast<uint32_t>(hi >> 32), static_cast<uint32_t>(loc),
+                     static_cast<uint32_t>(loc >> 32)};
+    asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_waitcnt vmcnt(0)" : : "v"(p), "v"(v) : "memory");
+}
+
 // ---- init -------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_init(uint4* keys, uint64_t* locs, uint64_t capacity) {
+// Claim words all ones, flag words zero, pairs {all ones, kEmpty}; the tail all ones.
+__global__ __launch_bounds__(256) void k_init(uint4* t, uint64_t capacity) {
+    const uint64_t n = capacity * 2 + 4;                 // 16-byte units: 8 per bucket, 4 in the tail
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
-    const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
-    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i <= capacity + 1; i += stride) {
-        if (i < capacity) keys[i] = marker;
-        locs[i] = kEmpty;
+    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
+        const bool flags = i < capacity * 2 && ((i & 7) == 2 || (i & 7) == 3);
+        t[i] = flags ? make_uint4(0u, 0u, 0u, 0u) : make_uint4(~0u, ~0u, ~0u, ~0u);
     }
 }
 
 // ---- lookup: one wavefront per request --------------------------------------------------------
-// A request's keys are probed in windows, one lane per key; a lane loads its key's whole 64-byte
-// bucket with four 16-byte loads issued together, and the next window's keys are fetched while
-// the current window's buckets are in flight.  A ballot finds the first absent key, which ends the
-// request.  The first window holds LOOKUP_FIRST keys and each later window twice as many, up to
-// 64: probes past a request's first miss are wasted bandwidth, so short prefixes (and misses on
-// the first key) probe few keys, while long prefixes soon reach full 64-key windows.
+// A request's keys are probed in windows, one lane per key; a lane loads its key's bucket (the
+// four claim words and the four pairs: six 16-byte loads issued together, 96 of its 128 bytes),
+// and the next window's keys are fetched while the current window's buckets are in flight.  A
+// ballot finds the first absent key, which ends the request.  The first window holds
+// LOOKUP_FIRST keys and each later window twice as many, up to 64: probes past a request's first
+// miss are wasted bandwidth, so short prefixes (and misses on the first key) probe few keys,
+// while long prefixes soon reach full 64-key windows.
 #ifndef PKV_LOOKUP_FIRST
 #define PKV_LOOKUP_FIRST 16
 #endif
 constexpr int kLookupWaves = 4;
 constexpr uint32_t kFirstWindow = PKV_LOOKUP_FIRST;
 
-// Probe of one key (lane-private): bucket slots already loaded in sl[0..3].  Returns the slot
-// holding the key, or -1 when it is absent; continues to later buckets while a full bucket
-// neither matches nor ends the path.
-__device__ __forceinline__ int64_t probe_key(const uint4* __restrict__ tkeys, const uint64_t* __restrict__ tlocs,
-                                             uint64_t capacity, uint64_t bmask, const uint4& key, uint64_t b,
-                                             uint4 sl[4]) {
+struct Bucket {
+    uint4 c[2];      // claim words 0-1, 2-3
+    uint4 p[4];      // pair j: {key bytes 8..15, location}
+};
+
+__device__ __forceinline__ void load_bucket(const uint4* __restrict__ t, uint64_t b, Bucket& bk) {
+    const uint4* q = t + b * (kBucketWords / 2);
+    bk.c[0] = q[0];
+    bk.c[1] = q[1];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bk.p[j] = q[4 + j];
+}
+
+// Probe of one key (lane-private) whose home bucket is already loaded in bk.  Returns the slot
+// holding the key, or -1 when it is absent; continues to later buckets while a bucket neither
+// matches nor holds a never-used slot.
+__device__ __forceinline__ int64_t probe_key(const uint4* __restrict__ t, uint64_t capacity, uint64_t bmask,
+                                             const uint4& key, uint64_t b, Bucket& bk) {
+    const uint64_t* w = reinterpret_cast<const uint64_t*>(t);
     const uint64_t rs = dev::reserved_slot(key, capacity);
-    if (rs) return tlocs[rs] != kEmpty ? static_cast<int64_t>(rs) : -1;
+    if (rs) return w[capacity * 4 + (rs - capacity)] != kEmpty ? static_cast<int64_t>(rs) : -1;
+    const KeyWords kw = key_words(key);
     const uint64_t n_buckets = bmask + 1;
     for (uint64_t it = 0; it < n_buckets; ++it) {
         bool empty = false;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            if (eq4(sl[j], key)) return static_cast<int64_t>(b * kSlotsPerBucket + j);
-            empty |= is_marker(sl[j]);
+            const uint4 cw = bk.c[j >> 1];
+            const uint64_t claim = (j & 1) ? ((static_cast<uint64_t>(cw.w) << 32) | cw.z)
+                                           : ((static_cast<uint64_t>(cw.y) << 32) | cw.x);
+            const uint64_t hi = (static_cast<uint64_t>(bk.p[j].y) << 32) | bk.p[j].x;
+            const uint64_t loc = (static_cast<uint64_t>(bk.p[j].w) << 32) | bk.p[j].z;
+            const uint64_t s = b * kSlotsPerBucket + j;
+            if (claim == kw.claim && hi == kw.hi && loc != kEmpty &&
+                (kw.claim != kLoSub || w[b * kBucketWords + 4 + j] == kw.flag))
+                return static_cast<int64_t>(s);
+            empty |= claim == kLoEmpty;
         }
         if (empty) return -1;
         b = (b + 1) & bmask;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sl[j] = tkeys[b * kSlotsPerBucket + j];
+        load_bucket(t, b, bk);
     }
     return -1;
 }
 
-__global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __restrict__ tkeys,
-                                                            const uint64_t* __restrict__ tlocs, uint64_t capacity,
+__global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __restrict__ t, uint64_t capacity,
                                                             const uint4* __restrict__ keys,
                                                             const int64_t* __restrict__ key_off, uint32_t n_req,
                                                             uint64_t n_keys, int32_t* __restrict__ hits,
-                                                            uint32_t* __restrict__ epochs, uint32_t epoch,
-                                                            int32_t* status) {
+                                                            uint32_t* epochs, uint32_t epoch, int32_t* status) {
     const uint32_t lane = lane_id();
     const uint32_t r = blockIdx.x * kLookupWaves + (threadIdx.x >> 6);
     if (r >= n_req) return;
@@ -128,16 +190,13 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
         const uint4 ck = nk;
         const bool v = lane < width && base + lane < n;
         const uint64_t bk = home_bucket(ck, bmask);
-        uint4 sl[4];
-        if (v) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) sl[j] = tkeys[bk * kSlotsPerBucket + j];
-        }
+        Bucket bucket;
+        if (v) load_bucket(t, bk, bucket);
         // next window: twice as wide, up to the wavefront
         const uint32_t next_width = width * 2 < 64 ? width * 2 : 64;
         const int64_t next_base = base + width;
         nk = key_at(next_base + lane, lane < next_width);
-        const int64_t fslot = v ? probe_key(tkeys, tlocs, capacity, bmask, ck, bk, sl) : -1;
+        const int64_t fslot = v ? probe_key(t, capacity, bmask, ck, bk, bucket) : -1;
         const uint64_t miss = __ballot(v && fslot < 0);
         const int64_t stop = miss ? base + __builtin_ctzll(miss) : -1;
         if (epochs && fslot >= 0 && (stop < 0 || base + lane < stop))   // a touching lookup refreshes hits
@@ -157,9 +216,7 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
 // covers 64 consecutive keys: one (wave-uniform) binary search finds the request of its first
 // key, and each lane walks forward over the few request boundaries inside the wavefront.
 struct StoreArgs {
-    uint4* tkeys;
-    uint64_t* tlocs;
-    uint64_t capacity;
+    Tab t;
     const uint4* keys;
     const int64_t* key_off;
     uint32_t n_req;
@@ -193,53 +250,26 @@ __device__ __forceinline__ uint64_t wave_base_of(uint32_t block_threads) {
     return static_cast<uint64_t>(blockIdx.x) * block_threads + wave * 64ull;
 }
 
-// Device-coherent 16-byte accesses to one key slot.  The sc1 bit gives the same agent-scope
-// coherence that the compiler uses for relaxed agent-scope atomics (the access bypasses the
-// non-coherent part of the XCD's L2), for all 16 bytes in one memory operation instead of two
-// 8-byte ones.  Each statement waits for its own access (vmcnt 0), so the result is in place when
-// it returns and the compiler need not track the access.
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ uint4 load_key_coherent(const uint4* p) {
-    u32x4 v;
-    asm volatile("global_load_dwordx4 %0, %1, off sc1\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(p) : "memory");
-    return make_uint4(v.x, v.y, v.z, v.w);
-}
-
-__device__ __forceinline__ void store_key_coherent(uint4* p, const uint4& k) {
-    const u32x4 v = {k.x, k.y, k.z, k.w};
-    asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_waitcnt vmcnt(0)" : : "v"(p), "v"(v) : "memory");
-}
-
-// Key bytes of a slot whose location word was seen published.  During one store launch a key
-// slot only ever holds a marker pattern (empty or removed) or its final key, so a key whose
-// 8-byte halves match neither marker's half is final.  One that does is re-read after an acquire
-// fence: either it really has that value, or the read was stale.
-constexpr uint64_t kTombHi = (static_cast<uint64_t>(kTombW) << 32) | 0xFFFFFFFFull;
-
-__device__ __forceinline__ uint4 read_slot_key(uint4* tkeys, uint64_t s) {
-    uint4 k = load_key_coherent(tkeys + s);
-    const uint64_t lo = (static_cast<uint64_t>(k.y) << 32) | k.x, hi = (static_cast<uint64_t>(k.w) << 32) | k.z;
-    if (lo == ~0ull || hi == ~0ull || hi == kTombHi) {
+// The pair of a slot whose claim word matched and whose location word is published.  The pair is
+// written by one 16-byte store after the claim; a first half that still reads as the value every
+// free slot holds (all ones) is re-read after an acquire fence, in case the read was stale.
+__device__ __forceinline__ void read_published_pair(const uint64_t* p, uint64_t& hi, uint64_t& loc) {
+    load_pair_coherent(p, hi, loc);
+    if (hi == ~0ull && loc != kEmpty) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        k = load_key_coherent(tkeys + s);
+        load_pair_coherent(p, hi, loc);
     }
-    return k;
 }
 
-// Writes a claimed slot's key and then publishes its location word.  The key is one 16-byte
-// device-coherent store, complete (vmcnt 0) before the location store is issued, so any lane that
-// reads the published location word afterwards reads the final key.  This is the gfx950
-// agent-scope release without its L2 writeback: that writeback exists for preceding non-atomic
-// stores, and none precede the publication here.  The asm statement's memory clobber keeps the
-// compiler from moving the stores across each other.
-__device__ __forceinline__ void publish_slot(uint4* tkeys, uint64_t* tlocs, uint64_t s, const uint4& k, uint64_t v) {
-    store_key_coherent(tkeys + s, k);
-    __hip_atomic_store(tlocs + s, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ uint64_t load_relaxed(uint64_t* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Publishes a claimed slot: a substitute claim word first gets its flag word (complete before the
+// pair is written, so a lane that sees the published location reads the final flag), then the
+// pair {key bytes 8..15, location} is written with one 16-byte store.
+__device__ __forceinline__ void publish_slot(const Tab& t, uint64_t s, const KeyWords& kw, uint64_t v) {
+    if (kw.flag) {
+        store_relaxed(t.flag(s), kw.flag);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    store_pair_coherent(t.pair(s), kw.hi, v);
 }
 
 constexpr uint32_t kStoreThreads = 256;
@@ -252,6 +282,7 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
         if (k == 0) report(a.status, PKV_ELAYOUT);
         return;
     }
+    const Tab& t = a.t;
     bool active = candidate(a, wave_base, k, total);
     uint64_t want = 0;
     uint4 key = make_uint4(0, 0, 0, 0);
@@ -266,10 +297,10 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
     }
     bool claimed = false;
     uint64_t my_slot = 0;
-    const uint64_t rs = active ? dev::reserved_slot(key, a.capacity) : 0;
+    const uint64_t rs = active ? dev::reserved_slot(key, t.capacity) : 0;
     if (rs) {
         // a reserved key lives in its own location word; there are no key bytes to publish
-        uint64_t* p = a.tlocs + rs;
+        uint64_t* p = t.loc(rs);
         for (uint32_t spin = 0; spin < kWaitLimit; ++spin) {
             const uint64_t l = load_relaxed(p);
             if (l == kEmpty) {
@@ -281,44 +312,51 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
         }
         if (a.epochs) a.epochs[rs] = a.epoch;
     } else if (active) {
-        const uint64_t slot_mask = a.capacity - 1;
-        uint64_t s = home_bucket(key, (a.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
+        const KeyWords kw = key_words(key);
+        const uint64_t slot_mask = t.capacity - 1;
+        uint64_t s = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
         uint64_t steps = 0, first_free = ~0ull;  // slots passed in the current phase; first removed slot
         uint32_t waits = 0;
         bool scanning = true;                    // phase 1: the key may still sit further along
         while (true) {
-            const uint64_t l = load_relaxed(a.tlocs + s);
-            if (l == kPending) {
-                if (++waits >= kWaitLimit) { report(a.status, PKV_ESTALL); break; }
-                continue;
-            }
-            const bool free_slot = l == kEmpty || l == kTomb;
-            if (free_slot && !(scanning && l == kTomb)) {
-                if (scanning) {                  // an empty slot ends the path: the key is absent
+            const uint64_t c = load_relaxed(t.lo(s));
+            if (c == kLoEmpty || c == kLoRemoved) {
+                bool claim = !scanning;
+                if (scanning && c == kLoEmpty) {     // a never-used slot ends the path: the key is absent
                     scanning = false;
                     steps = 0;
-                    if (first_free != ~0ull) {   // claim the first removed slot on the path instead
+                    if (first_free != ~0ull) {       // claim the first removed slot on the path instead
                         s = first_free;
                         continue;
                     }
+                    claim = true;
                 }
-                if (cas_relaxed(a.tlocs + s, l, kPending)) {
-                    publish_slot(a.tkeys, a.tlocs, s, key, want);
+                if (claim) {
+                    if (cas_relaxed(t.lo(s), c, kw.claim)) {
+                        publish_slot(t, s, kw, want);
+                        if (a.epochs) a.epochs[s] = a.epoch;
+                        claimed = true;
+                        my_slot = s | (c == kLoRemoved ? kFromTomb : 0);
+                        break;
+                    }
+                    continue;                        // lost the race: read the slot again
+                }
+                if (first_free == ~0ull) first_free = s;   // a removed slot met while scanning
+            } else if (c == kw.claim) {
+                uint64_t hi, loc;
+                read_published_pair(t.pair(s), hi, loc);
+                if (loc == kEmpty) {                 // claimed, not yet published: read it again
+                    if (++waits >= kWaitLimit) { report(a.status, PKV_ESTALL); break; }
+                    continue;
+                }
+                if (hi == kw.hi && (kw.claim != kLoSub || load_relaxed(t.flag(s)) == kw.flag)) {
+                    if (loc & kFresh) min_relaxed(t.pair(s) + 1, want);
                     if (a.epochs) a.epochs[s] = a.epoch;
-                    claimed = true;
-                    my_slot = s | (l == kTomb ? kFromTomb : 0);
                     break;
                 }
-                continue;                       // lost the race: read the slot again
             }
-            if (!free_slot && eq4(read_slot_key(a.tkeys, s), key)) {
-                if (l & kFresh) min_relaxed(a.tlocs + s, want);
-                if (a.epochs) a.epochs[s] = a.epoch;
-                break;
-            }
-            if (free_slot && first_free == ~0ull) first_free = s;   // a removed slot met while scanning
             s = (s + 1) & slot_mask;
-            if (++steps >= a.capacity) {         // a whole cycle
+            if (++steps >= t.capacity) {         // a whole cycle
                 if (scanning && first_free != ~0ull) {
                     scanning = false;
                     steps = 0;
@@ -354,16 +392,17 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
 }
 
 // Clears the fresh bit of the slots the store logged (the index is quiescent: plain accesses).
-__global__ __launch_bounds__(256) void k_store_finish_log(uint64_t* tlocs, uint64_t capacity, const uint64_t* slots,
-                                                          const uint64_t* n_slots, uint64_t max_slots) {
+__global__ __launch_bounds__(256) void k_store_finish_log(Tab t, const uint64_t* slots, const uint64_t* n_slots,
+                                                          uint64_t max_slots) {
     uint64_t n = *n_slots;
     if (n > max_slots) n = max_slots;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
         const uint64_t s = slots[i] & ~kFromTomb;
-        if (s > capacity + 1) continue;
-        const uint64_t l = tlocs[s];
-        if (l != kEmpty && l != kPending && l != kTomb && (l & kFresh)) tlocs[s] = l & ~kFresh;
+        if (s > t.capacity + 1) continue;
+        uint64_t* p = t.loc(s);
+        const uint64_t l = *p;
+        if (l != kEmpty && (l & kFresh)) *p = l & ~kFresh;
     }
 }
 
@@ -374,55 +413,85 @@ __global__ __launch_bounds__(kStoreThreads) void k_store_finish_probe(StoreArgs 
     const int64_t total = a.key_off[a.n_req];
     if (total < 0 || static_cast<uint64_t>(total) > a.n_keys) return;
     if (!candidate(a, wave_base, k, total)) return;
+    const Tab& t = a.t;
     const uint4 key = a.keys[k];
-    uint64_t s = dev::reserved_slot(key, a.capacity);
+    uint64_t s = dev::reserved_slot(key, t.capacity);
     if (!s) {
-        const uint64_t slot_mask = a.capacity - 1;
-        s = home_bucket(key, (a.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
+        const KeyWords kw = key_words(key);
+        const uint64_t slot_mask = t.capacity - 1;
+        s = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
         uint64_t probes = 0;
         while (true) {
-            const uint64_t l = a.tlocs[s];
-            if (l == kEmpty || l == kPending) return;   // not stored (an error was reported)
-            if (l != kTomb && eq4(a.tkeys[s], key)) break;
+            const uint64_t c = *t.lo(s);
+            if (c == kLoEmpty) return;                    // not stored (an error was reported)
+            if (c == kw.claim && t.pair(s)[0] == kw.hi && (kw.claim != kLoSub || *t.flag(s) == kw.flag)) break;
             s = (s + 1) & slot_mask;
-            if (++probes >= a.capacity) return;
+            if (++probes >= t.capacity) return;
         }
     }
-    const uint64_t l = a.tlocs[s];
-    if (l != kEmpty && l != kPending && l != kTomb && (l & kFresh)) a.tlocs[s] = l & ~kFresh;
+    uint64_t* p = t.loc(s);
+    const uint64_t l = *p;
+    if (l != kEmpty && (l & kFresh)) *p = l & ~kFresh;
 }
 
 // ---- rollback and export ------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_rollback(uint4* tkeys, uint64_t* tlocs, uint64_t capacity,
-                                                  const uint64_t* slots, const uint64_t* n_slots, uint64_t max_slots) {
+// A slot back to the state a store found it in: never used, or removed.
+__device__ __forceinline__ void free_slot(const Tab& t, uint64_t s, bool removed) {
+    *t.lo(s) = removed ? kLoRemoved : kLoEmpty;
+    *t.flag(s) = 0;
+    uint64_t* p = t.pair(s);
+    p[0] = ~0ull;
+    p[1] = kEmpty;
+}
+
+__global__ __launch_bounds__(256) void k_rollback(Tab t, const uint64_t* slots, const uint64_t* n_slots,
+                                                  uint64_t max_slots) {
     uint64_t n = *n_slots;
     if (n > max_slots) n = max_slots;
-    const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
         const uint64_t s = slots[i] & ~kFromTomb;
-        if (s < capacity) {
-            const bool tomb = (slots[i] & kFromTomb) != 0;   // back to the state the store found
-            tkeys[s] = tomb ? make_uint4(~0u, ~0u, ~0u, kTombW) : marker;
-            tlocs[s] = tomb ? kTomb : kEmpty;
-        } else if (s <= capacity + 1) {
-            tlocs[s] = kEmpty;
+        if (s < t.capacity) {
+            free_slot(t, s, (slots[i] & kFromTomb) != 0);
+        } else if (s <= t.capacity + 1) {
+            *t.loc(s) = kEmpty;
         }
     }
 }
 
 __global__ void k_zero_u64(uint64_t* p) { *p = 0; }
 
-__global__ __launch_bounds__(256) void k_export(const uint4* tkeys, const uint64_t* tlocs, uint64_t capacity,
-                                                uint4* out_keys, uint64_t* out_locs, uint64_t* count) {
+// Occupied entry of slot s (< capacity + 2): its key and location, or false.
+__device__ __forceinline__ bool slot_entry(const Tab& t, uint64_t s, uint4& key, uint64_t& loc) {
+    if (s >= t.capacity) {
+        loc = *t.loc(s);
+        key = make_uint4(~0u, ~0u, ~0u, s == t.capacity ? ~0u : kTombW);
+        return loc != kEmpty;
+    }
+    uint64_t c = *t.lo(s);
+    if (c == kLoEmpty || c == kLoRemoved) return false;
+    const uint64_t* p = t.pair(s);
+    loc = p[1];
+    if (loc == kEmpty) return false;
+    if (c == kLoSub) {
+        const uint64_t f = *t.flag(s);
+        c = f == 1 ? kLoEmpty : (f == 2 ? kLoRemoved : kLoSub);
+    }
+    const uint64_t hi = p[0];
+    key = make_uint4(static_cast<uint32_t>(c), static_cast<uint32_t>(c >> 32), static_cast<uint32_t>(hi),
+                     static_cast<uint32_t>(hi >> 32));
+    return true;
+}
+
+__global__ __launch_bounds__(256) void k_export(Tab t, uint4* out_keys, uint64_t* out_locs, uint64_t* count) {
     const uint32_t lane = lane_id();
     const uint64_t waves = static_cast<uint64_t>(gridDim.x) * (blockDim.x / 64);
     const uint64_t wave = blockIdx.x * static_cast<uint64_t>(blockDim.x / 64) + (threadIdx.x >> 6);
-    const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
-    for (uint64_t base = wave * 64; base <= capacity + 1; base += waves * 64) {
+    for (uint64_t base = wave * 64; base <= t.capacity + 1; base += waves * 64) {
         const uint64_t s = base + lane;
-        const uint64_t l = s <= capacity + 1 ? tlocs[s] : kEmpty;
-        const bool occ = l != kEmpty && !(s < capacity && l == kTomb);
+        uint4 key = make_uint4(0u, 0u, 0u, 0u);
+        uint64_t l = 0;
+        const bool occ = s <= t.capacity + 1 && slot_entry(t, s, key, l);
         const uint64_t mask = __ballot(occ);
         if (!mask) continue;
         const uint32_t leader = __builtin_ctzll(mask);
@@ -432,7 +501,7 @@ __global__ __launch_bounds__(256) void k_export(const uint4* tkeys, const uint64
                                          __HIP_MEMORY_SCOPE_AGENT);
         pos = __shfl(pos, leader, 64) + __popcll(mask & ((1ull << lane) - 1));
         if (occ) {
-            out_keys[pos] = s < capacity ? tkeys[s] : (s == capacity ? marker : make_uint4(~0u, ~0u, ~0u, kTombW));
+            out_keys[pos] = key;
             out_locs[pos] = l;
         }
     }
@@ -440,12 +509,12 @@ __global__ __launch_bounds__(256) void k_export(const uint4* tkeys, const uint64
 
 // ---- eviction to a budget (quiescent index) ---------------------------------------------------
 // Generational: with E* the smallest epoch such that at most `budget` live entries were last used
-// at or after E*, every live entry used before E* is removed (its key slot becomes a removed
-// slot; a reserved key's location word becomes empty).  E* is found by a radix select over the
-// 32-bit epochs in three digits (bits 21-31, 10-20, 0-9): per digit, a histogram pass over the
-// index and a one-workgroup scan.  Histograms are kept per workgroup in LDS and flushed with one
-// global atomic per non-empty bin, so entries that share an epoch do not contend on one address.
-// The work area holds the three histograms and a small control block.
+// at or after E*, every live entry used before E* is removed (its slot becomes a removed slot; a
+// reserved key's location word becomes empty).  E* is found by a radix select over the 32-bit
+// epochs in three digits (bits 21-31, 10-20, 0-9): per digit, a histogram pass over the index and
+// a one-workgroup scan.  Histograms are kept per workgroup in LDS and flushed with one global
+// atomic per non-empty bin, so entries that share an epoch do not contend on one address.  The
+// work area holds the three histograms and a small control block.
 constexpr uint32_t kDigitBins = 2048;
 constexpr uint32_t kSelectThreads = 1024;
 constexpr uint32_t kHistThreads = 1024;
@@ -465,8 +534,10 @@ __device__ __forceinline__ EvictCtl* evict_ctl(uint32_t* work) {
     return reinterpret_cast<EvictCtl*>(work + 3 * kDigitBins);
 }
 
-__device__ __forceinline__ bool live_slot(uint64_t s, uint64_t l, uint64_t capacity) {
-    return l != kEmpty && !(s < capacity && (l == kTomb || l == kPending));
+__device__ __forceinline__ bool live_slot(const Tab& t, uint64_t s) {
+    if (s >= t.capacity) return *t.loc(s) != kEmpty;
+    const uint64_t c = *t.lo(s);
+    return c != kLoEmpty && c != kLoRemoved && t.pair(s)[1] != kEmpty;
 }
 
 __global__ __launch_bounds__(256) void k_evict_clear(uint32_t* work, uint64_t* n_evicted) {
@@ -497,8 +568,7 @@ __device__ __forceinline__ void lds_hist_add(uint32_t* h, bool act, uint32_t bin
 }
 
 // Histogram of digit d over the live entries whose higher digits equal the selected prefix.
-__global__ __launch_bounds__(kHistThreads) void k_evict_hist(const uint64_t* tlocs, uint64_t capacity,
-                                                             const uint32_t* epochs, uint32_t* work, int d) {
+__global__ __launch_bounds__(kHistThreads) void k_evict_hist(Tab t, const uint32_t* epochs, uint32_t* work, int d) {
     __shared__ uint32_t h[kDigitBins];
     const EvictCtl* c = evict_ctl(work);
     if (c->done) return;                       // uniform: the control block is read-only here
@@ -509,11 +579,11 @@ __global__ __launch_bounds__(kHistThreads) void k_evict_hist(const uint64_t* tlo
     __syncthreads();
     const uint64_t waves = static_cast<uint64_t>(gridDim.x) * (blockDim.x / 64);
     const uint64_t wave = blockIdx.x * static_cast<uint64_t>(blockDim.x / 64) + (threadIdx.x >> 6);
-    for (uint64_t base = wave * 64; base < capacity + 2; base += waves * 64) {
+    for (uint64_t base = wave * 64; base < t.capacity + 2; base += waves * 64) {
         const uint64_t s = base + lane_id();
         bool act = false;
         uint32_t bin = 0;
-        if (s < capacity + 2 && live_slot(s, tlocs[s], capacity)) {
+        if (s < t.capacity + 2 && live_slot(t, s)) {
             const uint32_t e = epochs[s];
             const uint32_t high = d == 0 ? 0u : (e >> (shift + (d == 1 ? 11 : 10)));
             act = high == prefix;
@@ -583,19 +653,15 @@ __global__ __launch_bounds__(kSelectThreads) void k_evict_select(uint32_t* work,
     }
 }
 
-__global__ __launch_bounds__(256) void k_evict_apply(uint4* tkeys, uint64_t* tlocs, uint64_t capacity,
-                                                     const uint32_t* epochs, uint32_t* work) {
+__global__ __launch_bounds__(256) void k_evict_apply(Tab t, const uint32_t* epochs, uint32_t* work) {
     const uint64_t cut = evict_ctl(work)->cut;
     if (cut == 0) return;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
-    for (uint64_t s = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; s < capacity + 2; s += stride) {
-        if (!live_slot(s, tlocs[s], capacity) || epochs[s] >= cut) continue;
-        if (s < capacity) {
-            tkeys[s] = make_uint4(~0u, ~0u, ~0u, kTombW);
-            tlocs[s] = kTomb;
-        } else {
-            tlocs[s] = kEmpty;
-        }
+    for (uint64_t s = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; s < t.capacity + 2;
+         s += stride) {
+        if (!live_slot(t, s) || epochs[s] >= cut) continue;
+        if (s < t.capacity) free_slot(t, s, true);
+        else *t.loc(s) = kEmpty;
     }
 }
 
@@ -645,41 +711,41 @@ int launch_sum_hits(const int32_t* hits, uint32_t n_req, const int64_t* group_of
     return check_launch("pkv_sum_hits");
 }
 
-int launch_evict(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint32_t* epochs, uint64_t budget,
-                 uint32_t* work, uint64_t* n_evicted, hipStream_t s) {
+int launch_evict(uint64_t* table, uint64_t capacity, const uint32_t* epochs, uint64_t budget, uint32_t* work,
+                 uint64_t* n_evicted, hipStream_t s) {
+    const Tab t{table, capacity};
     const unsigned g = grid_for(capacity + 2, kHistThreads, kHistBlocks);
     hipLaunchKernelGGL(k_evict_clear, dim3(8), dim3(256), 0, s, work, n_evicted);
     for (int d = 0; d < 3; ++d) {
-        hipLaunchKernelGGL(k_evict_hist, dim3(g), dim3(kHistThreads), 0, s, tlocs, capacity, epochs, work, d);
+        hipLaunchKernelGGL(k_evict_hist, dim3(g), dim3(kHistThreads), 0, s, t, epochs, work, d);
         hipLaunchKernelGGL(k_evict_select, dim3(1), dim3(kSelectThreads), 0, s, work, budget, d, n_evicted);
     }
-    hipLaunchKernelGGL(k_evict_apply, dim3(grid_for(capacity + 2, 256, 16384)), dim3(256), 0, s,
-                       reinterpret_cast<uint4*>(tkeys), tlocs, capacity, epochs, work);
+    hipLaunchKernelGGL(k_evict_apply, dim3(grid_for(capacity + 2, 256, 16384)), dim3(256), 0, s, t, epochs, work);
     return check_launch("pkv_table_evict");
 }
 
-int launch_table_init(uint8_t* keys, uint64_t* locs, uint64_t capacity, hipStream_t s) {
-    hipLaunchKernelGGL(k_init, dim3(grid_for(capacity + 2, 256, 16384)), dim3(256), 0, s,
-                       reinterpret_cast<uint4*>(keys), locs, capacity);
+int launch_table_init(uint64_t* table, uint64_t capacity, hipStream_t s) {
+    hipLaunchKernelGGL(k_init, dim3(grid_for(capacity * 2 + 4, 256, 16384)), dim3(256), 0, s,
+                       reinterpret_cast<uint4*>(table), capacity);
     return check_launch("pkv_table_init");
 }
 
-int launch_lookup(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity, const uint8_t* keys,
-                  const int64_t* key_off, uint32_t n_req, uint64_t n_keys, int32_t* hits, uint32_t* epochs,
-                  uint32_t epoch, int32_t* status, hipStream_t s) {
+int launch_lookup(const uint64_t* table, uint64_t capacity, const uint8_t* keys, const int64_t* key_off,
+                  uint32_t n_req, uint64_t n_keys, int32_t* hits, uint32_t* epochs, uint32_t epoch, int32_t* status,
+                  hipStream_t s) {
     if (n_req == 0) return PKV_OK;
     hipLaunchKernelGGL(k_lookup, dim3((n_req + kLookupWaves - 1) / kLookupWaves), dim3(64 * kLookupWaves), 0, s,
-                       reinterpret_cast<const uint4*>(tkeys), tlocs, capacity, reinterpret_cast<const uint4*>(keys),
+                       reinterpret_cast<const uint4*>(table), capacity, reinterpret_cast<const uint4*>(keys),
                        key_off, n_req, n_keys, hits, epochs, epoch, status);
     return check_launch("pkv_lookup_prefix");
 }
 
-int launch_store(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint8_t* keys, const int64_t* key_off,
-                 uint32_t n_req, uint64_t n_keys, const int32_t* hits, const uint64_t* locs, uint64_t* new_slots,
-                 uint64_t* n_new, uint32_t* epochs, uint32_t epoch, int32_t* status, hipStream_t s) {
+int launch_store(uint64_t* table, uint64_t capacity, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
+                 uint64_t n_keys, const int32_t* hits, const uint64_t* locs, uint64_t* new_slots, uint64_t* n_new,
+                 uint32_t* epochs, uint32_t epoch, int32_t* status, hipStream_t s) {
     if (n_req == 0 || n_keys == 0) return PKV_OK;
-    StoreArgs a{reinterpret_cast<uint4*>(tkeys), tlocs, capacity, reinterpret_cast<const uint4*>(keys),
-                key_off, n_req, n_keys, hits, locs, new_slots, n_new, epochs, epoch, status};
+    StoreArgs a{Tab{table, capacity}, reinterpret_cast<const uint4*>(keys), key_off, n_req, n_keys, hits, locs,
+                new_slots, n_new, epochs, epoch, status};
     const uint64_t blocks = (n_keys + kStoreThreads - 1) / kStoreThreads;
     if (blocks > 0x7fffffffull) return set_error(PKV_EINVAL, "pkv_store: too many keys (%llu)",
                                                  static_cast<unsigned long long>(n_keys));
@@ -687,30 +753,30 @@ int launch_store(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint8
     int rc = check_launch("pkv_store");
     if (rc) return rc;
     if (new_slots) {
-        hipLaunchKernelGGL(k_store_finish_log, dim3(grid_for(n_keys, 256, 4096)), dim3(256), 0, s, tlocs, capacity,
-                           new_slots, n_new, n_keys);
+        hipLaunchKernelGGL(k_store_finish_log, dim3(grid_for(n_keys, 256, 4096)), dim3(256), 0, s, a.t, new_slots,
+                           n_new, n_keys);
     } else {
         hipLaunchKernelGGL(k_store_finish_probe, dim3(static_cast<unsigned>(blocks)), dim3(kStoreThreads), 0, s, a);
     }
     return check_launch("pkv_store (finish)");
 }
 
-int launch_rollback(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint64_t* slots, const uint64_t* n_slots,
+int launch_rollback(uint64_t* table, uint64_t capacity, const uint64_t* slots, const uint64_t* n_slots,
                     uint64_t max_slots, hipStream_t s) {
     if (max_slots == 0) return PKV_OK;
-    hipLaunchKernelGGL(k_rollback, dim3(grid_for(max_slots, 256, 8192)), dim3(256), 0, s,
-                       reinterpret_cast<uint4*>(tkeys), tlocs, capacity, slots, n_slots, max_slots);
+    hipLaunchKernelGGL(k_rollback, dim3(grid_for(max_slots, 256, 8192)), dim3(256), 0, s, Tab{table, capacity}, slots,
+                       n_slots, max_slots);
     return check_launch("pkv_table_rollback");
 }
 
-int launch_export(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity, uint8_t* out_keys,
-                  uint64_t* out_locs, uint64_t* count, hipStream_t s) {
+int launch_export(const uint64_t* table, uint64_t capacity, uint8_t* out_keys, uint64_t* out_locs, uint64_t* count,
+                  hipStream_t s) {
     hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(1), 0, s, count);
     int rc = check_launch("pkv_table_export (zero)");
     if (rc) return rc;
-    hipLaunchKernelGGL(k_export, dim3(grid_for(capacity + 2, 256, 8192)), dim3(256), 0, s,
-                       reinterpret_cast<const uint4*>(tkeys), tlocs, capacity, reinterpret_cast<uint4*>(out_keys),
-                       out_locs, count);
+    const Tab t{const_cast<uint64_t*>(table), capacity};
+    hipLaunchKernelGGL(k_export, dim3(grid_for(capacity + 2, 256, 8192)), dim3(256), 0, s, t,
+                       reinterpret_cast<uint4*>(out_keys), out_locs, count);
     return check_launch("pkv_table_export");
 }
 

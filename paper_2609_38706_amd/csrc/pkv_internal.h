@@ -22,23 +22,46 @@ static constexpr uint32_t kRoundK[64] = {
 static constexpr uint32_t kInitH[8] = {0x6a09e667u, 0xbb67ae85u, 0x3c6ef372u, 0xa54ff53au,
                                       0x510e527fu, 0x9b05688cu, 0x1f83d9abu, 0x5be0cd19u};
 
-// Index slot encoding.  A slot's location word is the state of the slot:
-//   kEmpty    -- never used (its key bytes are all 0xFF); ends every probe path through it;
-//   kTomb     -- removed by eviction (its key bytes are the removed-entry pattern): free for a
-//                new key, but probe paths continue through it;
-//   kPending  -- claimed by an inserting lane that has not yet published the key;
-//   other     -- occupied; bit 63 (kFresh) marks an entry inserted by the running store batch,
-//                whose location may still be lowered to the batch minimum.
-// Valid caller locations are < 2^62, so no occupied value collides with the markers.  Two key
-// byte patterns are reserved (all 0xFF: empty; all 0xFF with a last byte 0xFE: removed); keys
-// equal to them live in the location words at [capacity] and [capacity + 1].
+// Index layout.  The table is one array of 128-byte buckets of 4 slots, followed by a 64-byte tail:
+//   bucket word  0..3  claim word of slot j: the key's first 8 bytes (little-endian), or a marker;
+//   bucket word  4..7  flag word of slot j: which key prefix a substitute claim word stands for;
+//   bucket word  8..15 {key bytes 8..15, location word} of slot j, one 16-byte pair per slot;
+//   tail word    0, 1  location words of the two reserved keys (below).
+// Claim word:
+//   kLoEmpty    -- never used; ends every probe path through it;
+//   kLoRemoved  -- removed by eviction: free for a new key, probe paths continue through it;
+//   other       -- claimed by the key whose first 8 bytes it holds.  A key whose first 8 bytes
+//                  equal one of the two markers claims with kLoSub instead, and its slot's flag
+//                  word says which (1: kLoEmpty, 2: kLoRemoved; 0 for every other key).
+// Location word: kEmpty until the claiming lane publishes the entry, then the location; bit 63
+// (kFresh) marks an entry inserted by the running store batch, whose location may still be
+// lowered to the batch minimum.  Valid caller locations are < 2^62.
+// Two key byte patterns (all 0xFF; all 0xFF with a last byte 0xFE) keep their location in the
+// tail words [capacity] and [capacity + 1] and do not count against the capacity.
+static constexpr uint64_t kLoEmpty = ~0ull;
+static constexpr uint64_t kLoRemoved = ~0ull - 1;
+static constexpr uint64_t kLoSub = ~0ull - 2;
 static constexpr uint64_t kEmpty = ~0ull;
-static constexpr uint64_t kPending = ~0ull - 1;
-static constexpr uint64_t kTomb = ~0ull - 2;
 static constexpr uint64_t kFresh = 1ull << 63;
 static constexpr uint64_t kFromTomb = 1ull << 63;   // slot-log flag: the claimed slot was a removed entry
-static constexpr uint32_t kTombW = 0xFEFFFFFFu;     // last 32-bit word of the removed-entry pattern
-static constexpr uint32_t kSlotsPerBucket = 4;   // 4 x 16-byte keys = one 64-byte segment
+static constexpr uint32_t kTombW = 0xFEFFFFFFu;     // last 32-bit word of the second reserved pattern
+static constexpr uint32_t kSlotsPerBucket = 4;
+static constexpr uint64_t kBucketWords = 16;        // 128 bytes
+
+// Word addresses of slot s (< capacity) and of the tail words.
+struct Tab {
+    uint64_t* w;
+    uint64_t capacity;
+    __device__ __forceinline__ uint64_t* lo(uint64_t s) const { return w + (s >> 2) * kBucketWords + (s & 3); }
+    __device__ __forceinline__ uint64_t* flag(uint64_t s) const { return w + (s >> 2) * kBucketWords + 4 + (s & 3); }
+    __device__ __forceinline__ uint64_t* pair(uint64_t s) const {
+        return w + (s >> 2) * kBucketWords + 8 + 2 * (s & 3);
+    }
+    // location word of a slot index, the two reserved keys included (capacity, capacity + 1)
+    __device__ __forceinline__ uint64_t* loc(uint64_t s) const {
+        return s < capacity ? pair(s) + 1 : w + capacity * (kBucketWords / kSlotsPerBucket) + (s - capacity);
+    }
+};
 
 namespace dev {
 
@@ -96,10 +119,8 @@ __device__ __forceinline__ void report(int32_t* status, int32_t code) {
 __device__ __forceinline__ bool eq4(const uint4& a, const uint4& b) {
     return ((a.x ^ b.x) | (a.y ^ b.y) | (a.z ^ b.z) | (a.w ^ b.w)) == 0;
 }
-__device__ __forceinline__ bool is_marker(const uint4& a) { return (a.x & a.y & a.z & a.w) == 0xFFFFFFFFu; }
-__device__ __forceinline__ bool is_tomb_key(const uint4& a) { return (a.x & a.y & a.z) == 0xFFFFFFFFu && a.w == kTombW; }
-// Location word of a reserved key (capacity for the empty pattern, capacity + 1 for the removed
-// pattern), or 0 for an ordinary key.
+// Slot index of a reserved key (capacity for the all-0xFF pattern, capacity + 1 for the other),
+// or 0 for an ordinary key.
 __device__ __forceinline__ uint64_t reserved_slot(const uint4& a, uint64_t capacity) {
     if ((a.x & a.y & a.z) != 0xFFFFFFFFu) return 0;
     return a.w == 0xFFFFFFFFu ? capacity : (a.w == kTombW ? capacity + 1 : 0);
@@ -119,18 +140,17 @@ int launch_key_offsets(const int64_t* tok_off, uint32_t n_req, uint32_t block, i
 int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_off, uint32_t n_req,
                   const uint8_t* digests, uint32_t block, const int64_t* key_off, uint64_t n_keys,
                   uint8_t* keys, int32_t* status, hipStream_t s);
-int launch_table_init(uint8_t* keys, uint64_t* locs, uint64_t capacity, hipStream_t s);
-int launch_lookup(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity, const uint8_t* keys,
-                  const int64_t* key_off, uint32_t n_req, uint64_t n_keys, int32_t* hits, uint32_t* epochs,
-                  uint32_t epoch, int32_t* status, hipStream_t s);
-int launch_store(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint8_t* keys, const int64_t* key_off,
-                 uint32_t n_req, uint64_t n_keys, const int32_t* hits, const uint64_t* locs,
-                 uint64_t* new_slots, uint64_t* n_new, uint32_t* epochs, uint32_t epoch, int32_t* status,
-                 hipStream_t s);
-int launch_evict(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint32_t* epochs, uint64_t budget,
-                 uint32_t* work, uint64_t* n_evicted, hipStream_t s);
-int launch_rollback(uint8_t* tkeys, uint64_t* tlocs, uint64_t capacity, const uint64_t* slots,
-                    const uint64_t* n_slots, uint64_t max_slots, hipStream_t s);
+int launch_table_init(uint64_t* table, uint64_t capacity, hipStream_t s);
+int launch_lookup(const uint64_t* table, uint64_t capacity, const uint8_t* keys, const int64_t* key_off,
+                  uint32_t n_req, uint64_t n_keys, int32_t* hits, uint32_t* epochs, uint32_t epoch, int32_t* status,
+                  hipStream_t s);
+int launch_store(uint64_t* table, uint64_t capacity, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
+                 uint64_t n_keys, const int32_t* hits, const uint64_t* locs, uint64_t* new_slots, uint64_t* n_new,
+                 uint32_t* epochs, uint32_t epoch, int32_t* status, hipStream_t s);
+int launch_evict(uint64_t* table, uint64_t capacity, const uint32_t* epochs, uint64_t budget, uint32_t* work,
+                 uint64_t* n_evicted, hipStream_t s);
+int launch_rollback(uint64_t* table, uint64_t capacity, const uint64_t* slots, const uint64_t* n_slots,
+                    uint64_t max_slots, hipStream_t s);
 int launch_sum_hits(const int32_t* hits, uint32_t n_req, const int64_t* group_off, uint32_t n_groups, uint64_t* sums,
                     int32_t* status, hipStream_t s);
 // Content-identity trees (k_tree.hip).
@@ -143,8 +163,8 @@ struct TreeLayout {
 TreeLayout tree_layout(uint64_t n_bytes, uint32_t n_tensors);
 int launch_tensor_roots(const uint8_t* data, uint64_t n_bytes, const int64_t* tensor_off, const int64_t* tensor_len,
                         uint32_t n, uint8_t* work, uint8_t* roots, int32_t* status, hipStream_t s);
-int launch_export(const uint8_t* tkeys, const uint64_t* tlocs, uint64_t capacity, uint8_t* out_keys,
-                  uint64_t* out_locs, uint64_t* count, hipStream_t s);
+int launch_export(const uint64_t* table, uint64_t capacity, uint8_t* out_keys, uint64_t* out_locs,
+                  uint64_t* count, hipStream_t s);
 
 // Host-side error text (api.cpp).
 int set_error(int code, const char* fmt, ...);

@@ -26,7 +26,7 @@ def import_pairs(table: Table, keys, locs, stream=None):
     """Inserts (key, location) pairs (device tensors uint8 [n, 16], int64 [n]) into `table`;
     returns the status word (device) and the new-entry counter (device)."""
     import torch
-    dev = table.keys.device
+    dev = table.slots.device
     n = int(keys.shape[0])
     key_off = torch.tensor([0, n], dtype=torch.int64, device=dev)
     hits = torch.zeros(1, dtype=torch.int32, device=dev)

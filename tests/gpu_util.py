@@ -58,17 +58,49 @@ def gpu_fill(table, batch):
     return db
 
 
-def raw_table(table):
-    keys = table.keys.cpu().numpy()
-    locs = table.locs.cpu().numpy().view(np.uint64)
-    return keys, locs
-
-
 EMPTY = np.uint64(0xFFFFFFFFFFFFFFFF)
 PENDING = np.uint64(0xFFFFFFFFFFFFFFFE)
 TOMB = np.uint64(0xFFFFFFFFFFFFFFFD)
 FRESH = np.uint64(1 << 63)
 TOMB_KEY = np.array([0xFF] * 15 + [0xFE], np.uint8)
+
+
+LO_EMPTY = np.uint64(0xFFFFFFFFFFFFFFFF)
+LO_REMOVED = np.uint64(0xFFFFFFFFFFFFFFFE)
+LO_SUB = np.uint64(0xFFFFFFFFFFFFFFFD)
+
+
+def raw_table(table):
+    """The index decoded slot by slot (include/pkv.h layout) into (keys uint8 [capacity, 16], locs
+    uint64 [capacity + 2]): a never-used slot reads as the all-0xFF key with location EMPTY, a
+    removed slot as the removed pattern with location TOMB, a claimed but unpublished slot with
+    location PENDING; locs[capacity], locs[capacity + 1] are the reserved keys' words.  Also checks
+    the layout's own invariants (free slots hold no key bytes, flags or location; flag words appear
+    only with the substitute claim word)."""
+    cap = table.capacity
+    w = table.slots.cpu().numpy().view(np.uint64)
+    b = w[: cap * 4].reshape(cap // 4, 16)
+    claim = b[:, 0:4].reshape(-1)
+    flag = b[:, 4:8].reshape(-1)
+    hi = b[:, 8:16:2].reshape(-1)
+    loc = b[:, 9:16:2].reshape(-1)
+    free = (claim == LO_EMPTY) | (claim == LO_REMOVED)
+    assert (flag[free] == 0).all() and (hi[free] == EMPTY).all() and (loc[free] == EMPTY).all(), \
+        "free slot with contents"
+    assert ((flag == 0) | (claim == LO_SUB)).all(), "flag word without the substitute claim word"
+    assert (flag <= 2).all(), "unknown flag word"
+    lo = np.where(flag == 1, LO_EMPTY, np.where(flag == 2, LO_REMOVED, claim))
+    keys = np.concatenate([lo.view(np.uint8).reshape(-1, 8), hi.view(np.uint8).reshape(-1, 8)], axis=1)
+    locs = np.empty(cap + 2, np.uint64)
+    locs[:cap] = np.where(loc == EMPTY, PENDING, loc)
+    keys[claim == LO_EMPTY] = 0xFF
+    locs[:cap][claim == LO_EMPTY] = EMPTY
+    keys[claim == LO_REMOVED] = TOMB_KEY
+    locs[:cap][claim == LO_REMOVED] = TOMB
+    locs[cap:] = w[cap * 4: cap * 4 + 2]
+    return keys, locs
+
+
 
 
 def check_structure(table):

@@ -33,7 +33,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 19
+    assert len(names) == 20
     lib = pkv.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -92,8 +92,8 @@ def test_encode_buffer_too_small():
     assert n.value == 8 + 4 + 8 + 4 + 1
 
 
-def _table(cap, keys=0x1000, locs=0x2000):
-    return pkv.pkv_table(keys, locs, cap)
+def _table(cap, slots=0x1000):
+    return pkv.pkv_table(slots, cap)
 
 
 @pytest.mark.parametrize("cap", [0, 2, 3, 6, 1000])
@@ -103,9 +103,15 @@ def test_bad_capacity_rejected_on_host(cap):
 
 
 def test_misaligned_table_rejected_on_host():
-    t = _table(1024, keys=0x1010)
+    t = _table(1024, slots=0x1040)
     assert pkv.lib().pkv_table_init(ctypes.byref(t), None) == pkv.PKV_EINVAL
-    assert b"64-byte" in pkv.lib().pkv_last_error()
+    assert b"128-byte" in pkv.lib().pkv_last_error()
+
+
+@pytest.mark.parametrize("cap,nbytes", [(4, 4 * 32 + 64), (1 << 20, (1 << 20) * 32 + 64), (0, 0), (6, 0),
+                                        (1 << 57, 0)])
+def test_table_bytes(cap, nbytes):
+    assert pkv.lib().pkv_table_bytes(cap) == nbytes
 
 
 def test_zero_block_rejected_on_host():
