@@ -121,6 +121,12 @@ def test_reserved_patterns_and_wide_epochs(pkv):
     keys[3] = 0xFF
     keys[7] = 0xFF
     keys[7, 15] = 0xFE
+    # first 8 bytes equal to the never-used and removed claim markers and to the substitute word
+    keys[1, :8] = 0xFF
+    keys[5, :8] = 0xFF
+    keys[5, 0] = 0xFE
+    keys[8, :8] = 0xFF
+    keys[8, 0] = 0xFD
     status = torch.zeros(1, dtype=torch.int32, device="cuda")
     n_new = torch.zeros(1, dtype=torch.int64, device="cuda")
     n_ev = torch.zeros(1, dtype=torch.int64, device="cuda")

@@ -184,6 +184,73 @@ def test_lookup_and_store_random_keys(pkv, seed, capacity):
         assert check_structure(table) == len(idx)
 
 
+def _marker_prefixed_pool(rng):
+    """Keys whose first 8 bytes (the slot claim word, little-endian) equal the never-used marker
+    (all 0xFF), the removed marker (0xFE then 0xFF) or the substitute claim word (0xFD then 0xFF),
+    with random and all-ones second halves; the two reserved patterns; ordinary keys.  The first
+    three prefixes all map to the last buckets, so they also contend and wrap around."""
+    pool = []
+    for first in (0xFF, 0xFE, 0xFD):
+        for hi in range(6):
+            k = np.full(16, 0xFF, np.uint8)
+            k[0] = first
+            if hi < 4:
+                k[8:] = rng.integers(0, 256, size=8, dtype=np.uint8)
+            elif hi == 5:
+                k[8] = 0xFE                                 # one byte off all ones
+            pool.append(k)
+    pool.append(np.full(16, 0xFF, np.uint8))                # reserved: all 0xFF
+    tomb = np.full(16, 0xFF, np.uint8)
+    tomb[15] = 0xFE
+    pool.append(tomb)                                       # reserved: the removed pattern
+    pool.extend(rng.integers(0, 256, size=(10, 16), dtype=np.uint8))
+    return np.stack(pool)
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("capacity", [32, 256])
+def test_marker_prefixed_keys(pkv, seed, capacity):
+    """Claim-word edge cases: keys that claim with the substitute word keep their own identity
+    (flag words), equal keys still merge, lookups find exactly the stored ones, and a rollback
+    restores the index."""
+    import torch
+    from paper_2609_38706_amd.pipeline import export_sorted
+    rng = np.random.default_rng(100 + seed)
+    pool = _marker_prefixed_pool(rng)
+    idx = oracle.Index(capacity)
+    table = pkv.Table(capacity)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for rnd in range(3):
+        n_req = int(rng.integers(1, 60))
+        keys, ko = _key_batch(rng, pool, n_req, 8)
+        locs = rng.permutation(1 << 16)[: keys.shape[0]].astype(np.uint64) + np.uint64(rnd << 40)
+        hits_o = idx.lookup(keys, ko)
+        dk, dko = _dev(keys, torch.uint8).reshape(-1, 16), _dev(ko, torch.int64)
+        hits = torch.zeros(max(1, n_req), dtype=torch.int32, device="cuda")
+        pkv.pkv_lookup_prefix(table, dk, dko, hits[:n_req], status)
+        assert (hits[:n_req].cpu().numpy() == hits_o).all(), (rnd, hits[:n_req].cpu().numpy(), hits_o)
+        before = export_sorted(table)
+        n_new = torch.zeros(1, dtype=torch.int64, device="cuda")
+        slots = torch.empty(max(1, keys.shape[0]), dtype=torch.int64, device="cuda")
+        rc = idx.store(keys, ko, hits_o, locs)
+        pkv.pkv_store(table, dk, dko, hits[:n_req], _dev(locs, torch.int64), n_new, status, slots)
+        torch.cuda.synchronize()
+        assert rc == 0 and int(status.item()) == 0
+        gk, gl = export_sorted(table)
+        ok, ol = idx.dump()
+        assert gk.shape == ok.shape and (gk == ok).all() and (gl == ol).all()
+        assert check_structure(table) == len(idx)
+        if rnd == 1:                                        # undo this round on both sides
+            pkv.pkv_table_rollback(table, slots, n_new)
+            after = export_sorted(table)
+            assert (after[0] == before[0]).all() and (after[1] == before[1]).all()
+            check_structure(table)
+            idx = oracle.Index(capacity)
+            if before[0].shape[0]:
+                assert idx.store(before[0], np.array([0, before[0].shape[0]], np.int64), np.zeros(1, np.int32),
+                                 before[1]) == 0
+
+
 def test_duplicate_heavy_store_is_deterministic(pkv):
     """Every request carries the same key chain: maximal contention on one set of slots.  The index
     must equal the oracle's whatever the request order and however the lanes race."""
