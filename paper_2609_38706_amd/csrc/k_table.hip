@@ -435,13 +435,13 @@ __global__ __launch_bounds__(kStoreThreads) void k_store_finish_probe(StoreArgs 
 }
 
 // ---- rollback and export ------------------------------------------------------------------------
-// A slot back to the state a store found it in: never used, or removed.
+// A slot back to the state a store found it in: never used, or removed.  Only a substitute claim
+// word comes with a non-zero flag word.
 __device__ __forceinline__ void free_slot(const Tab& t, uint64_t s, bool removed) {
-    *t.lo(s) = removed ? kLoRemoved : kLoEmpty;
-    *t.flag(s) = 0;
-    uint64_t* p = t.pair(s);
-    p[0] = ~0ull;
-    p[1] = kEmpty;
+    uint64_t* c = t.lo(s);
+    if (*c == kLoSub) *t.flag(s) = 0;
+    *c = removed ? kLoRemoved : kLoEmpty;
+    *reinterpret_cast<uint4*>(t.pair(s)) = make_uint4(~0u, ~0u, ~0u, ~0u);   // key bytes 8..15, kEmpty
 }
 
 __global__ __launch_bounds__(256) void k_rollback(Tab t, const uint64_t* slots, const uint64_t* n_slots,
