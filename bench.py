@@ -91,6 +91,17 @@ def chain_ceiling_frac(n_chains: int) -> float:
     return min(1.0, n_chains * per_chain / (CUS * LANES_PER_CU))
 
 
+# The tighter bound of the kernels' own round: one wavefront issues a VALU instruction at most every
+# 4 cycles, and the lane-pair round of a chain is 11 instructions long, so a chain finishes at most
+# one round per 44 cycles (and needs two lanes, so 32 chains fill a wavefront).
+PAIR_ROUND_INSTRUCTIONS = 11
+
+
+def issue_ceiling_frac(n_chains: int) -> float:
+    per_chain = OPS_PER_COMPRESSION / (64 * PAIR_ROUND_INSTRUCTIONS * CYCLES_PER_OP)
+    return min(1.0, n_chains * per_chain / (CUS * LANES_PER_CU))
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -608,7 +619,8 @@ def main():
     roofline = {"bound": "alu", "achieved": round(achieved / 1e12, 4), "peak": round(INT_PEAK / 1e12, 4),
                 "unit": "Tops/s", "frac": round(achieved / INT_PEAK, 5), "traffic": measured_traffic(args.workload),
                 "kernel": "derive", "ops_per_key": compressions_per_key(block) * OPS_PER_COMPRESSION,
-                "chain_ceiling_frac": round(chain_ceiling_frac(n_chains), 5)}
+                "chain_ceiling_frac": round(chain_ceiling_frac(n_chains), 5),
+                "issue_ceiling_frac": round(issue_ceiling_frac(n_chains), 5)}
     ser = g["serial"]
     lookup_bps = g["probes"] * BYTES_PER_PROBE / (ser["lookup_ms"] * 1e-3)
     roofline_lookup = {"bound": "hbm", "achieved": round(lookup_bps / 1e9, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
