@@ -336,7 +336,7 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
                         publish_slot(t, s, kw, want);
                         if (a.epochs) a.epochs[s] = a.epoch;
                         claimed = true;
-                        my_slot = s | (c == kLoRemoved ? kFromTomb : 0);
+                        my_slot = s | (c == kLoRemoved ? kFromRemoved : 0);
                         break;
                     }
                     continue;                        // lost the race: read the slot again
@@ -398,7 +398,7 @@ __global__ __launch_bounds__(256) void k_store_finish_log(Tab t, const uint64_t*
     if (n > max_slots) n = max_slots;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
-        const uint64_t s = slots[i] & ~kFromTomb;
+        const uint64_t s = slots[i] & ~kFromRemoved;
         if (s > t.capacity + 1) continue;
         uint64_t* p = t.loc(s);
         const uint64_t l = *p;
@@ -450,9 +450,9 @@ __global__ __launch_bounds__(256) void k_rollback(Tab t, const uint64_t* slots, 
     if (n > max_slots) n = max_slots;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
-        const uint64_t s = slots[i] & ~kFromTomb;
+        const uint64_t s = slots[i] & ~kFromRemoved;
         if (s < t.capacity) {
-            free_slot(t, s, (slots[i] & kFromTomb) != 0);
+            free_slot(t, s, (slots[i] & kFromRemoved) != 0);
         } else if (s <= t.capacity + 1) {
             *t.loc(s) = kEmpty;
         }
@@ -465,7 +465,7 @@ __global__ void k_zero_u64(uint64_t* p) { *p = 0; }
 __device__ __forceinline__ bool slot_entry(const Tab& t, uint64_t s, uint4& key, uint64_t& loc) {
     if (s >= t.capacity) {
         loc = *t.loc(s);
-        key = make_uint4(~0u, ~0u, ~0u, s == t.capacity ? ~0u : kTombW);
+        key = make_uint4(~0u, ~0u, ~0u, s == t.capacity ? ~0u : kResvW);
         return loc != kEmpty;
     }
     uint64_t c = *t.lo(s);

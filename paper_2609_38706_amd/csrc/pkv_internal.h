@@ -43,8 +43,8 @@ static constexpr uint64_t kLoRemoved = ~0ull - 1;
 static constexpr uint64_t kLoSub = ~0ull - 2;
 static constexpr uint64_t kEmpty = ~0ull;
 static constexpr uint64_t kFresh = 1ull << 63;
-static constexpr uint64_t kFromTomb = 1ull << 63;   // slot-log flag: the claimed slot was a removed entry
-static constexpr uint32_t kTombW = 0xFEFFFFFFu;     // last 32-bit word of the second reserved pattern
+static constexpr uint64_t kFromRemoved = 1ull << 63;   // slot-log flag: the claimed slot was a removed entry
+static constexpr uint32_t kResvW = 0xFEFFFFFFu;     // last 32-bit word of the second reserved pattern
 static constexpr uint32_t kSlotsPerBucket = 4;
 static constexpr uint64_t kBucketWords = 16;        // 128 bytes
 
@@ -123,7 +123,7 @@ __device__ __forceinline__ bool eq4(const uint4& a, const uint4& b) {
 // or 0 for an ordinary key.
 __device__ __forceinline__ uint64_t reserved_slot(const uint4& a, uint64_t capacity) {
     if ((a.x & a.y & a.z) != 0xFFFFFFFFu) return 0;
-    return a.w == 0xFFFFFFFFu ? capacity : (a.w == kTombW ? capacity + 1 : 0);
+    return a.w == 0xFFFFFFFFu ? capacity : (a.w == kResvW ? capacity + 1 : 0);
 }
 
 // Home bucket: the key is a SHA-256 output, so its first eight bytes are already uniform.
