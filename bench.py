@@ -113,6 +113,8 @@ def parse():
     p.add_argument("--no-saturation", action="store_true", help="skip the derive-at-full-occupancy diagnostic")
     p.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (0 = host cores, at most 16)")
     p.add_argument("--calib-copy", action="store_true", help="run only a plain 1 GiB device copy (counter calibration)")
+    p.add_argument("--cold-reps", type=int, default=20,
+                   help="reps of the cold-cache per-kernel measurement after the timed region (0 = skip)")
     p.add_argument("--quiet", action="store_true")
     return p.parse_args()
 
@@ -210,6 +212,40 @@ def serial_leg(args, table, run):
             "store_ms": float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))}
 
 
+def cold_leg(args, table, run, reps):
+    """Per-kernel times with cold caches, outside the timed region: before every rep (untimed) the
+    index is restored from a pristine device copy and a 1 GiB scratch buffer is written, which
+    evicts L2 and the 256 MB Infinity Cache; then key offsets, digests, derive, lookup and store run
+    once on one stream, the last three bracketed by events.  Medians over the reps."""
+    import torch
+    if reps <= 0:
+        return None
+    pristine = table.slots.clone()
+    scratch = torch.empty(1 << 28, dtype=torch.int32, device="cuda")        # 1 GiB
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+    for i in range(reps):
+        table.slots.copy_(pristine)
+        scratch.fill_(i)
+        run.n_new.zero_()
+        run.key_offsets()
+        run.digest()
+        evs[i][0].record()
+        run.derive()
+        evs[i][1].record()
+        run.lookup(table)
+        evs[i][2].record()
+        run.store(table)
+        evs[i][3].record()
+    torch.cuda.synchronize()
+    table.slots.copy_(pristine)
+    torch.cuda.synchronize()
+    if run.host_status() != 0:
+        raise RuntimeError(f"cold leg failed: status {run.host_status()}")
+    med = lambda a, b: round(float(np.median([e[a].elapsed_time(e[b]) for e in evs])), 4)
+    return {"reps": reps, "derive": med(0, 1), "lookup": med(1, 2), "store": med(2, 3),
+            "how": "index restored from a pristine copy and a 1 GiB scratch buffer written before each rep"}
+
+
 def gpu_leg(args, w):
     """The timed region: K steps, consecutive steps overlapped on two streams (the derive of step k+1
     runs while step k is looked up, stored and rolled back).  Only the derive is bracketed by events,
@@ -241,9 +277,11 @@ def gpu_leg(args, w):
     hits = run.host_hits()
     nk = np.diff(run.key_off.cpu().numpy())
     probes = int(np.minimum(np.maximum(hits, 0) + 1, nk).sum())         # algorithmic: up to the first miss
+    new_entries = int(run.n_new.item())
+    cold = cold_leg(args, table, run, args.cold_reps)
     return {"probes": probes, "ms": (t1 - t0) * 1e3 / args.steps, "derive_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evs if e is not None])),
             "derive_timed_launches": sum(e is not None for e in evs), "serial": serial, "n_keys": run.n_keys, "n_req": run.n_req, "hit_blocks": int(hits.sum()),
-            "new_entries": int(run.n_new.item()), "fill": fill}
+            "new_entries": new_entries, "fill": fill, "cold": cold}
 
 
 def saturation_leg(args, n_chains=131072, blocks=16, reps=5):
@@ -656,6 +694,7 @@ def main():
                    "keys": g["n_keys"], "block": block, "capacity": w.capacity, "parallelism": "1 GPU"},
         "kernels_ms": {"derive": round(g["derive_ms"], 4), "lookup": round(g["serial"]["lookup_ms"], 4),
                        "store": round(g["serial"]["store_ms"], 4), "derive_serial": round(g["serial"]["derive_ms"], 4)},
+        "kernels_ms_cold": g["cold"],
         "pipeline": {"streams": 2, "overlap": "derive of step k+1 with lookup/store/rollback of step k",
                      "serial_ms_per_step": round(g["serial"]["ms"], 4),
                      "serial_value": round(g["n_keys"] / (g["serial"]["ms"] * 1e-3) / 1e9, 6),
