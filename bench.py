@@ -536,26 +536,55 @@ def cpu_leg(args, w, target_s=10.0, max_reps=2000):
     b = w.batch
     locs = locations(oracle.key_offsets(b.tok_off, b.block), b.tag)
     total_s, total_keys, reps = 0.0, 0, 0
+    phase = {"digests": 0.0, "derive": 0.0, "lookup": 0.0, "store": 0.0}
     while total_s < target_s and reps < max_reps:
         step_idx = idx.clone()                       # untimed: every step meets the same index
         t0 = time.perf_counter()
         digs = oracle.batch_digests(b)
         ko = oracle.key_offsets(b.tok_off, b.block)
-        keys = oracle.derive(b.tokens, b.tok_off, digs, b.block, threads)
-        hits = step_idx.lookup(keys, ko)
-        rc = step_idx.store(keys, ko, hits, locs)
         t1 = time.perf_counter()
+        keys = oracle.derive(b.tokens, b.tok_off, digs, b.block, threads)
+        t2 = time.perf_counter()
+        hits = step_idx.lookup(keys, ko)
+        t3 = time.perf_counter()
+        rc = step_idx.store(keys, ko, hits, locs)
+        t4 = time.perf_counter()
         assert rc == 0
         del step_idx
-        total_s += t1 - t0
+        for name, dt in zip(phase, (t1 - t0, t2 - t1, t3 - t2, t4 - t3)):
+            phase[name] += dt
+        total_s += t4 - t0
         total_keys += int(ko[-1])
         reps += 1
     n_keys = total_keys // reps
+    # the derive on one thread, over the leading requests of the batch (about 2^17 keys)
+    ko = oracle.key_offsets(b.tok_off, b.block)
+    n_sub = max(1, min(b.n_req, int(np.searchsorted(ko, 1 << 17, side="right")) - 1))
+    sub_off = np.ascontiguousarray(b.tok_off[:n_sub + 1])
+    sub_tok = np.ascontiguousarray(b.tokens[:int(sub_off[-1])])
+    sub_digs = np.ascontiguousarray(oracle.batch_digests(b)[:n_sub])
+    t0 = time.perf_counter()
+    oracle.derive(sub_tok, sub_off, sub_digs, b.block, 1)
+    one_s = time.perf_counter() - t0
     return {"value": round(total_keys / total_s / 1e9, 6), "unit": "Gkeys/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} full steps of the same workload ({b.n_req} requests, {n_keys} keys each), each on a "
                       f"fresh copy of the prepared index: digests, derive on {threads} threads, lookup and store "
                       f"single-threaded; {total_s:.2f} s timed",
-            "seconds": round(total_s, 3), "steps": reps}
+            "seconds": round(total_s, 3), "steps": reps, "cpu_model": cpu_model(),
+            "phase_ms_per_step": {k: round(v / reps * 1e3, 3) for k, v in phase.items()},
+            "derive_one_thread": {"requests": n_sub, "keys": int(ko[n_sub]), "seconds": round(one_s, 6),
+                                  "gkeys_per_s": round(int(ko[n_sub]) / one_s / 1e9, 6)}}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main():
