@@ -206,24 +206,11 @@ struct PairLane {
     uint32_t m, nm, r1, r2, r3;       // all-ones on the a lane; its rotate amounts
 };
 
-// Two ways to place a chain's lane pair in the wavefront.
-//   RowHalves: lanes i and i + 8 of a 16-lane row (lanes 0..7 of each row are e lanes).  The
-//     partner is read with DPP row_ror:8, and a DPP bank mask writes one half of a row, which the
-//     10-instruction round below needs.
-//   Adjacent: lanes 2c and 2c + 1 (even lanes are e lanes), partner by DPP quad_perm [1,0,3,2];
-//     a bank mask cannot tell the two lanes of a quad apart, so the round selects what each lane
-//     sends (11 instructions).
-// k_derive_b16_pp uses RowHalves; k_derive_m16_pp keeps Adjacent, which measured faster for it.
-enum class Pairing { RowHalves, Adjacent };
-
-template <Pairing P>
-__device__ __forceinline__ uint32_t pair_chain(uint32_t lane) {
-    return P == Pairing::RowHalves ? (((lane >> 4) << 3) | (lane & 7u)) : (lane >> 1);
-}
-template <Pairing P>
-__device__ __forceinline__ bool pair_is_a(uint32_t lane) {
-    return P == Pairing::RowHalves ? (lane & 8u) != 0 : (lane & 1u) != 0;
-}
+// The lane's chain (0..31) and half of its pair: lanes i and i + 8 of each 16-lane row (lanes
+// 0..7 of each row are e lanes).  The partner is read with DPP row_ror:8, and a DPP bank mask
+// writes one half of a row.
+__device__ __forceinline__ uint32_t pair_chain(uint32_t lane) { return ((lane >> 4) << 3) | (lane & 7u); }
+__device__ __forceinline__ bool pair_is_a(uint32_t lane) { return (lane & 8u) != 0; }
 
 // One paired round with the operand roles (x0, x1, x2, x3): the new x0 is written into x3's
 // register and Q of the next round is formed from x2 (next round's x3) and KWN.  Bit tables of
@@ -238,84 +225,62 @@ __device__ __forceinline__ bool pair_is_a(uint32_t lane) {
     "v_bitop3_b32 %[t1], %[" #X0 "], %[" #X1 "], %[m] bitop3:0xd2\n"                              \
     "v_bitop3_b32 %[t1], %[t1], %[" #X1 "], %[" #X2 "] bitop3:0xca\n"                             \
     "v_add3_u32 %[t0], %[t0], %[t1], %[q]\n"
-// RowHalves: on the e lane x3 is h, which only Q used, and e' = d + T1 overwrites it; on the a
-// lane x3 is d, which the partner has read by then, and a' = T1 + Sigma0 + Maj overwrites it.
-// The e lane's add and the Q add sit between Y and the a lane's DPP read of it (two wait states).
-#define PKV_RH_ROUND(X0, X1, X2, X3, KWN)                                                          \
+// On the e lane x3 is h, which only Q used, and e' = d + T1 overwrites it; on the a lane x3 is
+// d, which the partner has read by then, and a' = T1 + Sigma0 + Maj overwrites it.  The e lane's
+// add and the Q add sit between Y and the a lane's DPP read of it (two wait states).
+#define PKV_PAIR_ROUND(X0, X1, X2, X3, KWN)                                                          \
     PKV_ROUND_HEAD(X0, X1, X2)                                                                    \
     "v_add_u32_dpp %[" #X3 "], %[" #X3 "], %[t0] row_ror:8 row_mask:0xf bank_mask:0x3\n"          \
     "v_add_u32_dpp %[q], %[" #X2 "], %[" #KWN "] quad_perm:[0,1,2,3] row_mask:0xf bank_mask:0x3\n" \
     "v_add_u32_dpp %[" #X3 "], %[t0], %[t0] row_ror:8 row_mask:0xf bank_mask:0xc\n"
 // Without forming the next round's Q (the caller forms it from K + W words that are still
 // arriving); one wait state more covers the a lane's DPP read of Y.
-#define PKV_RH_ROUND_LAST(X0, X1, X2, X3)                                                          \
+#define PKV_PAIR_ROUND_LAST(X0, X1, X2, X3)                                                          \
     PKV_ROUND_HEAD(X0, X1, X2)                                                                    \
     "v_add_u32_dpp %[" #X3 "], %[" #X3 "], %[t0] row_ror:8 row_mask:0xf bank_mask:0x3\n"          \
     "s_nop 0\n"                                                                                   \
     "v_add_u32_dpp %[" #X3 "], %[t0], %[t0] row_ror:8 row_mask:0xf bank_mask:0xc\n"
-// Adjacent: one select of what to send (d from the a lane, T1 from the e lane) and one add of the
-// swapped value; the next round's Q (add, then AND with the e lane's all-ones mask) sits between
-// the select and the DPP read of it.
-#define PKV_ADJ_ROUND(X0, X1, X2, X3, KWN)                                                         \
-    PKV_ROUND_HEAD(X0, X1, X2)                                                                    \
-    "v_bitop3_b32 %[t1], %[m], %[" #X3 "], %[t0] bitop3:0xca\n"                                   \
-    "v_add_u32_e32 %[q], %[" #X2 "], %[" #KWN "]\n"                                               \
-    "v_and_b32_e32 %[q], %[q], %[nm]\n"                                                           \
-    "v_add_u32_dpp %[" #X3 "], %[t1], %[t0] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
-#define PKV_ADJ_ROUND_LAST(X0, X1, X2, X3)                                                         \
-    PKV_ROUND_HEAD(X0, X1, X2)                                                                    \
-    "v_bitop3_b32 %[t1], %[m], %[" #X3 "], %[t0] bitop3:0xca\n"                                   \
-    "s_nop 1\n"                                                                                   \
-    "v_add_u32_dpp %[" #X3 "], %[t1], %[t0] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n"
-
+// gfx950 fetches 8-byte instructions (VOP3, DPP) that are not 8-byte aligned at about one cycle
+// more each: a run of the 10-instruction round placed 4 bytes off takes 50 cycles instead of 40.
+// The compiler puts 4-byte instructions (s_nop, VOP2) between asm statements, so each block of
+// rounds starts by padding itself back to an 8-byte boundary (the assembler pads with s_nop).
+#define PKV_ALIGN8 ".p2align 3\n"
 #define PKV_ROUNDS4_OPERANDS                                                                      \
     : [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [q] "+v"(q), [a] "+v"(x0), [b] "+v"(x1),  \
       [c] "+v"(x2), [d] "+v"(x3)                                                                  \
-    : [m] "v"(pl.m), [nm] "v"(pl.nm), [r1] "v"(pl.r1), [r2] "v"(pl.r2), [r3] "v"(pl.r3), [k1] "v"(k1), \
-      [k2] "v"(k2), [k3] "v"(k3)
+    : [m] "v"(pl.m), [r1] "v"(pl.r1), [r2] "v"(pl.r2), [r3] "v"(pl.r3), [k1] "v"(k1), [k2] "v"(k2),     \
+      [k3] "v"(k3)
 
 // Four paired rounds; k1..k4 are K + W of the four rounds that follow each of them.
-template <Pairing P>
 __device__ __forceinline__ void pair_rounds4(uint32_t& x0, uint32_t& x1, uint32_t& x2, uint32_t& x3, uint32_t& q,
                                              const PairLane& pl, uint32_t k1, uint32_t k2, uint32_t k3,
                                              uint32_t k4) {
     uint32_t t0, t1, t2;
-    if constexpr (P == Pairing::RowHalves)
-        asm volatile(PKV_RH_ROUND(a, b, c, d, k1) PKV_RH_ROUND(d, a, b, c, k2) PKV_RH_ROUND(c, d, a, b, k3)
-                         PKV_RH_ROUND(b, c, d, a, k4) PKV_ROUNDS4_OPERANDS, [k4] "v"(k4));
-    else
-        asm volatile(PKV_ADJ_ROUND(a, b, c, d, k1) PKV_ADJ_ROUND(d, a, b, c, k2) PKV_ADJ_ROUND(c, d, a, b, k3)
-                         PKV_ADJ_ROUND(b, c, d, a, k4) PKV_ROUNDS4_OPERANDS, [k4] "v"(k4));
+    asm volatile(PKV_ALIGN8 PKV_PAIR_ROUND(a, b, c, d, k1) PKV_PAIR_ROUND(d, a, b, c, k2) PKV_PAIR_ROUND(c, d, a, b, k3)
+                     PKV_PAIR_ROUND(b, c, d, a, k4) PKV_ROUNDS4_OPERANDS, [k4] "v"(k4));
 }
 
 // Four paired rounds whose last one leaves Q of the following round to the caller.
-template <Pairing P>
 __device__ __forceinline__ void pair_rounds4_last(uint32_t& x0, uint32_t& x1, uint32_t& x2, uint32_t& x3, uint32_t q,
                                                   const PairLane& pl, uint32_t k1, uint32_t k2, uint32_t k3) {
     uint32_t t0, t1, t2;
-    if constexpr (P == Pairing::RowHalves)
-        asm volatile(PKV_RH_ROUND(a, b, c, d, k1) PKV_RH_ROUND(d, a, b, c, k2) PKV_RH_ROUND(c, d, a, b, k3)
-                         PKV_RH_ROUND_LAST(b, c, d, a) PKV_ROUNDS4_OPERANDS);
-    else
-        asm volatile(PKV_ADJ_ROUND(a, b, c, d, k1) PKV_ADJ_ROUND(d, a, b, c, k2) PKV_ADJ_ROUND(c, d, a, b, k3)
-                         PKV_ADJ_ROUND_LAST(b, c, d, a) PKV_ROUNDS4_OPERANDS);
+    asm volatile(PKV_ALIGN8 PKV_PAIR_ROUND(a, b, c, d, k1) PKV_PAIR_ROUND(d, a, b, c, k2) PKV_PAIR_ROUND(c, d, a, b, k3)
+                     PKV_PAIR_ROUND_LAST(b, c, d, a) PKV_ROUNDS4_OPERANDS);
 }
 #undef PKV_ROUNDS4_OPERANDS
-#undef PKV_ADJ_ROUND_LAST
-#undef PKV_ADJ_ROUND
-#undef PKV_RH_ROUND_LAST
-#undef PKV_RH_ROUND
+#undef PKV_ALIGN8
+#undef PKV_PAIR_ROUND_LAST
+#undef PKV_PAIR_ROUND
 #undef PKV_ROUND_HEAD
 
 // 16 paired rounds; kw[j] = K + W of round t0 + j, `after` = K + W of round t0 + 16 (any value
 // when the caller recomputes q before the next round).
-template <Pairing P>
 __device__ __forceinline__ void pair_rounds16(uint32_t x[4], uint32_t& q, const PairLane& pl, const uint32_t* kw,
                                               uint32_t after) {
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, kw[1], kw[2], kw[3], kw[4]);
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, kw[5], kw[6], kw[7], kw[8]);
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, kw[9], kw[10], kw[11], kw[12]);
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, kw[13], kw[14], kw[15], after);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[1], kw[2], kw[3], kw[4]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[5], kw[6], kw[7], kw[8]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[9], kw[10], kw[11], kw[12]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[13], kw[14], kw[15], after);
 }
 
 // Compression 1 of a key on the consumer: rounds 0..15 take K + W from kw (registers), the other
@@ -323,54 +288,46 @@ __device__ __forceinline__ void pair_rounds16(uint32_t x[4], uint32_t& q, const 
 // barrier that makes a phase's rows visible sits four rounds before the phase starts, and the rows
 // are read right after it, so the last four rounds of the previous phase cover their LDS latency;
 // those four rounds leave Q of the phase's first round to be formed from the new words.
-template <Pairing P>
 __device__ __forceinline__ void pair_comp1(uint32_t x[4], const PairLane& pl, const uint32_t kw[16],
                                            const uint4 (*rows)[kPpChains], uint32_t c) {
     uint32_t ka[16], kb[16];
     uint32_t q = (x[3] + kw[0]) & pl.nm;
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, kw[1], kw[2], kw[3], kw[4]);
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, kw[5], kw[6], kw[7], kw[8]);
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, kw[9], kw[10], kw[11], kw[12]);      // rounds 0..11
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[1], kw[2], kw[3], kw[4]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[5], kw[6], kw[7], kw[8]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[9], kw[10], kw[11], kw[12]);      // rounds 0..11
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < 4; ++j) get4(&rows[j][c], ka + 4 * j);
-    pair_rounds4_last<P>(x[0], x[1], x[2], x[3], q, pl, kw[13], kw[14], kw[15]);         // rounds 12..15
+    pair_rounds4_last(x[0], x[1], x[2], x[3], q, pl, kw[13], kw[14], kw[15]);         // rounds 12..15
     q = (x[3] + ka[0]) & pl.nm;
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, ka[1], ka[2], ka[3], ka[4]);
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, ka[5], ka[6], ka[7], ka[8]);
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, ka[9], ka[10], ka[11], ka[12]);      // rounds 16..27
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, ka[1], ka[2], ka[3], ka[4]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, ka[5], ka[6], ka[7], ka[8]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, ka[9], ka[10], ka[11], ka[12]);      // rounds 16..27
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < 4; ++j) get4(&rows[4 + j][c], kb + 4 * j);
-    pair_rounds4_last<P>(x[0], x[1], x[2], x[3], q, pl, ka[13], ka[14], ka[15]);         // rounds 28..31
+    pair_rounds4_last(x[0], x[1], x[2], x[3], q, pl, ka[13], ka[14], ka[15]);         // rounds 28..31
     q = (x[3] + kb[0]) & pl.nm;
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, kb[1], kb[2], kb[3], kb[4]);
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, kb[5], kb[6], kb[7], kb[8]);
-    pair_rounds4<P>(x[0], x[1], x[2], x[3], q, pl, kb[9], kb[10], kb[11], kb[12]);      // rounds 32..43
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kb[1], kb[2], kb[3], kb[4]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kb[5], kb[6], kb[7], kb[8]);
+    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kb[9], kb[10], kb[11], kb[12]);      // rounds 32..43
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < 4; ++j) get4(&rows[8 + j][c], ka + 4 * j);
-    pair_rounds4_last<P>(x[0], x[1], x[2], x[3], q, pl, kb[13], kb[14], kb[15]);         // rounds 44..47
+    pair_rounds4_last(x[0], x[1], x[2], x[3], q, pl, kb[13], kb[14], kb[15]);         // rounds 44..47
     q = (x[3] + ka[0]) & pl.nm;
-    pair_rounds16<P>(x, q, pl, ka, 0u);                                                   // rounds 48..63
+    pair_rounds16(x, q, pl, ka, 0u);                                                   // rounds 48..63
 }
 
-// v of the pair's other lane.
-template <Pairing P>
+// v of the pair's other lane (DPP row_ror:8).
 __device__ __forceinline__ uint32_t lane_swap(uint32_t v) {
-    constexpr int kCtrl = P == Pairing::RowHalves ? 0x128 : 0xB1;     // row_ror:8 / quad_perm [1,0,3,2]
-    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), kCtrl, 0xF, 0xF, false));
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x128, 0xF, 0xF, false));
 }
 
 // a + (b of the partner lane), one instruction; two wait states cover a just-written b.
-template <Pairing P>
 __device__ __forceinline__ uint32_t add_swapped(uint32_t a, uint32_t b) {
     uint32_t r;
-    if constexpr (P == Pairing::RowHalves)
-        asm("s_nop 1\n\tv_add_u32_dpp %0, %1, %2 row_ror:8 row_mask:0xf bank_mask:0xf" : "=v"(r) : "v"(b), "v"(a));
-    else
-        asm("s_nop 1\n\tv_add_u32_dpp %0, %1, %2 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf"
-            : "=v"(r) : "v"(b), "v"(a));
+    asm("s_nop 1\n\tv_add_u32_dpp %0, %1, %2 row_ror:8 row_mask:0xf bank_mask:0xf" : "=v"(r) : "v"(b), "v"(a));
     return r;
 }
 
@@ -401,10 +358,9 @@ __device__ __forceinline__ PairK make_pair_k(bool odd) {
 // W_{2j+1}.  v[k] is the lane's own word k+1 steps back.  The e lane needs its partner's
 // W_{2j-7} and W_{2j-15}, the a lane its partner's W_{2j-6} and W_{2j-14}; each lane sends
 // sigma0 of the older one plus the newer one.
-template <Pairing P>
 __device__ __forceinline__ uint32_t pair_schedule_step(uint32_t v[8], uint32_t m) {
     const uint32_t z = dev::ssig0(bsel(m, v[7], v[6])) + bsel(m, v[3], v[2]);
-    const uint32_t w = dev::ssig1(v[0]) + add_swapped<P>(v[7], z);
+    const uint32_t w = dev::ssig1(v[0]) + add_swapped(v[7], z);
 #pragma unroll
     for (int k = 7; k > 0; --k) v[k] = v[k - 1];
     v[0] = w;
@@ -413,11 +369,11 @@ __device__ __forceinline__ uint32_t pair_schedule_step(uint32_t v[8], uint32_t m
 
 // Steps j = J0 .. J0+7 of the paired schedule; each lane writes K + W of its word into a column of
 // uint4 rows whose first row holds words T0 .. T0+3 (kw1hi: T0 = 16; a token slot: T0 = 0).
-template <Pairing P, int J0, int T0 = 16>
+template <int J0, int T0 = 16>
 __device__ __forceinline__ void pair_schedule8(uint32_t v[8], const PairK& pk, uint32_t* col) {
 #pragma unroll
     for (int j = J0; j < J0 + 8; ++j) {
-        const uint32_t w = pair_schedule_step<P>(v, pk.m);
+        const uint32_t w = pair_schedule_step(v, pk.m);
         const uint32_t k = pk.k[j];
         // word t = 2j + odd lives at [(t - T0) / 4][chain].component(t % 4); the lane's column
         // pointer already includes its chain and parity
@@ -440,7 +396,6 @@ __device__ __forceinline__ void load_tokens_pair(const int32_t* tp, int64_t key,
 // Token-only data of one key (B = 16) by a lane pair: each lane writes its parity of compression
 // 1's words 8..15 (and their K + W) and of compression 2's K + W words, computing its parity of
 // compression 2's schedule with pair_schedule8.
-template <Pairing P>
 __device__ __forceinline__ void produce_key_pair(PpShared& sh, uint32_t chain, bool odd, const PairK& pk, int buf,
                                                  const uint32_t tk[8]) {
     const uint32_t o = odd ? 1u : 0u;
@@ -467,9 +422,9 @@ __device__ __forceinline__ void produce_key_pair(PpShared& sh, uint32_t chain, b
     uint32_t v[8];                                     // own words, newest first
 #pragma unroll
     for (int k = 0; k < 8; ++k) v[k] = own[7 - k];
-    pair_schedule8<P, 8, 0>(v, pk, col);
-    pair_schedule8<P, 16, 0>(v, pk, col);
-    pair_schedule8<P, 24, 0>(v, pk, col);
+    pair_schedule8<8, 0>(v, pk, col);
+    pair_schedule8<16, 0>(v, pk, col);
+    pair_schedule8<24, 0>(v, pk, col);
 }
 
 // P consumer/helper pairs per workgroup (P = 2 puts two consumers on one compute unit, each on its
@@ -483,9 +438,8 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
     const uint32_t pair = wave % P;                // consumers are waves 0..P-1, helpers P..2P-1
     PpShared& sh = sh_pairs[pair];
     const uint32_t lane = threadIdx.x & 63;
-    constexpr Pairing kP = Pairing::RowHalves;
-    const uint32_t c = pair_chain<kP>(lane);                   // chain of this lane pair
-    const bool odd = pair_is_a<kP>(lane);
+    const uint32_t c = pair_chain(lane);                   // chain of this lane pair
+    const bool odd = pair_is_a(lane);
     const uint32_t base = (blockIdx.x * P + pair) * kPpChains;
     const uint32_t r = base + c;
     int64_t t0 = 0, k0 = 0, n = 0;
@@ -533,18 +487,18 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             for (int ph = 0; ph < 16; ++ph) get4(&sh.kw2[buf][ph][c], kw2 + 4 * ph);
 #pragma unroll
             for (int j = 0; j < 4; ++j) x[j] = iv[j];
-            pair_comp1<kP>(x, pl, kw, sh.kw1hi, c);            // three barriers inside
+            pair_comp1(x, pl, kw, sh.kw1hi, c);            // three barriers inside
 #pragma unroll
             for (int j = 0; j < 4; ++j) { hmid[j] = x[j] + iv[j]; x[j] = hmid[j]; }
             q = (x[3] + kw2[0]) & pl.nm;
 #pragma unroll
             for (int ph = 0; ph < 4; ++ph)                     // compression 2
-                pair_rounds16<kP>(x, q, pl, kw2 + 16 * ph, ph < 3 ? kw2[16 * ph + 16] : 0u);
+                pair_rounds16(x, q, pl, kw2 + 16 * ph, ph < 3 ? kw2[16 * ph + 16] : 0u);
             uint32_t key[4];                                   // the key on the a lane
 #pragma unroll
             for (int j = 0; j < 4; ++j) key[j] = x[j] + hmid[j];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) kwp[j] = lane_swap<kP>(key[j]) + kRoundK[j];
+            for (int j = 0; j < 4; ++j) kwp[j] = lane_swap(key[j]) + kRoundK[j];
             if (odd) {
                 if (i < n)
                     reinterpret_cast<uint4*>(a.keys)[k0 + i] =
@@ -564,7 +518,7 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
         uint32_t tk[8], pre[8];
         load_tokens_pair(tp, 0, n, odd, tk);
         load_tokens_pair(tp, 1, n, odd, pre);
-        produce_key_pair<kP>(sh, c, odd, pk, 0, tk);
+        produce_key_pair(sh, c, odd, pk, 0, tk);
         __syncthreads();                                       // prologue
         for (int64_t i = 0; i < nmax; ++i) {
             const int buf = static_cast<int>(i & 1);
@@ -579,16 +533,16 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             v[5] = dsel[0];
             v[6] = bsel(pk.m, pv[3], pv[2]);
             v[7] = bsel(pk.m, pv[1], pv[0]);
-            pair_schedule8<kP, 8>(v, pk, kw1hi_col);
+            pair_schedule8<8>(v, pk, kw1hi_col);
             __syncthreads();
-            pair_schedule8<kP, 16>(v, pk, kw1hi_col);
+            pair_schedule8<16>(v, pk, kw1hi_col);
             __syncthreads();
-            pair_schedule8<kP, 24>(v, pk, kw1hi_col);
+            pair_schedule8<24>(v, pk, kw1hi_col);
             __syncthreads();
 #pragma unroll
             for (int q = 0; q < 8; ++q) tk[q] = pre[q];        // the next key's token-only data
             load_tokens_pair(tp, i + 2, n, odd, pre);
-            produce_key_pair<kP>(sh, c, odd, pk, buf ^ 1, tk);
+            produce_key_pair(sh, c, odd, pk, buf ^ 1, tk);
             __syncthreads();                                   // end of key
         }
     }
@@ -830,7 +784,7 @@ __device__ __forceinline__ void load_production_pair(const int32_t* tp, uint32_t
 // Production g by a lane pair: each lane byte-swaps its parity of the message words, computes its
 // parity of the schedule (pair_schedule8) and writes its K + W words into the slot; for c == 1
 // also its parity of compression 1's token words.
-template <Pairing P, typename Shared>
+template <typename Shared>
 __device__ __forceinline__ void produce_comp_pair(Shared& sh, uint32_t chain, bool odd, const PairK& pk, uint32_t m,
                                                   uint32_t bitlen, int64_t g, const PairProduction& pr) {
     const int64_t key = g / m;
@@ -866,9 +820,9 @@ __device__ __forceinline__ void produce_comp_pair(Shared& sh, uint32_t chain, bo
     uint32_t v[8];                                     // own words, newest first
 #pragma unroll
     for (int k = 0; k < 8; ++k) v[k] = own[7 - k];
-    pair_schedule8<P, 8, 0>(v, pk, col);
-    pair_schedule8<P, 16, 0>(v, pk, col);
-    pair_schedule8<P, 24, 0>(v, pk, col);
+    pair_schedule8<8, 0>(v, pk, col);
+    pair_schedule8<16, 0>(v, pk, col);
+    pair_schedule8<24, 0>(v, pk, col);
 }
 
 struct PpmShared {
@@ -883,9 +837,8 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
     __shared__ PpmShared sh;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t lane = threadIdx.x & 63;
-    constexpr Pairing kP = Pairing::Adjacent;
-    const uint32_t c = pair_chain<kP>(lane);                   // chain of this lane pair
-    const bool odd = pair_is_a<kP>(lane);
+    const uint32_t c = pair_chain(lane);                   // chain of this lane pair
+    const bool odd = pair_is_a(lane);
     const uint32_t r = blockIdx.x * kPpChains + c;
     const uint32_t B = a.block, m = B / 16;
     const uint32_t bitlen = (32u + 4u * B) * 8u;
@@ -930,14 +883,14 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) x[j] = iv[j];
             q = (x[3] + kw[0]) & pl.nm;
-            pair_rounds16<kP>(x, q, pl, kw, 0u);               // rounds 0..15
+            pair_rounds16(x, q, pl, kw, 0u);               // rounds 0..15
             __syncthreads();
 #pragma unroll
             for (int ph = 0; ph < 3; ++ph) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) get4(&sh.kw1hi[4 * ph + j][c], kw + 4 * j);
                 q = (x[3] + kw[0]) & pl.nm;
-                pair_rounds16<kP>(x, q, pl, kw, 0u);
+                pair_rounds16(x, q, pl, kw, 0u);
                 if (ph < 2) __syncthreads();
             }
 #pragma unroll
@@ -951,21 +904,21 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
                 q = (x[3] + kwa[0]) & pl.nm;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) get4(&sh.kwt[slot][4 + j][c], kwb + 4 * j);
-                pair_rounds16<kP>(x, q, pl, kwa, kwb[0]);      // rounds 0..15
+                pair_rounds16(x, q, pl, kwa, kwb[0]);      // rounds 0..15
 #pragma unroll
                 for (int j = 0; j < 4; ++j) get4(&sh.kwt[slot][8 + j][c], kwa + 4 * j);
-                pair_rounds16<kP>(x, q, pl, kwb, kwa[0]);      // rounds 16..31
+                pair_rounds16(x, q, pl, kwb, kwa[0]);      // rounds 16..31
 #pragma unroll
                 for (int j = 0; j < 4; ++j) get4(&sh.kwt[slot][12 + j][c], kwb + 4 * j);
-                pair_rounds16<kP>(x, q, pl, kwa, kwb[0]);      // rounds 32..47
+                pair_rounds16(x, q, pl, kwa, kwb[0]);      // rounds 32..47
 #pragma unroll
                 for (int j = 0; j < 4; ++j) get4(&sh.kwt[nslot][j][c], kwa + 4 * j);
-                pair_rounds16<kP>(x, q, pl, kwb, 0u);          // rounds 48..63
+                pair_rounds16(x, q, pl, kwb, 0u);          // rounds 48..63
 #pragma unroll
                 for (int j = 0; j < 4; ++j) h[j] += x[j];
                 if (cc == m) {                                 // h on the a lane is the key
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) kwp[j] = lane_swap<kP>(h[j]) + kRoundK[j];
+                    for (int j = 0; j < 4; ++j) kwp[j] = lane_swap(h[j]) + kRoundK[j];
                     if (odd) {
                         if (i < n)
                             reinterpret_cast<uint4*>(a.keys)[k0 + i] =
@@ -988,8 +941,8 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
         PairProduction p0, p1, p2;
         load_production_pair(tp, B, m, n, 0, odd, p0);
         load_production_pair(tp, B, m, n, 1, odd, p1);
-        produce_comp_pair<kP>(sh, c, odd, pk, m, bitlen, 0, p0);
-        produce_comp_pair<kP>(sh, c, odd, pk, m, bitlen, 1, p1);
+        produce_comp_pair(sh, c, odd, pk, m, bitlen, 0, p0);
+        produce_comp_pair(sh, c, odd, pk, m, bitlen, 1, p1);
         load_production_pair(tp, B, m, n, 2, odd, p0);         // p0, p1 = productions g + 2, g + 3
         load_production_pair(tp, B, m, n, 3, odd, p1);
         __syncthreads();                                       // prologue
@@ -1005,11 +958,11 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
             v[5] = dsel[0];
             v[6] = bsel(pk.m, pv[3], pv[2]);
             v[7] = bsel(pk.m, pv[1], pv[0]);
-            pair_schedule8<kP, 8>(v, pk, kw1hi_col);
+            pair_schedule8<8>(v, pk, kw1hi_col);
             __syncthreads();
-            pair_schedule8<kP, 16>(v, pk, kw1hi_col);
+            pair_schedule8<16>(v, pk, kw1hi_col);
             __syncthreads();
-            pair_schedule8<kP, 24>(v, pk, kw1hi_col);
+            pair_schedule8<24>(v, pk, kw1hi_col);
             __syncthreads();
             __syncthreads();                                   // end of compression 1
             for (uint32_t cc = 1; cc <= m; ++cc) {
@@ -1017,7 +970,7 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
                 p2 = p0;
                 p0 = p1;
                 load_production_pair(tp, B, m, n, g + 2, odd, p1);
-                if (g < total) produce_comp_pair<kP>(sh, c, odd, pk, m, bitlen, g, p2);
+                if (g < total) produce_comp_pair(sh, c, odd, pk, m, bitlen, g, p2);
                 __syncthreads();                               // end of token compression cc
             }
         }
