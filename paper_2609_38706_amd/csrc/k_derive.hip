@@ -324,13 +324,6 @@ __device__ __forceinline__ uint32_t lane_swap(uint32_t v) {
     return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x128, 0xF, 0xF, false));
 }
 
-// a + (b of the partner lane), one instruction; two wait states cover a just-written b.
-__device__ __forceinline__ uint32_t add_swapped(uint32_t a, uint32_t b) {
-    uint32_t r;
-    asm("s_nop 1\n\tv_add_u32_dpp %0, %1, %2 row_ror:8 row_mask:0xf bank_mask:0xf" : "=v"(r) : "v"(b), "v"(a));
-    return r;
-}
-
 // Bitwise select m ? a : b in one instruction (v_bfi_b32), with the lane's parity mask m as an
 // ordinary register: no condition register to rebuild around each use.
 __device__ __forceinline__ uint32_t bsel(uint32_t m, uint32_t a, uint32_t b) {
@@ -357,12 +350,32 @@ __device__ __forceinline__ PairK make_pair_k(bool odd) {
 // One step of a message schedule split over a lane pair: the e lane computes W_{2j}, the a lane
 // W_{2j+1}.  v[k] is the lane's own word k+1 steps back.  The e lane needs its partner's
 // W_{2j-7} and W_{2j-15}, the a lane its partner's W_{2j-6} and W_{2j-14}; each lane sends
-// sigma0 of the older one plus the newer one.
-__device__ __forceinline__ uint32_t pair_schedule_step(uint32_t v[8], uint32_t m) {
-    const uint32_t z = dev::ssig0(bsel(m, v[7], v[6])) + bsel(m, v[3], v[2]);
-    const uint32_t w = dev::ssig1(v[0]) + add_swapped(v[7], z);
+// sigma0 of the older one plus the newer one (z), and adds what its partner sent.  Returns the
+// new word and sets wk = word + k.  One asm block of 14 eight-byte instructions, aligned to 8
+// bytes (see the rounds above); the partner's z is read by DPP four instructions after it is
+// written, so no wait state is needed.
+__device__ __forceinline__ uint32_t pair_schedule_step(uint32_t v[8], uint32_t m, uint32_t k, uint32_t& wk) {
+    uint32_t w, t0, t1, t2, z;
+    asm volatile(".p2align 3\n"
+                 "v_bfi_b32 %[t0], %[m], %[v7], %[v6]\n"                  // sigma0 operand
+                 "v_alignbit_b32 %[t1], %[t0], %[t0], 7\n"
+                 "v_alignbit_b32 %[t2], %[t0], %[t0], 18\n"
+                 "v_lshrrev_b32_e64 %[t0], 3, %[t0]\n"
+                 "v_bitop3_b32 %[z], %[t1], %[t2], %[t0] bitop3:0x96\n"
+                 "v_bfi_b32 %[t0], %[m], %[v3], %[v2]\n"
+                 "v_add_u32_e64 %[z], %[z], %[t0]\n"                      // what the partner needs
+                 "v_alignbit_b32 %[t1], %[v0], %[v0], 17\n"
+                 "v_alignbit_b32 %[t2], %[v0], %[v0], 19\n"
+                 "v_lshrrev_b32_e64 %[t0], 10, %[v0]\n"
+                 "v_bitop3_b32 %[t1], %[t1], %[t2], %[t0] bitop3:0x96\n"  // sigma1(own word 2 back)
+                 "v_add_u32_dpp %[t2], %[z], %[v7] row_ror:8 row_mask:0xf bank_mask:0xf\n"
+                 "v_add_u32_e64 %[w], %[t1], %[t2]\n"
+                 "v_add_u32_e64 %[wk], %[w], %[k]\n"
+                 : [w] "=&v"(w), [wk] "=&v"(wk), [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [z] "=&v"(z)
+                 : [m] "v"(m), [v0] "v"(v[0]), [v2] "v"(v[2]), [v3] "v"(v[3]), [v6] "v"(v[6]), [v7] "v"(v[7]),
+                   [k] "v"(k));
 #pragma unroll
-    for (int k = 7; k > 0; --k) v[k] = v[k - 1];
+    for (int j = 7; j > 0; --j) v[j] = v[j - 1];
     v[0] = w;
     return w;
 }
@@ -373,11 +386,11 @@ template <int J0, int T0 = 16>
 __device__ __forceinline__ void pair_schedule8(uint32_t v[8], const PairK& pk, uint32_t* col) {
 #pragma unroll
     for (int j = J0; j < J0 + 8; ++j) {
-        const uint32_t w = pair_schedule_step(v, pk.m);
-        const uint32_t k = pk.k[j];
+        uint32_t wk;
+        pair_schedule_step(v, pk.m, pk.k[j], wk);
         // word t = 2j + odd lives at [(t - T0) / 4][chain].component(t % 4); the lane's column
         // pointer already includes its chain and parity
-        col[((2 * j - T0) >> 2) * (kPpChains * 4) + ((2 * j) & 3)] = w + k;
+        col[((2 * j - T0) >> 2) * (kPpChains * 4) + ((2 * j) & 3)] = wk;
     }
 }
 
