@@ -267,6 +267,26 @@ __device__ __forceinline__ void pair_rounds4_last(uint32_t& x0, uint32_t& x1, ui
     asm volatile(PKV_ALIGN8 PKV_PAIR_ROUND(a, b, c, d, k1) PKV_PAIR_ROUND(d, a, b, c, k2) PKV_PAIR_ROUND(c, d, a, b, k3)
                      PKV_PAIR_ROUND_LAST(b, c, d, a) PKV_ROUNDS4_OPERANDS);
 }
+
+// 16 paired rounds as one asm statement, for K + W words that are all in registers already (the
+// compiler's separator and the alignment padding then come once per 16 rounds instead of once
+// per 4).  kw[j] = K + W of round t0 + j, `after` = K + W of round t0 + 16.
+#define PKV_PAIR_ROUNDS4(K1, K2, K3, K4)                                                            \
+    PKV_PAIR_ROUND(a, b, c, d, K1) PKV_PAIR_ROUND(d, a, b, c, K2) PKV_PAIR_ROUND(c, d, a, b, K3)      \
+    PKV_PAIR_ROUND(b, c, d, a, K4)
+__device__ __forceinline__ void pair_rounds16_regs(uint32_t x[4], uint32_t& q, const PairLane& pl, const uint32_t* kw,
+                                                   uint32_t after) {
+    uint32_t t0, t1, t2;
+    asm volatile(PKV_ALIGN8 PKV_PAIR_ROUNDS4(k1, k2, k3, k4) PKV_PAIR_ROUNDS4(k5, k6, k7, k8)
+                     PKV_PAIR_ROUNDS4(k9, k10, k11, k12) PKV_PAIR_ROUNDS4(k13, k14, k15, k16)
+                 : [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [q] "+v"(q), [a] "+v"(x[0]), [b] "+v"(x[1]),
+                   [c] "+v"(x[2]), [d] "+v"(x[3])
+                 : [m] "v"(pl.m), [r1] "v"(pl.r1), [r2] "v"(pl.r2), [r3] "v"(pl.r3), [k1] "v"(kw[1]),
+                   [k2] "v"(kw[2]), [k3] "v"(kw[3]), [k4] "v"(kw[4]), [k5] "v"(kw[5]), [k6] "v"(kw[6]),
+                   [k7] "v"(kw[7]), [k8] "v"(kw[8]), [k9] "v"(kw[9]), [k10] "v"(kw[10]), [k11] "v"(kw[11]),
+                   [k12] "v"(kw[12]), [k13] "v"(kw[13]), [k14] "v"(kw[14]), [k15] "v"(kw[15]), [k16] "v"(after));
+}
+#undef PKV_PAIR_ROUNDS4
 #undef PKV_ROUNDS4_OPERANDS
 #undef PKV_ALIGN8
 #undef PKV_PAIR_ROUND_LAST
@@ -506,7 +526,7 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             q = (x[3] + kw2[0]) & pl.nm;
 #pragma unroll
             for (int ph = 0; ph < 4; ++ph)                     // compression 2
-                pair_rounds16(x, q, pl, kw2 + 16 * ph, ph < 3 ? kw2[16 * ph + 16] : 0u);
+                pair_rounds16_regs(x, q, pl, kw2 + 16 * ph, ph < 3 ? kw2[16 * ph + 16] : 0u);
             uint32_t key[4];                                   // the key on the a lane
 #pragma unroll
             for (int j = 0; j < 4; ++j) key[j] = x[j] + hmid[j];
