@@ -92,9 +92,9 @@ def chain_ceiling_frac(n_chains: int) -> float:
 
 
 # The tighter bound of the kernels' own round: one wavefront issues a VALU instruction at most every
-# 4 cycles, and the lane-pair round of a chain is 11 instructions long, so a chain finishes at most
-# one round per 44 cycles (and needs two lanes, so 32 chains fill a wavefront).
-PAIR_ROUND_INSTRUCTIONS = 11
+# 4 cycles, and the lane-pair round of a chain is 10 instructions long, so a chain finishes at most
+# one round per 40 cycles (and needs two lanes, so 32 chains fill a wavefront).
+PAIR_ROUND_INSTRUCTIONS = 10
 
 
 def issue_ceiling_frac(n_chains: int) -> float:
