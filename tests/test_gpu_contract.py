@@ -99,6 +99,27 @@ def test_derive_kernels_agree_at_the_switches(pkv, n_req, block):
     assert (db.host_keys() == want).all()
 
 
+@pytest.mark.parametrize("block", [16, 32])
+@pytest.mark.parametrize("n_req", [1, 7, 8, 9, 15, 16, 17, 24, 31, 33, 40, 63, 65])
+def test_lane_pair_rows_with_partial_waves(pkv, n_req, block):
+    """The lane-pair kernels give chain i of a row lanes i and i + 8; request counts that end inside
+    a row, inside a wavefront or just past one, with chains of different lengths (0 to 40 keys, so
+    partners stop at different keys), must all give the oracle's keys."""
+    rng = np.random.default_rng(1000 + n_req + block)
+    lens = rng.integers(0, 40 * block, size=n_req)
+    off = np.zeros(n_req + 1, np.int64)
+    off[1:] = np.cumsum(lens)
+    toks = rng.integers(0, 128256, size=int(off[-1]), dtype=np.int32)
+    descs = [_with(BASE, b"salt", b"%d" % i) for i in range(5)]
+    b = Batch(toks, off, block, descs, rng.integers(0, 5, size=n_req).astype(np.int32))
+    db = gpu_batch(b)
+    db.digest()
+    db.derive()
+    want, _ = oracle_keys(b)
+    assert db.host_status() == 0
+    assert (db.host_keys() == want).all()
+
+
 @pytest.mark.parametrize("name", [n for n, _ in BASE])
 def test_one_dimension_change_changes_every_key_on_gpu(pkv, name):
     rng = np.random.default_rng(11)
