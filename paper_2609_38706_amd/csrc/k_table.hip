@@ -231,13 +231,33 @@ struct StoreArgs {
 };
 
 __device__ __forceinline__ bool candidate(const StoreArgs& a, uint64_t wave_base, uint64_t k, int64_t total) {
-    uint32_t lo = 0, hi = a.n_req;            // largest r with key_off[r] <= wave_base
+    // largest r < n_req with key_off[r] <= wave_base: start where equal-length requests would put
+    // it, widen by doubling steps until [lo, hi) brackets it, then bisect (a batch of equal
+    // lengths needs two loads instead of log2(n_req)); key_off[0] = 0 <= wave_base always
+    const int64_t wb = static_cast<int64_t>(wave_base);
+    const uint64_t n = a.n_req;
+    uint64_t lo = 0, hi = n;
+    if (total > 0 && n > 2) {
+        uint64_t g = static_cast<uint64_t>(static_cast<double>(wave_base) * static_cast<double>(n) /
+                                           static_cast<double>(total));
+        if (g >= n) g = n - 1;
+        uint64_t step = 1;
+        if (a.key_off[g] <= wb) {
+            lo = g;
+            while (lo + step < n && a.key_off[lo + step] <= wb) { lo += step; step <<= 1; }
+            hi = lo + step < n ? lo + step : n;
+        } else {
+            hi = g;
+            while (hi > step && a.key_off[hi - step] > wb) { hi -= step; step <<= 1; }
+            lo = hi > step ? hi - step : 0;
+        }
+    }
     while (hi - lo > 1) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (a.key_off[mid] <= static_cast<int64_t>(wave_base)) lo = mid; else hi = mid;
+        const uint64_t mid = (lo + hi) >> 1;
+        if (a.key_off[mid] <= wb) lo = mid; else hi = mid;
     }
     if (static_cast<int64_t>(k) >= total) return false;
-    uint32_t r = lo;
+    uint32_t r = static_cast<uint32_t>(lo);
     while (r + 1 < a.n_req && a.key_off[r + 1] <= static_cast<int64_t>(k)) ++r;
     const int64_t j = static_cast<int64_t>(k) - a.key_off[r];
     int64_t h = a.hits[r];
