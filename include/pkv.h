@@ -151,7 +151,8 @@ int pkv_lookup_prefix(const pkv_table* table, const uint8_t* d_keys, const int64
  * d_n_new: one uint64 counter that the call increments by the number of new entries; the
  * caller zeroes it.  d_new_slots: NULL, or room for n_keys uint64: the slot index of each new
  * entry is appended at d_new_slots[old *d_n_new ...] (a reserved key's slot is `capacity` or
- * `capacity + 1`; bit 63 marks a slot that was removed by eviction before).
+ * `capacity + 1`; bit 63 marks a slot that was removed by eviction before, bit 62 a key whose
+ * first 8 bytes equal one of the index's marker values, stored with the substitute claim word).
  * No free slot for a new key sets PKV_EFULL. */
 int pkv_store(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off,
               uint32_t n_req, uint64_t n_keys, const int32_t* d_hit_blocks, const uint64_t* d_locs,

@@ -356,7 +356,7 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
                         publish_slot(t, s, kw, want);
                         if (a.epochs) a.epochs[s] = a.epoch;
                         claimed = true;
-                        my_slot = s | (c == kLoRemoved ? kFromRemoved : 0);
+                        my_slot = s | (c == kLoRemoved ? kFromRemoved : 0) | (kw.claim == kLoSub ? kSubLogged : 0);
                         break;
                     }
                     continue;                        // lost the race: read the slot again
@@ -418,7 +418,7 @@ __global__ __launch_bounds__(256) void k_store_finish_log(Tab t, const uint64_t*
     if (n > max_slots) n = max_slots;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
-        const uint64_t s = slots[i] & ~kFromRemoved;
+        const uint64_t s = slots[i] & ~kLogFlags;
         if (s > t.capacity + 1) continue;
         uint64_t* p = t.loc(s);
         const uint64_t l = *p;
@@ -457,11 +457,13 @@ __global__ __launch_bounds__(kStoreThreads) void k_store_finish_probe(StoreArgs 
 // ---- rollback and export ------------------------------------------------------------------------
 // A slot back to the state a store found it in: never used, or removed.  Only a substitute claim
 // word comes with a non-zero flag word.
-__device__ __forceinline__ void free_slot(const Tab& t, uint64_t s, bool removed) {
-    uint64_t* c = t.lo(s);
-    if (*c == kLoSub) *t.flag(s) = 0;
-    *c = removed ? kLoRemoved : kLoEmpty;
+__device__ __forceinline__ void clear_slot(const Tab& t, uint64_t s, bool removed, bool sub) {
+    if (sub) *t.flag(s) = 0;
+    *t.lo(s) = removed ? kLoRemoved : kLoEmpty;
     *reinterpret_cast<uint4*>(t.pair(s)) = make_uint4(~0u, ~0u, ~0u, ~0u);   // key bytes 8..15, kEmpty
+}
+__device__ __forceinline__ void free_slot(const Tab& t, uint64_t s, bool removed) {
+    clear_slot(t, s, removed, *t.lo(s) == kLoSub);
 }
 
 __global__ __launch_bounds__(256) void k_rollback(Tab t, const uint64_t* slots, const uint64_t* n_slots,
@@ -470,9 +472,10 @@ __global__ __launch_bounds__(256) void k_rollback(Tab t, const uint64_t* slots, 
     if (n > max_slots) n = max_slots;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
-        const uint64_t s = slots[i] & ~kFromRemoved;
-        if (s < t.capacity) {
-            free_slot(t, s, (slots[i] & kFromRemoved) != 0);
+        const uint64_t e = slots[i];
+        const uint64_t s = e & ~kLogFlags;
+        if (s < t.capacity) {                        // the log says how the slot was found: no read
+            clear_slot(t, s, (e & kFromRemoved) != 0, (e & kSubLogged) != 0);
         } else if (s <= t.capacity + 1) {
             *t.loc(s) = kEmpty;
         }

@@ -44,6 +44,8 @@ static constexpr uint64_t kLoSub = ~0ull - 2;
 static constexpr uint64_t kEmpty = ~0ull;
 static constexpr uint64_t kFresh = 1ull << 63;
 static constexpr uint64_t kFromRemoved = 1ull << 63;   // slot-log flag: the claimed slot was a removed entry
+static constexpr uint64_t kSubLogged = 1ull << 62;     // slot-log flag: the slot's claim word is the substitute
+static constexpr uint64_t kLogFlags = kFromRemoved | kSubLogged;
 static constexpr uint32_t kResvW = 0xFEFFFFFFu;     // last 32-bit word of the second reserved pattern
 static constexpr uint32_t kSlotsPerBucket = 4;
 static constexpr uint64_t kBucketWords = 16;        // 128 bytes
