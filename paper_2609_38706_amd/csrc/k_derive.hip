@@ -777,8 +777,9 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pc(ChainArgs a) {
 // ---- B = 16m (m >= 2), each chain on a lane pair (used while chains are very scarce) -----------
 // The consumer of k_derive_m16_pc with the lane-pair rounds of k_derive_b16_pp: compression 1 of a
 // key runs in four barrier phases while the helper's lane pairs compute its schedule; each of the
-// m token-only compressions reads its 64 K + W words from a ring of three LDS slots that one
-// helper lane per chain fills two compressions ahead.
+// m token-only compressions reads its 64 K + W words from a ring of three LDS slots that the
+// helper's lane pairs fill two compressions ahead.
+//
 // Token words of one production for a lane pair: this lane's parity of the 16 words of token
 // compression (key, c) (for the last compression only its 8 token words; the padding is added when
 // the words are produced), and for c == 1 its parity of tokens 0..7 (compression 1's words).
