@@ -184,6 +184,54 @@ def test_lookup_and_store_random_keys(pkv, seed, capacity):
         assert check_structure(table) == len(idx)
 
 
+@pytest.mark.parametrize("shape", ["long-first", "long-last", "long-middle", "alternating", "many-empty"])
+def test_store_with_skewed_request_lengths(pkv, shape):
+    """Each store wavefront finds the request of its first key from a guess that assumes equal
+    lengths and widens from there (up or down); very unequal lengths and runs of empty requests
+    must give the same index as the oracle."""
+    import torch
+    from paper_2609_38706_amd.pipeline import export_sorted
+    rng = np.random.default_rng(7 + len(shape))
+    n_req = 700
+    lens = np.zeros(n_req, np.int64)
+    if shape == "long-first":
+        lens[0] = 3000
+        lens[1:] = rng.integers(0, 3, size=n_req - 1)
+    elif shape == "long-last":
+        lens[:-1] = rng.integers(0, 3, size=n_req - 1)
+        lens[-1] = 3000
+    elif shape == "long-middle":
+        lens[:] = rng.integers(0, 2, size=n_req)
+        lens[350] = 2500
+        lens[351:360] = 0
+    elif shape == "alternating":
+        lens[::2] = 0
+        lens[1::2] = rng.integers(1, 12, size=n_req // 2)
+    else:
+        lens[rng.permutation(n_req)[:20]] = rng.integers(60, 200, size=20)
+    ko = np.zeros(n_req + 1, np.int64)
+    ko[1:] = np.cumsum(lens)
+    n_keys = int(ko[-1])
+    keys = rng.integers(0, 256, size=(n_keys, 16), dtype=np.uint8)
+    keys[: n_keys // 3] = keys[n_keys // 3: 2 * (n_keys // 3)]       # duplicates across requests
+    locs = rng.permutation(1 << 22)[:n_keys].astype(np.uint64)
+    h = np.minimum(rng.integers(0, 4, size=n_req), lens).astype(np.int32)
+    capacity = 1 << 14
+    idx = oracle.Index(capacity)
+    table = pkv.Table(capacity)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    n_new = torch.zeros(1, dtype=torch.int64, device="cuda")
+    rc = idx.store(keys, ko, h, locs)
+    pkv.pkv_store(table, _dev(keys, torch.uint8).reshape(-1, 16), _dev(ko, torch.int64), _dev(h, torch.int32),
+                  _dev(locs, torch.int64), n_new, status)
+    torch.cuda.synchronize()
+    assert rc == 0 and int(status.item()) == 0
+    gk, gl = export_sorted(table)
+    ok, ol = idx.dump()
+    assert gk.shape == ok.shape and (gk == ok).all() and (gl == ol).all()
+    assert int(n_new.item()) == len(idx)
+
+
 def _marker_prefixed_pool(rng):
     """Keys whose first 8 bytes (the slot claim word, little-endian) equal the never-used marker
     (all 0xFF), the removed marker (0xFE then 0xFF) or the substitute claim word (0xFD then 0xFF),
