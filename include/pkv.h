@@ -219,9 +219,11 @@ int pkv_sum_hits(const int32_t* d_hit_blocks, uint32_t n_req, const int64_t* d_g
  *
  * pkv_tensor_roots (device): the roots of n_tensors tensors whose bytes lie in d_data (n_bytes, a
  * multiple of 4, 4-byte aligned); tensor t occupies [d_tensor_off[t], d_tensor_off[t] +
- * d_tensor_len[t]) (int64; every start a multiple of 4; tensors may leave gaps and may overlap).
+ * d_tensor_len[t]) (int64; every start a multiple of 4).  Tensors may leave gaps and may overlap,
+ * provided their lengths add up to at most n_bytes: the work area is sized for that.
  * d_work: pkv_tree_work_bytes(n_bytes, n_tensors) bytes, 256-byte aligned; d_roots: n_tensors x 32
- * bytes.  A tensor outside the data sets PKV_ELAYOUT.
+ * bytes.  A tensor outside the data, or lengths that add up to more than n_bytes, set PKV_ELAYOUT;
+ * the roots are then unspecified, and nothing outside d_work and d_roots is written.
  * pkv_content_identity (host, pure): the identity from the tensors' metadata and roots;
  * duplicate tensor names or configuration keys are PKV_EDUPDIM. */
 typedef struct {

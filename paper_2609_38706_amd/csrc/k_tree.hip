@@ -159,60 +159,83 @@ __device__ __forceinline__ uint32_t find_owner(const int64_t* csr, uint32_t n, i
     return i >= csr[n] ? n : owner(csr, n, i);
 }
 
+// Digests reserved per tree level in the work area (tree_layout), passed to the kernels by value.
+struct LevelBounds {
+    uint64_t b[32];
+};
+
 // One workgroup: the CSR of every level, csr_l[t] = sum over t' < t of the nodes of tensor t' at
 // level l.  Level 0 counts the leaves of each tensor (its start and length are validated: a bad
-// tensor counts one leaf and reports PKV_ELAYOUT); level l + 1 counts ceil(level l / 16).
+// tensor counts one leaf and reports PKV_ELAYOUT); level l + 1 counts ceil(level l / 16).  Tensors
+// whose lengths add up to more than the data are PKV_ELAYOUT as well: the work area reserves, per
+// level, room for the nodes of tensors that fit the data side by side (tree_layout), and a level
+// whose node total exceeds its reservation is reported the same way.  The hashing kernels never
+// index past a level's reservation, so such input yields unspecified roots but no access outside
+// the work area.
 __global__ __launch_bounds__(kCsrThreads) void k_tree_csr(const int64_t* tensor_off, const int64_t* tensor_len,
                                                           uint64_t n_bytes, uint32_t n, uint32_t levels,
-                                                          int64_t* csr, int32_t* status) {
+                                                          LevelBounds bounds, int64_t* csr, int32_t* status) {
     __shared__ int64_t wave_sum[kCsrThreads / 64];
+    __shared__ uint64_t wave_bytes[kCsrThreads / 64];
     __shared__ int64_t carry;
+    __shared__ uint64_t byte_total;
     const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (uint32_t l = 0; l < levels; ++l) {
         int64_t* out = csr + static_cast<uint64_t>(l) * (n + 1ull);
-        if (tid == 0) { carry = 0; out[0] = 0; }
+        if (tid == 0) { carry = 0; byte_total = 0; out[0] = 0; }
         __syncthreads();
         for (uint32_t base = 0; base < n; base += kCsrThreads) {
             const uint32_t t = base + tid;
             int64_t cnt = 0;
+            uint64_t bytes = 0;
             if (t < n) {
                 const int64_t a = tensor_off[t], len = tensor_len[t];
                 const bool ok = a >= 0 && len >= 0 && static_cast<uint64_t>(a) <= n_bytes &&
                                 static_cast<uint64_t>(len) <= n_bytes - static_cast<uint64_t>(a) && (a & 3) == 0;
                 if (!ok && l == 0) dev::report(status, PKV_ELAYOUT);
-                const int64_t bytes = ok ? len : 0;
-                cnt = bytes == 0 ? 1 : (bytes + kLeafBytes - 1) / kLeafBytes;
+                bytes = ok ? static_cast<uint64_t>(len) : 0u;
+                cnt = bytes == 0 ? 1 : static_cast<int64_t>((bytes + kLeafBytes - 1) / kLeafBytes);
                 for (uint32_t k = 0; k < l; ++k) cnt = (cnt + kFanIn - 1) / kFanIn;
             }
             int64_t incl = cnt;
+            uint64_t bsum = bytes;                            // each length <= n_bytes < 2^56: no overflow
 #pragma unroll
             for (int d = 1; d < 64; d <<= 1) {
                 const int64_t y = __shfl_up(incl, d, 64);
                 if (lane >= static_cast<uint32_t>(d)) incl += y;
+                bsum += __shfl_xor(bsum, d, 64);
             }
             if (lane == 63) wave_sum[wave] = incl;
+            if (lane == 0) wave_bytes[wave] = bsum;
             __syncthreads();
             int64_t wave_base = 0, total = 0;
+            uint64_t btotal = 0;
             for (uint32_t q = 0; q < kCsrThreads / 64; ++q) {
                 if (q < wave) wave_base += wave_sum[q];
                 total += wave_sum[q];
+                btotal += wave_bytes[q];
             }
             if (t < n) out[t + 1] = carry + wave_base + incl;
             __syncthreads();
-            if (tid == 0) carry += total;
+            if (tid == 0) {
+                carry += total;
+                byte_total += btotal;
+            }
             __syncthreads();
         }
+        if (tid == 0 && ((l == 0 && byte_total > n_bytes) || static_cast<uint64_t>(carry) > bounds.b[l]))
+            dev::report(status, PKV_ELAYOUT);
     }
 }
 
 // Level 0: one lane per leaf of every tensor.
 __global__ __launch_bounds__(64) void k_tree_leaves(const uint8_t* data, uint64_t n_bytes, const int64_t* tensor_off,
                                                     const int64_t* tensor_len, uint32_t n, const int64_t* csr,
-                                                    uint8_t* out) {
+                                                    uint64_t bound, uint8_t* out) {
     __shared__ int64_t lcsr[kStagedCsr];
     const int64_t i = blockIdx.x * 64ll + threadIdx.x;
     const uint32_t t = find_owner(csr, n, i, lcsr);
-    if (t == n) return;
+    if (t == n || static_cast<uint64_t>(i) >= bound) return;       // past the level's reservation
     const int64_t a = tensor_off[t], l = tensor_len[t];
     if (a < 0 || l < 0 || static_cast<uint64_t>(a) > n_bytes || static_cast<uint64_t>(l) > n_bytes - a || (a & 3) != 0)
         return;                                                       // reported by k_tree_csr
@@ -231,15 +254,17 @@ __global__ __launch_bounds__(64) void k_tree_leaves(const uint8_t* data, uint64_
 
 // Level l > 0: one lane per node; children are the level below's digests of the same tensor.
 __global__ __launch_bounds__(64) void k_tree_nodes(uint32_t n, const int64_t* csr_below, const int64_t* csr,
-                                                   const uint8_t* below, uint8_t* out) {
+                                                   const uint8_t* below, uint64_t bound_below, uint64_t bound,
+                                                   uint8_t* out) {
     __shared__ int64_t lcsr[kStagedCsr];
     const int64_t i = blockIdx.x * 64ll + threadIdx.x;
     const uint32_t t = find_owner(csr, n, i, lcsr);
-    if (t == n) return;
+    if (t == n || static_cast<uint64_t>(i) >= bound) return;       // past the level's reservation
     const int64_t j = i - csr[t];
     const int64_t c0 = csr_below[t] + kFanIn * j;
     const int64_t end = csr_below[t + 1];
     const int64_t c1 = c0 + kFanIn < end ? c0 + kFanIn : end;
+    if (c0 < 0 || c1 <= c0 || static_cast<uint64_t>(c1) > bound_below) return;   // children past the level below
     if (end - csr_below[t] == 1) {                                    // already the root: carried up
         const uint4* src = reinterpret_cast<const uint4*>(below + 32 * c0);
         uint4* dst = reinterpret_cast<uint4*>(out + 32 * i);
@@ -252,18 +277,28 @@ __global__ __launch_bounds__(64) void k_tree_nodes(uint32_t n, const int64_t* cs
     store_digest(out, i, s);
 }
 
-__global__ __launch_bounds__(256) void k_tree_roots(uint32_t n, const int64_t* csr, const uint8_t* top, uint8_t* roots) {
+__global__ __launch_bounds__(256) void k_tree_roots(uint32_t n, const int64_t* csr, const uint8_t* top, uint64_t bound,
+                                                    uint8_t* roots) {
     const uint32_t t = blockIdx.x * 256 + threadIdx.x;
     if (t >= n) return;
-    const uint4* src = reinterpret_cast<const uint4*>(top + 32 * csr[t]);
     uint4* dst = reinterpret_cast<uint4*>(roots + 32 * static_cast<uint64_t>(t));
+    const int64_t at = csr[t];
+    if (at < 0 || static_cast<uint64_t>(at) >= bound) {                // reported by k_tree_csr
+        dst[0] = make_uint4(0u, 0u, 0u, 0u);
+        dst[1] = make_uint4(0u, 0u, 0u, 0u);
+        return;
+    }
+    const uint4* src = reinterpret_cast<const uint4*>(top + 32 * at);
     dst[0] = src[0];
     dst[1] = src[1];
 }
 
 }  // namespace
 
-// Levels and work-area layout for n_bytes of data in n tensors (host and device agree on it).
+// Levels and work-area layout for n_bytes of data in n tensors (host and device agree on it).  The
+// reservation of a level holds the nodes of any tensors whose lengths sum to at most n_bytes: level
+// 0 has sum of max(1, ceil(len_t / 1024)) <= n_bytes / 1024 + n leaves, and a level of T nodes has
+// at most T / 16 + n parents.
 TreeLayout tree_layout(uint64_t n_bytes, uint32_t n) {
     TreeLayout L{};
     uint64_t leaves_max = n_bytes / kLeafBytes + 1;                   // leaves of the largest tensor
@@ -288,16 +323,19 @@ int launch_tensor_roots(const uint8_t* data, uint64_t n_bytes, const int64_t* te
     const TreeLayout L = tree_layout(n_bytes, n);
     int64_t* csr = reinterpret_cast<int64_t*>(work);
     auto csr_of = [&](uint32_t l) { return csr + static_cast<uint64_t>(l) * (n + 1ull); };
+    LevelBounds bounds{};
+    for (uint32_t l = 0; l < L.levels; ++l) bounds.b[l] = L.bound[l];
     hipLaunchKernelGGL(k_tree_csr, dim3(1), dim3(kCsrThreads), 0, s, tensor_off, tensor_len, n_bytes, n, L.levels,
-                       csr, status);
+                       bounds, csr, status);
     hipLaunchKernelGGL(k_tree_leaves, dim3(static_cast<unsigned>((L.bound[0] + 63) / 64)), dim3(64), 0, s, data,
-                       n_bytes, tensor_off, tensor_len, n, csr_of(0), work + L.digest_off[0]);
+                       n_bytes, tensor_off, tensor_len, n, csr_of(0), L.bound[0], work + L.digest_off[0]);
     for (uint32_t l = 1; l < L.levels; ++l) {
         hipLaunchKernelGGL(k_tree_nodes, dim3(static_cast<unsigned>((L.bound[l] + 63) / 64)), dim3(64), 0, s, n,
-                           csr_of(l - 1), csr_of(l), work + L.digest_off[l - 1], work + L.digest_off[l]);
+                           csr_of(l - 1), csr_of(l), work + L.digest_off[l - 1], L.bound[l - 1], L.bound[l],
+                           work + L.digest_off[l]);
     }
     hipLaunchKernelGGL(k_tree_roots, dim3((n + 255) / 256), dim3(256), 0, s, n, csr_of(L.levels - 1),
-                       work + L.digest_off[L.levels - 1], roots);
+                       work + L.digest_off[L.levels - 1], L.bound[L.levels - 1], roots);
     return check_launch("pkv_tensor_roots");
 }
 

@@ -34,7 +34,8 @@ def test_roots_at_every_edge(pkv):
         pos += int(rng.integers(0, 3)) * 4            # gaps between tensors
         starts.append(pos)
         pos += (len(d) + 3) // 4 * 4
-    pool = np.zeros(pos + 64, np.uint8)
+    # room at the end for the shared tensor below: the lengths may add up to the pool size at most
+    pool = np.zeros(pos + 64 + len(datas[9]), np.uint8)
     for st, d in zip(starts, datas):
         pool[st:st + len(d)] = np.frombuffer(d, np.uint8)
     # one more tensor sharing the bytes of tensor 9
@@ -139,3 +140,43 @@ def test_identity_of_torch_tensors_matches_oracle(pkv):
                              t.contiguous().reshape(-1).view(torch.uint8).numpy().tobytes()) for n, t in tensors],
                            config)
     assert got == want
+
+
+def _roots_call(pkv, pool_bytes, starts, lens, guard=4096):
+    """One pkv_tensor_roots call; the work buffer carries `guard` canary bytes past the size the
+    library asks for.  Returns (status, roots, canary intact)."""
+    import torch
+    dev = torch.from_numpy(pool_bytes).cuda()
+    off = torch.tensor(starts, dtype=torch.int64, device="cuda")
+    ln = torch.tensor(lens, dtype=torch.int64, device="cuda")
+    need = pkv.pkv_tree_work_bytes(dev.numel(), len(starts))
+    work = torch.full(((need + guard + 7) // 8,), 0x5A5A5A5A5A5A5A5A, dtype=torch.int64, device="cuda")
+    roots = torch.empty((len(starts), 32), dtype=torch.uint8, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pkv.pkv_tensor_roots(dev, off, ln, work[: (need + 7) // 8], roots, status)
+    tail = work[(need + 7) // 8:].cpu().numpy()
+    return int(status.item()), [bytes(r) for r in roots.cpu().numpy()], bool((tail == 0x5A5A5A5A5A5A5A5A).all())
+
+
+def test_overlapping_tensors_within_the_pool_match_oracle(pkv):
+    """Tensors that share bytes, with lengths adding up to no more than the pool: the roots are the
+    oracle's."""
+    announce("tensor roots: overlapping tensors whose lengths sum to the pool size")
+    rng = np.random.default_rng(65)
+    pool = rng.integers(0, 256, size=1 << 20, dtype=np.uint8)
+    starts = [0, 4096, 100000, 100000, 524288]
+    lens = [300000, 200000, 150000, 150000, 200000]
+    assert sum(lens) <= pool.shape[0]
+    status, got, intact = _roots_call(pkv, pool, starts, lens)
+    assert status == 0 and intact
+    assert got == [tensor_root(pool[s:s + n].tobytes()) for s, n in zip(starts, lens)]
+
+
+def test_tensors_longer_than_the_pool_report_elayout(pkv):
+    """Eight tensors that each span a whole 1 MiB pool need eight times the leaves the work area
+    reserves: the call reports PKV_ELAYOUT and writes nothing past the work area."""
+    announce("tensor roots: 8 tensors spanning one 1 MiB pool (expect ELAYOUT, canary intact)")
+    pool = np.arange(1 << 20, dtype=np.uint32).astype(np.uint8)
+    status, _roots, intact = _roots_call(pkv, pool, [0] * 8, [1 << 20] * 8)
+    assert status == pkv.PKV_ELAYOUT
+    assert intact

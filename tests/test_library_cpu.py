@@ -141,3 +141,32 @@ def test_host_content_identity_matches_oracle():
         pkv.pkv_content_identity(recs + recs[:1], cfg)
     with pytest.raises(pkv.PkvError):
         pkv.pkv_content_identity(recs, cfg + cfg[:1])
+
+
+def _tree_nodes_per_level(lens):
+    """Per-level node totals of the content-identity trees of tensors of the given lengths: leaves
+    of 1024 bytes (one empty leaf for an empty tensor), parents of up to 16 children, every tensor
+    carried up to the height of the tallest one."""
+    counts = [max(1, -(-n // 1024)) for n in lens]
+    levels = [sum(counts)]
+    while max(counts) > 1:
+        counts = [-(-c // 16) for c in counts]
+        levels.append(sum(counts))
+    return levels
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_tree_work_area_holds_every_level(seed):
+    """pkv_tree_work_bytes covers the CSR arrays plus 32 bytes per node of every level for any
+    tensors whose lengths sum to at most the pool, overlapping or not (pure host arithmetic)."""
+    rng = np.random.default_rng(seed)
+    for _ in range(50):
+        n_bytes = int(rng.integers(1, 1 << 22)) * 4
+        n = int(rng.integers(1, 40))
+        cuts = np.sort(rng.integers(0, n_bytes + 1, size=n - 1))
+        lens = np.diff(np.concatenate([[0], cuts, [n_bytes]]))
+        lens = lens[rng.permutation(n)]
+        lens[rng.random(n) < 0.2] = 0                               # empty tensors: one leaf each
+        nodes = _tree_nodes_per_level(lens.tolist())
+        need = 8 * len(nodes) * (n + 1) + 32 * sum(nodes)
+        assert pkv.lib().pkv_tree_work_bytes(n_bytes, n) >= need
