@@ -38,10 +38,9 @@
  *     reserved for the insert protocol).
  *   - Device errors leave the index contents unspecified.
  *   - Index layout (pkv_table): one device buffer of pkv_table_bytes(capacity) bytes, 128-byte
- *     aligned, capacity a power of two in [4, 2^56].  Slots are indexed 0 .. capacity - 1; two more
- *     slot indices, capacity and capacity + 1, belong to the two reserved key byte patterns (all
- *     0xFF; all 0xFF with a last byte 0xFE), which keep their locations apart and do not count
- *     against the capacity.  A fixed-budget tier adds an epochs array of capacity + 2 uint32.
+ *     aligned, capacity a power of two in [4, 2^56].  Slots are indexed 0 .. capacity - 1, and an
+ *     index of capacity C holds at most C keys; every 128-bit value is an ordinary key.  A
+ *     fixed-budget tier adds an epochs array of capacity uint32.
  */
 #ifndef PKV_H
 #define PKV_H
@@ -81,9 +80,8 @@ typedef struct {
 /* The shared-tier index (section 2.1 shared KV-cache tier): open addressing over buckets of four
  * slots, one 128-byte bucket per HBM line.  Bucket b covers slots 4b .. 4b + 3 and holds, in order:
  * the four slots' claim words (the first 8 key bytes, or a free-slot marker), four flag words, and
- * four 16-byte pairs {key bytes 8..15, location}.  A 64-byte tail after the last bucket holds the
- * locations of the two reserved keys.  A key's home bucket is its first 8 bytes (little-endian)
- * modulo the bucket count; probing is linear over slots.
+ * four 16-byte pairs {key bytes 8..15, location}.  A key's home bucket is its first 8 bytes
+ * (little-endian) modulo the bucket count; probing is linear over slots.
  *   slots    : pkv_table_bytes(capacity) bytes of device memory, 128-byte aligned.
  *   capacity : a power of two in [4, 2^56].
  * The struct itself is host memory; the buffer is device memory owned by the caller. */
@@ -91,8 +89,8 @@ typedef struct {
     uint8_t* slots;
     uint64_t capacity;
 } pkv_table;
-/* Bytes of index memory for `capacity` slots (32 per slot plus the 64-byte tail), or 0 when the
- * capacity is not a power of two in [4, 2^56]. */
+/* Bytes of index memory for `capacity` slots (32 per slot), or 0 when the capacity is not a power
+ * of two in [4, 2^56]. */
 uint64_t pkv_table_bytes(uint64_t capacity);
 
 /* ---- host, pure, thread-safe ------------------------------------------------------------- */
@@ -150,10 +148,9 @@ int pkv_lookup_prefix(const pkv_table* table, const uint8_t* d_keys, const int64
  * d_locs: n_keys uint64 (< PKV_LOC_LIMIT, else PKV_ERESERVED).
  * d_n_new: one uint64 counter that the call increments by the number of new entries; the
  * caller zeroes it.  d_new_slots: NULL, or room for n_keys uint64: the slot index of each new
- * entry is appended at d_new_slots[old *d_n_new ...] (a reserved key's slot is `capacity` or
- * `capacity + 1`; bit 63 marks a slot that was removed by eviction before, bit 62 a key whose
- * first 8 bytes equal one of the index's marker values, stored with the substitute claim word).
- * No free slot for a new key sets PKV_EFULL. */
+ * entry is appended at d_new_slots[old *d_n_new ...] (bit 63 marks a slot that was removed by
+ * eviction before, bit 62 a key whose first 8 bytes equal one of the index's marker values,
+ * stored with the substitute claim word).  No free slot for a new key sets PKV_EFULL. */
 int pkv_store(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off,
               uint32_t n_req, uint64_t n_keys, const int32_t* d_hit_blocks, const uint64_t* d_locs,
               uint64_t* d_new_slots, uint64_t* d_n_new, int32_t* d_status, hipStream_t stream);
@@ -165,13 +162,13 @@ int pkv_table_rollback(const pkv_table* table, const uint64_t* d_new_slots, cons
                        uint64_t max_slots, hipStream_t stream);
 
 /* Copies every occupied (key, location) pair out, in no particular order.  d_keys_out: room for
- * capacity + 2 keys; d_locs_out: capacity + 2 words; *d_count receives the number of pairs (the
- * call zeroes it first). */
+ * capacity keys; d_locs_out: capacity words; *d_count receives the number of pairs (the call
+ * zeroes it first). */
 int pkv_table_export(const pkv_table* table, uint8_t* d_keys_out, uint64_t* d_locs_out,
                      uint64_t* d_count, hipStream_t stream);
 
 /* Fixed-budget shared tier (section 6.5, eviction under a fixed budget).  Every entry carries
- * the epoch of its last use in d_epochs (capacity + 2 uint32, owned by the caller; only entries
+ * the epoch of its last use in d_epochs (capacity uint32, owned by the caller; only entries
  * written through the touching calls have meaningful epochs).
  *
  * pkv_lookup_prefix_touch: pkv_lookup_prefix, and every hit key's epoch becomes `epoch`.

@@ -355,15 +355,6 @@ int orc_lookup_touch(orc_index* t, const uint8_t* keys, const int64_t* key_off, 
 
 #define ORC_LOC_LIMIT ((uint64_t)1 << 62)
 
-/* The two byte patterns an index reserves to mark free key slots: all 0xFF (empty) and all 0xFF
- * but a last byte of 0xFE (a removed entry).  Keys equal to either pattern have reserved places
- * of their own and do not count against the capacity. */
-static int reserved_key(const uint8_t key[16]) {
-    for (int i = 0; i < 15; ++i)
-        if (key[i] != 0xFF) return 0;
-    return key[15] == 0xFF || key[15] == 0xFE;
-}
-
 static int store_impl(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
                       const int32_t* hits, const uint64_t* locs, int touch, uint32_t epoch) {
     /* S = every (k_{r,j}, loc_{r,j}) with j >= h_r */
@@ -395,11 +386,8 @@ static int store_impl(orc_index* t, const uint8_t* keys, const int64_t* key_off,
         if (contains(t, s[i].key)) continue;
         s[n_new++] = s[i];                       /* compact the new keys in place, still sorted */
     }
-    /* Capacity counts ordinary keys (see reserved_key). */
-    uint64_t ordinary = 0;
-    for (uint64_t i = 0; i < t->size; ++i) ordinary += !reserved_key(t->e[i].key);
-    for (uint64_t i = 0; i < n_new; ++i) ordinary += !reserved_key(s[i].key);
-    if (ordinary > t->capacity) { free(s); return ORC_EFULL; }
+    /* an index of capacity C holds at most C keys */
+    if (t->size + n_new > t->capacity) { free(s); return ORC_EFULL; }
     /* a touching store refreshes the epoch of every candidate key already present */
     if (touch) {
         for (uint32_t r = 0; r < n_req; ++r) {

@@ -15,8 +15,8 @@
  *   lookup: h_r = largest h with k_{r,1..h} all in the index
  *   store:  every k_{r,j}, j > h_r, absent from the index is inserted once; among duplicates in
  *           one batch the smallest location wins; entries already present are never changed.
- *   capacity: an index of capacity C holds at most C keys other than the all-0xFF key, which has
- *           a reserved place of its own.
+ *   capacity: an index of capacity C holds at most C keys; a store whose new keys would exceed
+ *           that fails as a whole.
  *
  * Canonical order: the six core dimensions first, in the fixed registry order
  *   model_id, adapter_id, weight_dtype, weight_version, kv_format, salt,
@@ -84,8 +84,8 @@ int orc_lookup(const orc_index* t, const uint8_t* keys, const int64_t* key_off, 
                int32_t* hits);
 
 /* Inserts every key k_{r,j} with j >= hits[r] (0-based) that the index lacks.  On ORC_EFULL
- * or ORC_ERESERVED the index is left unchanged.  Capacity counts keys other than the two
- * reserved byte patterns (all 0xFF; all 0xFF with a last byte 0xFE). */
+ * or ORC_ERESERVED the index is left unchanged.  ORC_EFULL: the index would hold more keys than
+ * its capacity. */
 int orc_store(orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
               const int32_t* hits, const uint64_t* locs);
 

@@ -161,8 +161,8 @@ def pkv_derive_keys(tokens, tok_off, digests, block, key_off, keys, status, stre
 
 class Table:
     """Device memory of one index: ``slots`` uint8 [pkv_table_bytes(capacity)] (128-byte buckets of
-    four slots and a 64-byte tail, see include/pkv.h); with ``epochs=True`` also ``epochs`` int32
-    [capacity + 2] (the fixed-budget tier) and the eviction work area."""
+    four slots, see include/pkv.h); with ``epochs=True`` also ``epochs`` int32 [capacity] (the
+    fixed-budget tier) and the eviction work area."""
 
     def __init__(self, capacity: int, device="cuda", init=True, stream=None, epochs=False):
         import torch
@@ -174,7 +174,7 @@ class Table:
         self.slots = torch.empty(nbytes, dtype=torch.uint8, device=device)
         if self.slots.data_ptr() % 128:
             raise RuntimeError("index memory is not 128-byte aligned")
-        self.epochs = torch.zeros(capacity + 2, dtype=torch.int32, device=device) if epochs else None
+        self.epochs = torch.zeros(capacity, dtype=torch.int32, device=device) if epochs else None
         self.work = torch.empty(EVICT_WORK_BYTES // 8, dtype=torch.int64, device=device) if epochs else None
         if init:
             pkv_table_init(self, stream)

@@ -245,7 +245,7 @@ int pkv_derive_keys(const int32_t* d_tokens, uint64_t n_tokens, const int64_t* d
 
 uint64_t pkv_table_bytes(uint64_t capacity) {
     if (!pow2(capacity) || capacity < kSlotsPerBucket || capacity > (1ull << 56)) return 0;
-    return capacity * 32 + 64;
+    return capacity * 32;
 }
 
 int pkv_table_init(const pkv_table* table, hipStream_t stream) {

@@ -3,10 +3,9 @@
 //
 // Layout (pkv_internal.h): 128-byte buckets of 4 slots.  A bucket holds the four slots' claim words
 // (each the first 8 bytes of the slot's key, or a marker), their flag words, and for each slot one
-// 16-byte pair {key bytes 8..15, location word}; a 64-byte tail holds the location words of the
-// two reserved keys.  A key's home bucket is its first eight bytes masked to the bucket count;
-// probing is linear over slots, wrapping.  A fixed-budget tier adds epochs[capacity + 2] (uint32):
-// the epoch of each entry's last use.
+// 16-byte pair {key bytes 8..15, location word}.  A key's home bucket is its first eight bytes
+// masked to the bucket count; probing is linear over slots, wrapping.  A fixed-budget tier adds
+// epochs[capacity] (uint32): the epoch of each entry's last use.
 //
 // Lookup reads whole buckets: a key is present iff some slot on its probe path holds it, and absent
 // once the path meets a never-used slot (removed slots have their own claim marker, so paths run
@@ -82,12 +81,12 @@ __device__ __forceinline__ void store_pair_coherent(uint64_t* p, uint64_t hi, ui
 }
 
 // ---- init -------------------------------------------------------------------------------------
-// Claim words all ones, flag words zero, pairs {all ones, kEmpty}; the tail all ones.
+// Claim words all ones, flag words zero, pairs {all ones, kEmpty}.
 __global__ __launch_bounds__(256) void k_init(uint4* t, uint64_t capacity) {
-    const uint64_t n = capacity * 2 + 4;                 // 16-byte units: 8 per bucket, 4 in the tail
+    const uint64_t n = capacity * 2;                     // 16-byte units: 8 per bucket
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
-        const bool flags = i < capacity * 2 && ((i & 7) == 2 || (i & 7) == 3);
+        const bool flags = (i & 7) == 2 || (i & 7) == 3;
         t[i] = flags ? make_uint4(0u, 0u, 0u, 0u) : make_uint4(~0u, ~0u, ~0u, ~0u);
     }
 }
@@ -125,8 +124,6 @@ __device__ __forceinline__ void load_bucket(const uint4* __restrict__ t, uint64_
 __device__ __forceinline__ int64_t probe_key(const uint4* __restrict__ t, uint64_t capacity, uint64_t bmask,
                                              const uint4& key, uint64_t b, Bucket& bk) {
     const uint64_t* w = reinterpret_cast<const uint64_t*>(t);
-    const uint64_t rs = dev::reserved_slot(key, capacity);
-    if (rs) return w[capacity * 4 + (rs - capacity)] != kEmpty ? static_cast<int64_t>(rs) : -1;
     const KeyWords kw = key_words(key);
     const uint64_t n_buckets = bmask + 1;
     for (uint64_t it = 0; it < n_buckets; ++it) {
@@ -317,21 +314,7 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
     }
     bool claimed = false;
     uint64_t my_slot = 0;
-    const uint64_t rs = active ? dev::reserved_slot(key, t.capacity) : 0;
-    if (rs) {
-        // a reserved key lives in its own location word; there are no key bytes to publish
-        uint64_t* p = t.loc(rs);
-        for (uint32_t spin = 0; spin < kWaitLimit; ++spin) {
-            const uint64_t l = load_relaxed(p);
-            if (l == kEmpty) {
-                if (cas_relaxed(p, kEmpty, want)) { claimed = true; my_slot = rs; break; }
-                continue;
-            }
-            if (l & kFresh) min_relaxed(p, want);
-            break;
-        }
-        if (a.epochs) a.epochs[rs] = a.epoch;
-    } else if (active) {
+    if (active) {
         const KeyWords kw = key_words(key);
         const uint64_t slot_mask = t.capacity - 1;
         uint64_t s = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
@@ -419,7 +402,7 @@ __global__ __launch_bounds__(256) void k_store_finish_log(Tab t, const uint64_t*
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
         const uint64_t s = slots[i] & ~kLogFlags;
-        if (s > t.capacity + 1) continue;
+        if (s >= t.capacity) continue;
         uint64_t* p = t.loc(s);
         const uint64_t l = *p;
         if (l != kEmpty && (l & kFresh)) *p = l & ~kFresh;
@@ -435,19 +418,16 @@ __global__ __launch_bounds__(kStoreThreads) void k_store_finish_probe(StoreArgs 
     if (!candidate(a, wave_base, k, total)) return;
     const Tab& t = a.t;
     const uint4 key = a.keys[k];
-    uint64_t s = dev::reserved_slot(key, t.capacity);
-    if (!s) {
-        const KeyWords kw = key_words(key);
-        const uint64_t slot_mask = t.capacity - 1;
-        s = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
-        uint64_t probes = 0;
-        while (true) {
-            const uint64_t c = *t.lo(s);
-            if (c == kLoEmpty) return;                    // not stored (an error was reported)
-            if (c == kw.claim && t.pair(s)[0] == kw.hi && (kw.claim != kLoSub || *t.flag(s) == kw.flag)) break;
-            s = (s + 1) & slot_mask;
-            if (++probes >= t.capacity) return;
-        }
+    const KeyWords kw = key_words(key);
+    const uint64_t slot_mask = t.capacity - 1;
+    uint64_t s = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
+    uint64_t probes = 0;
+    while (true) {
+        const uint64_t c = *t.lo(s);
+        if (c == kLoEmpty) return;                        // not stored (an error was reported)
+        if (c == kw.claim && t.pair(s)[0] == kw.hi && (kw.claim != kLoSub || *t.flag(s) == kw.flag)) break;
+        s = (s + 1) & slot_mask;
+        if (++probes >= t.capacity) return;
     }
     uint64_t* p = t.loc(s);
     const uint64_t l = *p;
@@ -474,23 +454,15 @@ __global__ __launch_bounds__(256) void k_rollback(Tab t, const uint64_t* slots, 
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
         const uint64_t e = slots[i];
         const uint64_t s = e & ~kLogFlags;
-        if (s < t.capacity) {                        // the log says how the slot was found: no read
+        if (s < t.capacity)                          // the log says how the slot was found: no read
             clear_slot(t, s, (e & kFromRemoved) != 0, (e & kSubLogged) != 0);
-        } else if (s <= t.capacity + 1) {
-            *t.loc(s) = kEmpty;
-        }
     }
 }
 
 __global__ void k_zero_u64(uint64_t* p) { *p = 0; }
 
-// Occupied entry of slot s (< capacity + 2): its key and location, or false.
+// Occupied entry of slot s (< capacity): its key and location, or false.
 __device__ __forceinline__ bool slot_entry(const Tab& t, uint64_t s, uint4& key, uint64_t& loc) {
-    if (s >= t.capacity) {
-        loc = *t.loc(s);
-        key = make_uint4(~0u, ~0u, ~0u, s == t.capacity ? ~0u : kResvW);
-        return loc != kEmpty;
-    }
     uint64_t c = *t.lo(s);
     if (c == kLoEmpty || c == kLoRemoved) return false;
     const uint64_t* p = t.pair(s);
@@ -510,11 +482,11 @@ __global__ __launch_bounds__(256) void k_export(Tab t, uint4* out_keys, uint64_t
     const uint32_t lane = lane_id();
     const uint64_t waves = static_cast<uint64_t>(gridDim.x) * (blockDim.x / 64);
     const uint64_t wave = blockIdx.x * static_cast<uint64_t>(blockDim.x / 64) + (threadIdx.x >> 6);
-    for (uint64_t base = wave * 64; base <= t.capacity + 1; base += waves * 64) {
+    for (uint64_t base = wave * 64; base < t.capacity; base += waves * 64) {
         const uint64_t s = base + lane;
         uint4 key = make_uint4(0u, 0u, 0u, 0u);
         uint64_t l = 0;
-        const bool occ = s <= t.capacity + 1 && slot_entry(t, s, key, l);
+        const bool occ = s < t.capacity && slot_entry(t, s, key, l);
         const uint64_t mask = __ballot(occ);
         if (!mask) continue;
         const uint32_t leader = __builtin_ctzll(mask);
@@ -532,8 +504,7 @@ __global__ __launch_bounds__(256) void k_export(Tab t, uint4* out_keys, uint64_t
 
 // ---- eviction to a budget (quiescent index) ---------------------------------------------------
 // Generational: with E* the smallest epoch such that at most `budget` live entries were last used
-// at or after E*, every live entry used before E* is removed (its slot becomes a removed slot; a
-// reserved key's location word becomes empty).  E* is found by a radix select over the 32-bit
+// at or after E*, every live entry used before E* is removed (its slot becomes a removed slot).  E* is found by a radix select over the 32-bit
 // epochs in three digits (bits 21-31, 10-20, 0-9): per digit, a histogram pass over the index and
 // a one-workgroup scan.  Histograms are kept per workgroup in LDS and flushed with one global
 // atomic per non-empty bin, so entries that share an epoch do not contend on one address.  The
@@ -558,7 +529,6 @@ __device__ __forceinline__ EvictCtl* evict_ctl(uint32_t* work) {
 }
 
 __device__ __forceinline__ bool live_slot(const Tab& t, uint64_t s) {
-    if (s >= t.capacity) return *t.loc(s) != kEmpty;
     const uint64_t c = *t.lo(s);
     return c != kLoEmpty && c != kLoRemoved && t.pair(s)[1] != kEmpty;
 }
@@ -602,11 +572,11 @@ __global__ __launch_bounds__(kHistThreads) void k_evict_hist(Tab t, const uint32
     __syncthreads();
     const uint64_t waves = static_cast<uint64_t>(gridDim.x) * (blockDim.x / 64);
     const uint64_t wave = blockIdx.x * static_cast<uint64_t>(blockDim.x / 64) + (threadIdx.x >> 6);
-    for (uint64_t base = wave * 64; base < t.capacity + 2; base += waves * 64) {
+    for (uint64_t base = wave * 64; base < t.capacity; base += waves * 64) {
         const uint64_t s = base + lane_id();
         bool act = false;
         uint32_t bin = 0;
-        if (s < t.capacity + 2 && live_slot(t, s)) {
+        if (s < t.capacity && live_slot(t, s)) {
             const uint32_t e = epochs[s];
             const uint32_t high = d == 0 ? 0u : (e >> (shift + (d == 1 ? 11 : 10)));
             act = high == prefix;
@@ -680,11 +650,9 @@ __global__ __launch_bounds__(256) void k_evict_apply(Tab t, const uint32_t* epoc
     const uint64_t cut = evict_ctl(work)->cut;
     if (cut == 0) return;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
-    for (uint64_t s = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; s < t.capacity + 2;
-         s += stride) {
+    for (uint64_t s = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; s < t.capacity; s += stride) {
         if (!live_slot(t, s) || epochs[s] >= cut) continue;
-        if (s < t.capacity) free_slot(t, s, true);
-        else *t.loc(s) = kEmpty;
+        free_slot(t, s, true);
     }
 }
 
@@ -737,18 +705,18 @@ int launch_sum_hits(const int32_t* hits, uint32_t n_req, const int64_t* group_of
 int launch_evict(uint64_t* table, uint64_t capacity, const uint32_t* epochs, uint64_t budget, uint32_t* work,
                  uint64_t* n_evicted, hipStream_t s) {
     const Tab t{table, capacity};
-    const unsigned g = grid_for(capacity + 2, kHistThreads, kHistBlocks);
+    const unsigned g = grid_for(capacity, kHistThreads, kHistBlocks);
     hipLaunchKernelGGL(k_evict_clear, dim3(8), dim3(256), 0, s, work, n_evicted);
     for (int d = 0; d < 3; ++d) {
         hipLaunchKernelGGL(k_evict_hist, dim3(g), dim3(kHistThreads), 0, s, t, epochs, work, d);
         hipLaunchKernelGGL(k_evict_select, dim3(1), dim3(kSelectThreads), 0, s, work, budget, d, n_evicted);
     }
-    hipLaunchKernelGGL(k_evict_apply, dim3(grid_for(capacity + 2, 256, 16384)), dim3(256), 0, s, t, epochs, work);
+    hipLaunchKernelGGL(k_evict_apply, dim3(grid_for(capacity, 256, 16384)), dim3(256), 0, s, t, epochs, work);
     return check_launch("pkv_table_evict");
 }
 
 int launch_table_init(uint64_t* table, uint64_t capacity, hipStream_t s) {
-    hipLaunchKernelGGL(k_init, dim3(grid_for(capacity * 2 + 4, 256, 16384)), dim3(256), 0, s,
+    hipLaunchKernelGGL(k_init, dim3(grid_for(capacity * 2, 256, 16384)), dim3(256), 0, s,
                        reinterpret_cast<uint4*>(table), capacity);
     return check_launch("pkv_table_init");
 }
@@ -798,7 +766,7 @@ int launch_export(const uint64_t* table, uint64_t capacity, uint8_t* out_keys, u
     int rc = check_launch("pkv_table_export (zero)");
     if (rc) return rc;
     const Tab t{const_cast<uint64_t*>(table), capacity};
-    hipLaunchKernelGGL(k_export, dim3(grid_for(capacity + 2, 256, 8192)), dim3(256), 0, s, t,
+    hipLaunchKernelGGL(k_export, dim3(grid_for(capacity, 256, 8192)), dim3(256), 0, s, t,
                        reinterpret_cast<uint4*>(out_keys), out_locs, count);
     return check_launch("pkv_table_export");
 }

@@ -22,11 +22,10 @@ static constexpr uint32_t kRoundK[64] = {
 static constexpr uint32_t kInitH[8] = {0x6a09e667u, 0xbb67ae85u, 0x3c6ef372u, 0xa54ff53au,
                                       0x510e527fu, 0x9b05688cu, 0x1f83d9abu, 0x5be0cd19u};
 
-// Index layout.  The table is one array of 128-byte buckets of 4 slots, followed by a 64-byte tail:
+// Index layout.  The table is one array of 128-byte buckets of 4 slots:
 //   bucket word  0..3  claim word of slot j: the key's first 8 bytes (little-endian), or a marker;
 //   bucket word  4..7  flag word of slot j: which key prefix a substitute claim word stands for;
-//   bucket word  8..15 {key bytes 8..15, location word} of slot j, one 16-byte pair per slot;
-//   tail word    0, 1  location words of the two reserved keys (below).
+//   bucket word  8..15 {key bytes 8..15, location word} of slot j, one 16-byte pair per slot.
 // Claim word:
 //   kLoEmpty    -- never used; ends every probe path through it;
 //   kLoRemoved  -- removed by eviction: free for a new key, probe paths continue through it;
@@ -35,9 +34,8 @@ static constexpr uint32_t kInitH[8] = {0x6a09e667u, 0xbb67ae85u, 0x3c6ef372u, 0x
 //                  word says which (1: kLoEmpty, 2: kLoRemoved; 0 for every other key).
 // Location word: kEmpty until the claiming lane publishes the entry, then the location; bit 63
 // (kFresh) marks an entry inserted by the running store batch, whose location may still be
-// lowered to the batch minimum.  Valid caller locations are < 2^62.
-// Two key byte patterns (all 0xFF; all 0xFF with a last byte 0xFE) keep their location in the
-// tail words [capacity] and [capacity + 1] and do not count against the capacity.
+// lowered to the batch minimum.  Valid caller locations are < 2^62.  Every 128-bit value is an
+// ordinary key: the markers live only in claim words, never in key bytes.
 static constexpr uint64_t kLoEmpty = ~0ull;
 static constexpr uint64_t kLoRemoved = ~0ull - 1;
 static constexpr uint64_t kLoSub = ~0ull - 2;
@@ -46,11 +44,10 @@ static constexpr uint64_t kFresh = 1ull << 63;
 static constexpr uint64_t kFromRemoved = 1ull << 63;   // slot-log flag: the claimed slot was a removed entry
 static constexpr uint64_t kSubLogged = 1ull << 62;     // slot-log flag: the slot's claim word is the substitute
 static constexpr uint64_t kLogFlags = kFromRemoved | kSubLogged;
-static constexpr uint32_t kResvW = 0xFEFFFFFFu;     // last 32-bit word of the second reserved pattern
 static constexpr uint32_t kSlotsPerBucket = 4;
 static constexpr uint64_t kBucketWords = 16;        // 128 bytes
 
-// Word addresses of slot s (< capacity) and of the tail words.
+// Word addresses of slot s (< capacity).
 struct Tab {
     uint64_t* w;
     uint64_t capacity;
@@ -59,10 +56,7 @@ struct Tab {
     __device__ __forceinline__ uint64_t* pair(uint64_t s) const {
         return w + (s >> 2) * kBucketWords + 8 + 2 * (s & 3);
     }
-    // location word of a slot index, the two reserved keys included (capacity, capacity + 1)
-    __device__ __forceinline__ uint64_t* loc(uint64_t s) const {
-        return s < capacity ? pair(s) + 1 : w + capacity * (kBucketWords / kSlotsPerBucket) + (s - capacity);
-    }
+    __device__ __forceinline__ uint64_t* loc(uint64_t s) const { return pair(s) + 1; }
 };
 
 namespace dev {
@@ -120,12 +114,6 @@ __device__ __forceinline__ void report(int32_t* status, int32_t code) {
 
 __device__ __forceinline__ bool eq4(const uint4& a, const uint4& b) {
     return ((a.x ^ b.x) | (a.y ^ b.y) | (a.z ^ b.z) | (a.w ^ b.w)) == 0;
-}
-// Slot index of a reserved key (capacity for the all-0xFF pattern, capacity + 1 for the other),
-// or 0 for an ordinary key.
-__device__ __forceinline__ uint64_t reserved_slot(const uint4& a, uint64_t capacity) {
-    if ((a.x & a.y & a.z) != 0xFFFFFFFFu) return 0;
-    return a.w == 0xFFFFFFFFu ? capacity : (a.w == kResvW ? capacity + 1 : 0);
 }
 
 // Home bucket: the key is a SHA-256 output, so its first eight bytes are already uniform.

@@ -108,8 +108,8 @@ def export_sorted(table: Table):
     """(keys uint8 [n, 16], locs uint64 [n]) of every occupied slot, sorted by key bytes."""
     import torch
     cap = table.capacity
-    keys = torch.empty((cap + 2, 16), dtype=torch.uint8, device=table.slots.device)
-    locs = torch.empty(cap + 2, dtype=torch.int64, device=table.slots.device)
+    keys = torch.empty((cap, 16), dtype=torch.uint8, device=table.slots.device)
+    locs = torch.empty(cap, dtype=torch.int64, device=table.slots.device)
     count = torch.zeros(1, dtype=torch.int64, device=table.slots.device)
     pkv_table_export(table, keys, locs, count)
     n = int(count.item())

@@ -72,14 +72,15 @@ LO_SUB = np.uint64(0xFFFFFFFFFFFFFFFD)
 
 def raw_table(table):
     """The index decoded slot by slot (include/pkv.h layout) into (keys uint8 [capacity, 16], locs
-    uint64 [capacity + 2]): a never-used slot reads as the all-0xFF key with location EMPTY, a
-    removed slot as the removed pattern with location TOMB, a claimed but unpublished slot with
-    location PENDING; locs[capacity], locs[capacity + 1] are the reserved keys' words.  Also checks
-    the layout's own invariants (free slots hold no key bytes, flags or location; flag words appear
-    only with the substitute claim word)."""
+    uint64 [capacity]): a never-used slot reads as the all-0xFF key with location EMPTY, a removed
+    slot as TOMB_KEY with location TOMB, a claimed but unpublished slot with location PENDING (these
+    key values only stand in for free slots here; a live slot may hold any key).  Also checks the
+    layout's own invariants (free slots hold no key bytes, flags or location; flag words appear only
+    with the substitute claim word)."""
     cap = table.capacity
     w = table.slots.cpu().numpy().view(np.uint64)
-    b = w[: cap * 4].reshape(cap // 4, 16)
+    assert w.shape[0] == cap * 4, "index buffer is not 32 bytes per slot"
+    b = w.reshape(cap // 4, 16)
     claim = b[:, 0:4].reshape(-1)
     flag = b[:, 4:8].reshape(-1)
     hi = b[:, 8:16:2].reshape(-1)
@@ -91,38 +92,31 @@ def raw_table(table):
     assert (flag <= 2).all(), "unknown flag word"
     lo = np.where(flag == 1, LO_EMPTY, np.where(flag == 2, LO_REMOVED, claim))
     keys = np.concatenate([lo.view(np.uint8).reshape(-1, 8), hi.view(np.uint8).reshape(-1, 8)], axis=1)
-    locs = np.empty(cap + 2, np.uint64)
-    locs[:cap] = np.where(loc == EMPTY, PENDING, loc)
+    locs = np.where(loc == EMPTY, PENDING, loc)
     keys[claim == LO_EMPTY] = 0xFF
-    locs[:cap][claim == LO_EMPTY] = EMPTY
+    locs[claim == LO_EMPTY] = EMPTY
     keys[claim == LO_REMOVED] = TOMB_KEY
-    locs[:cap][claim == LO_REMOVED] = TOMB
-    locs[cap:] = w[cap * 4: cap * 4 + 2]
+    locs[claim == LO_REMOVED] = TOMB
     return keys, locs
-
-
 
 
 def check_structure(table):
     """Index invariants: every live slot is reachable from its home bucket with no empty slot in
     between (removed slots do not break paths); no claimed-but-unpublished or batch-marked slot
-    survives a store; empty slots hold the all-0xFF key and removed slots the removed pattern; no
-    reserved pattern occupies an ordinary live slot; no key is stored twice.  Returns the number of
-    entries (live slots plus occupied reserved-key words)."""
+    survives a store; empty slots hold no key bytes and removed slots the removed placeholder; no key
+    is stored twice.  Returns the number of entries (live slots)."""
     keys, locs = raw_table(table)
     cap = table.capacity
-    assert locs.shape[0] == cap + 2
-    main = locs[:cap]
-    occ = main != EMPTY                      # on some probe path: live or removed
-    tomb = main == TOMB
+    assert locs.shape[0] == cap
+    occ = locs != EMPTY                      # on some probe path: live or removed
+    tomb = locs == TOMB
     live = occ & ~tomb
-    assert not (main == PENDING).any(), "pending slot left behind"
-    assert not (main[live] & FRESH).any(), "fresh bit left behind"
+    assert not (locs == PENDING).any(), "pending slot left behind"
+    assert not (locs[live] & FRESH).any(), "fresh bit left behind"
     assert (keys[~occ] == 0xFF).all(), "empty slot with key bytes"
-    assert (keys[tomb] == TOMB_KEY[None, :]).all(), "removed slot without the removed pattern"
-    marker = (keys == 0xFF).all(axis=1) | (keys == TOMB_KEY[None, :]).all(axis=1)
-    assert not (live & marker).any(), "reserved pattern stored in an ordinary slot"
+    assert (keys[tomb] == TOMB_KEY[None, :]).all(), "removed slot without the removed placeholder"
     if live.any():
+        claim = table.slots.cpu().numpy().view(np.uint64).reshape(cap // 4, 16)[:, 0:4].reshape(-1)
         lo = keys[:, :8].copy().view("<u8").reshape(-1)
         home = (lo & np.uint64(cap // 4 - 1)).astype(np.int64) * 4
         idx = np.arange(cap, dtype=np.int64)
@@ -136,6 +130,8 @@ def check_structure(table):
             dist_home = (s - home[live]) % cap
             dist_empty = s - last[live]
             assert (dist_home < dist_empty).all(), "live slot not reachable from its home bucket"
-        lk = keys[live]
-        assert np.unique(lk.view("V16").reshape(-1)).shape[0] == lk.shape[0], "duplicate key stored"
-    return int(live.sum()) + int(locs[cap] != EMPTY) + int(locs[cap + 1] != EMPTY)
+        assert not ((claim == LO_EMPTY) | (claim == LO_REMOVED))[live].any(), "live slot with a free marker"
+        w = np.ascontiguousarray(keys[live]).view(">u8").reshape(-1, 2)
+        w = w[np.lexsort((w[:, 1], w[:, 0]))]
+        assert not ((w[1:] == w[:-1]).all(axis=1)).any(), "duplicate key stored"
+    return int(live.sum())

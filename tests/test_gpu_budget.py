@@ -23,20 +23,11 @@ def pkv():
 
 
 def raw_entries(table):
-    """(keys, locs, epochs) of every entry, sorted by key (live slots plus reserved-key words)."""
+    """(keys, locs, epochs) of every entry, sorted by key."""
     keys, locs = raw_table(table)
     ep = table.epochs.cpu().numpy().view(np.uint32)
-    cap = table.capacity
-    live = (locs[:cap] != EMPTY) & (locs[:cap] != TOMB)
-    k = [keys[:cap][live]]
-    l = [locs[:cap][live]]
-    e = [ep[:cap][live]]
-    pats = [np.full(16, 0xFF, np.uint8), np.array([0xFF] * 15 + [0xFE], np.uint8)]
-    for i in range(2):
-        if locs[cap + i] != EMPTY:
-            k.append(pats[i][None, :])
-            l.append(locs[cap + i:cap + i + 1])
-            e.append(ep[cap + i:cap + i + 1])
+    live = (locs != EMPTY) & (locs != TOMB)
+    k, l, e = [keys[live]], [locs[live]], [ep[live]]
     k, l, e = np.concatenate(k), np.concatenate(l), np.concatenate(e)
     if k.shape[0] == 0:
         return k.reshape(0, 16), l, e
@@ -111,7 +102,9 @@ def test_rollback_restores_removed_slots(pkv):
     check_structure(table)
 
 
-def test_reserved_patterns_and_wide_epochs(pkv):
+def test_marker_keys_and_wide_epochs(pkv):
+    """Keys whose bytes equal the slot markers (all 0xFF; all 0xFF ending in 0xFE; first halves equal
+    to the claim markers) are ordinary entries: stored, touched and evicted like any other."""
     import torch
     cap = 64
     table = pkv.Table(cap, epochs=True)

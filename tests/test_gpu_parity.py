@@ -235,8 +235,9 @@ def test_store_with_skewed_request_lengths(pkv, shape):
 def _marker_prefixed_pool(rng):
     """Keys whose first 8 bytes (the slot claim word, little-endian) equal the never-used marker
     (all 0xFF), the removed marker (0xFE then 0xFF) or the substitute claim word (0xFD then 0xFF),
-    with random and all-ones second halves; the two reserved patterns; ordinary keys.  The first
-    three prefixes all map to the last buckets, so they also contend and wrap around."""
+    with random and all-ones second halves; the all-0xFF key and the all-0xFF key ending in 0xFE
+    (whose second halves also equal a free slot's key bytes); ordinary keys.  The first three
+    prefixes all map to the last buckets, so they also contend and wrap around."""
     pool = []
     for first in (0xFF, 0xFE, 0xFD):
         for hi in range(6):
@@ -247,10 +248,10 @@ def _marker_prefixed_pool(rng):
             elif hi == 5:
                 k[8] = 0xFE                                 # one byte off all ones
             pool.append(k)
-    pool.append(np.full(16, 0xFF, np.uint8))                # reserved: all 0xFF
+    pool.append(np.full(16, 0xFF, np.uint8))                # all 0xFF
     tomb = np.full(16, 0xFF, np.uint8)
     tomb[15] = 0xFE
-    pool.append(tomb)                                       # reserved: the removed pattern
+    pool.append(tomb)                                       # all 0xFF but the last byte
     pool.extend(rng.integers(0, 256, size=(10, 16), dtype=np.uint8))
     return np.stack(pool)
 

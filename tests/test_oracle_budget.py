@@ -4,7 +4,7 @@ Generational eviction: with E* the smallest epoch such that at most `budget` pai
 at or after E*, every pair used before E* is removed.  Pins: hand-computed cases, the defining
 properties on random indexes (the survivors fit, they are exactly the pairs at or after E*, and
 E* is minimal: keeping one more generation would exceed the budget), the touch semantics of
-lookup and store, and the two reserved key patterns."""
+lookup and store, and the capacity an eviction frees."""
 
 import numpy as np
 import pytest
@@ -80,14 +80,19 @@ def test_touch_semantics():
     assert [ep[bytes(x)] for x in k] == [2, 2, 3, 3, 3, 3]
 
 
-def test_reserved_patterns_do_not_use_capacity():
-    e = np.full((1, 16), 0xFF, np.uint8)
-    t = e.copy()
-    t[0, 15] = 0xFE
-    idx = oracle.Index(1)
+def test_eviction_frees_capacity():
+    """Evicted entries stop counting against the capacity: a full index refuses a new key until an
+    eviction to a smaller budget removes the least recently used ones."""
+    rng = np.random.default_rng(81)
+    k = rng.integers(0, 256, size=(3, 16), dtype=np.uint8)
     one = np.array([0, 1], np.int64)
-    for k in (e, t, np.zeros((1, 16), np.uint8)):
-        assert idx.store(k, one, np.zeros(1, np.int32), np.zeros(1, np.uint64)) == 0
-    assert len(idx) == 3
-    assert idx.store(np.ones((1, 16), np.uint8), one, np.zeros(1, np.int32), np.zeros(1, np.uint64)) == oracle.EFULL
-    assert idx.evict(0) == 3 and len(idx) == 0
+    idx = oracle.Index(2)
+    for i in range(2):
+        assert idx.store_touch(k[i:i + 1], one, np.zeros(1, np.int32), np.zeros(1, np.uint64), i + 1) == 0
+    assert idx.store_touch(k[2:3], one, np.zeros(1, np.int32), np.zeros(1, np.uint64), 3) == oracle.EFULL
+    assert len(idx) == 2
+    assert idx.evict(1) == 1 and len(idx) == 1
+    assert idx.store_touch(k[2:3], one, np.zeros(1, np.int32), np.zeros(1, np.uint64), 3) == 0
+    kk, _ = idx.dump()
+    assert sorted(bytes(x) for x in kk) == sorted([bytes(k[1]), bytes(k[2])])
+    assert idx.evict(0) == 2 and len(idx) == 0

@@ -119,15 +119,32 @@ def test_reserved_locations_rejected():
                      np.array([(1 << 62) - 1], np.uint64)) == 0
 
 
-def test_the_all_ff_key_does_not_use_capacity():
-    rng = np.random.default_rng(6)
-    keys = rng.integers(0, 255, size=(9, 16), dtype=np.uint8)
-    keys[8] = 0xFF
-    off = np.array([0, 9], np.int64)
-    idx = oracle.Index(8)
-    assert idx.store(keys, off, np.zeros(1, np.int32), np.arange(9, dtype=np.uint64)) == 0
-    assert len(idx) == 9
-    assert (idx.lookup(keys, off) == 9).all()
+@pytest.mark.parametrize("seed", range(8))
+def test_efull_exactly_when_distinct_keys_exceed_capacity(seed):
+    """Store is all or nothing against the capacity: it fails with EFULL iff the index would hold more
+    distinct keys than its capacity (section 3.4 store; any 128-bit value is an ordinary key), and a
+    failed store leaves the index as it was.  Checked against a Python set over random batches whose
+    keys repeat within and across batches."""
+    rng = np.random.default_rng(700 + seed)
+    cap = int(rng.integers(1, 12))
+    pool = rng.integers(0, 256, size=(20, 16), dtype=np.uint8)
+    idx = oracle.Index(cap)
+    model = set()
+    for _ in range(12):
+        n = int(rng.integers(0, 6))
+        k = pool[rng.integers(0, pool.shape[0], size=n)]
+        off = np.array([0, n], np.int64)
+        want_full = len(model | {bytes(x) for x in k}) > cap
+        before = idx.dump()
+        rc = idx.store(k, off, np.zeros(1, np.int32), np.arange(n, dtype=np.uint64))
+        if want_full:
+            assert rc == oracle.EFULL
+            after = idx.dump()
+            assert (before[0] == after[0]).all() and (before[1] == after[1]).all()
+        else:
+            assert rc == 0
+            model |= {bytes(x) for x in k}
+        assert len(idx) == len(model) <= cap
 
 
 @pytest.mark.parametrize("seed", range(6))

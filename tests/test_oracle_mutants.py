@@ -51,14 +51,14 @@ MUTANTS = [
     ("largest location wins", [("return (x->loc > y->loc) - (x->loc < y->loc);",
                                 "return (x->loc < y->loc) - (x->loc > y->loc);")]),
     ("present keys inserted again", [("if (contains(t, s[i].key)) continue;", "")]),
-    ("capacity off by one", [("if (ordinary > t->capacity)", "if (ordinary >= t->capacity)")]),
+    ("capacity off by one", [("if (t->size + n_new > t->capacity)", "if (t->size + n_new >= t->capacity)")]),
+    ("capacity counts every candidate", [("if (t->size + n_new > t->capacity)", "if (t->size + ns > t->capacity)")]),
     ("hit lengths ignored by the store", [("hits[r] < 0 ? 0 : hits[r]", "0")]),
     ("eviction cut one generation late", [("uint64_t cut = (uint64_t)ep[budget] + 1;",
                                            "uint64_t cut = (uint64_t)ep[budget];")]),
     ("touching store leaves present keys", [("if (p >= 0) t->e[p].epoch = epoch;", "if (p >= 0) (void)0;")]),
     ("touching lookup skips the first hit", [("for (int64_t j = 0; j < hits[r]; ++j) t->e[find",
                                               "for (int64_t j = 1; j < hits[r]; ++j) t->e[find")]),
-    ("removed-entry pattern counted", [("return key[15] == 0xFF || key[15] == 0xFE;", "return key[15] == 0xFF;")]),
 ]
 
 
