@@ -115,6 +115,15 @@ int pkv_digest_batch(const uint8_t* d_bytes, uint64_t n_bytes, const int64_t* d_
                      const uint32_t* d_msg_len, uint32_t n_msg, uint8_t* d_digests,
                      int32_t* d_status, hipStream_t stream);
 
+/* Per-request digests from per-descriptor digests (section 5.2: one canonical encoder and one
+ * digest per descriptor, shared by every request that carries it): d_digests[r] =
+ * d_desc_digests[d_desc_idx[r]] for r < n_req.  A batch digests each distinct descriptor once with
+ * pkv_digest_batch and expands the results here.  d_desc_digests: n_desc x 16 bytes; d_desc_idx:
+ * n_req uint32; d_digests: n_req x 16 bytes; both digest arrays 16-byte aligned.  An index >= n_desc
+ * sets PKV_ELAYOUT in *d_status and zeroes that request's digest. */
+int pkv_expand_digests(const uint8_t* d_desc_digests, uint32_t n_desc, const uint32_t* d_desc_idx, uint32_t n_req,
+                       uint8_t* d_digests, int32_t* d_status, hipStream_t stream);
+
 /* d_key_off[r] = sum over q < r of floor((tok_off[q+1] - tok_off[q]) / block), r = 0..n_req
  * (section 4.4: only complete chunks are keyed).  d_tok_off and d_key_off: n_req + 1 int64.
  * block >= 1.  Offsets must be non-decreasing. */

@@ -17,7 +17,8 @@ PKV_LOC_LIMIT = 1 << 62
 ERROR_NAMES = {0: "PKV_OK", -1: "PKV_EINVAL", -2: "PKV_EDUPDIM", -3: "PKV_ERESERVED", -4: "PKV_EFULL",
                -5: "PKV_EHIP", -6: "PKV_ELAYOUT", -7: "PKV_ESTALL"}
 
-EXPORTED = ["pkv_descriptor_encode", "pkv_descriptor_digest", "pkv_digest_batch", "pkv_key_offsets",
+EXPORTED = ["pkv_descriptor_encode", "pkv_descriptor_digest", "pkv_digest_batch", "pkv_expand_digests",
+            "pkv_key_offsets",
             "pkv_derive_keys", "pkv_table_bytes", "pkv_table_init", "pkv_lookup_prefix", "pkv_store", "pkv_table_rollback",
             "pkv_table_export", "pkv_sum_hits", "pkv_lookup_prefix_touch", "pkv_store_touch",
             "pkv_table_evict", "pkv_tree_work_bytes", "pkv_tensor_roots", "pkv_content_identity",
@@ -57,6 +58,7 @@ def lib() -> ctypes.CDLL:
             "pkv_descriptor_digest": [P, ctypes.c_size_t, P],
             "pkv_digest_batch": [P, U64, P, P, U32, P, P, P],
             "pkv_key_offsets": [P, U32, U32, P, P],
+            "pkv_expand_digests": [P, U32, P, U32, P, P, P],
             "pkv_derive_keys": [P, U64, P, U32, P, U32, P, U64, P, P, P],
             "pkv_table_init": [P, P],
             "pkv_lookup_prefix": [P, P, P, U32, U64, P, P, P],
@@ -143,6 +145,14 @@ def pkv_digest_batch(pool, msg_off, msg_len, digests, status, stream=None):
     _check(lib().pkv_digest_batch(_ptr(pool, torch.uint8), pool.numel(), _ptr(msg_off, torch.int64),
                                   _ptr(msg_len, torch.int32), msg_off.numel(), _ptr(digests, torch.uint8),
                                   _ptr(status, torch.int32), _stream(stream)))
+
+
+def pkv_expand_digests(desc_digests, desc_idx, digests, status, stream=None):
+    """digests[r] = desc_digests[desc_idx[r]] (desc_idx: int32 tensor holding uint32 indices)."""
+    import torch
+    _check(lib().pkv_expand_digests(_ptr(desc_digests, torch.uint8), desc_digests.numel() // 16,
+                                    _ptr(desc_idx, torch.int32), desc_idx.numel(), _ptr(digests, torch.uint8),
+                                    _ptr(status, torch.int32), _stream(stream)))
 
 
 def pkv_key_offsets(tok_off, block, key_off, stream=None):

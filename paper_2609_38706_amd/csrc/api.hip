@@ -222,6 +222,16 @@ int pkv_digest_batch(const uint8_t* d_bytes, uint64_t n_bytes, const int64_t* d_
     return launch_digest_batch(d_bytes, n_bytes, d_msg_off, d_msg_len, n_msg, d_digests, d_status, stream);
 }
 
+int pkv_expand_digests(const uint8_t* d_desc_digests, uint32_t n_desc, const uint32_t* d_desc_idx, uint32_t n_req,
+                       uint8_t* d_digests, int32_t* d_status, hipStream_t stream) {
+    if (n_req == 0) return PKV_OK;
+    if ((!d_desc_digests && n_desc) || !d_desc_idx || !d_digests || !d_status)
+        return set_error(PKV_EINVAL, "pkv_expand_digests: null argument");
+    if (!aligned(d_desc_digests, 16) || !aligned(d_digests, 16))
+        return set_error(PKV_EINVAL, "pkv_expand_digests: digests must be 16-byte aligned");
+    return launch_expand_digests(d_desc_digests, n_desc, d_desc_idx, n_req, d_digests, d_status, stream);
+}
+
 int pkv_key_offsets(const int64_t* d_tok_off, uint32_t n_req, uint32_t block, int64_t* d_key_off,
                     hipStream_t stream) {
     if (!d_tok_off || !d_key_off) return set_error(PKV_EINVAL, "pkv_key_offsets: null argument");

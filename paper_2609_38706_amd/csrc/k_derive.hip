@@ -1193,6 +1193,20 @@ __global__ __launch_bounds__(64) void k_digest(const uint8_t* bytes, uint64_t n_
     reinterpret_cast<uint4*>(out)[i] = make_uint4(bswap(s[0]), bswap(s[1]), bswap(s[2]), bswap(s[3]));
 }
 
+// ---- per-request digests from per-descriptor digests: one lane per request -------------------
+__global__ __launch_bounds__(256) void k_expand_digests(const uint4* desc_digests, uint32_t n_desc, const uint32_t* idx,
+                                                        uint32_t n_req, uint4* out, int32_t* status) {
+    const uint32_t r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= n_req) return;
+    const uint32_t d = idx[r];
+    if (d >= n_desc) {
+        dev::report(status, PKV_ELAYOUT);
+        out[r] = make_uint4(0u, 0u, 0u, 0u);
+        return;
+    }
+    out[r] = desc_digests[d];
+}
+
 // ---- key offsets: floor(len / B) scanned over the requests ------------------------------------
 // One workgroup scans a chunk of kScanChunk requests.  A batch of one chunk is done in one launch;
 // a larger batch scans every chunk locally (the last entry of each chunk then holds the chunk's
@@ -1329,6 +1343,15 @@ int launch_digest_batch(const uint8_t* bytes, uint64_t n_bytes, const int64_t* o
     if (n == 0) return PKV_OK;
     hipLaunchKernelGGL(k_digest, dim3((n + 63) / 64), dim3(64), 0, s, bytes, n_bytes, off, len, n, out, status);
     return check_launch("pkv_digest_batch");
+}
+
+int launch_expand_digests(const uint8_t* desc_digests, uint32_t n_desc, const uint32_t* idx, uint32_t n_req,
+                          uint8_t* out, int32_t* status, hipStream_t s) {
+    if (n_req == 0) return PKV_OK;
+    hipLaunchKernelGGL(k_expand_digests, dim3((n_req + 255) / 256), dim3(256), 0, s,
+                       reinterpret_cast<const uint4*>(desc_digests), n_desc, idx, n_req, reinterpret_cast<uint4*>(out),
+                       status);
+    return check_launch("pkv_expand_digests");
 }
 
 int launch_key_offsets(const int64_t* tok_off, uint32_t n_req, uint32_t block, int64_t* key_off, hipStream_t s) {

@@ -126,6 +126,8 @@ __device__ __forceinline__ uint64_t home_bucket(const uint4& k, uint64_t bucket_
 // ---- launchers (defined next to their kernels; return a PKV_* code) ------------------------
 int launch_digest_batch(const uint8_t* bytes, uint64_t n_bytes, const int64_t* off, const uint32_t* len,
                         uint32_t n, uint8_t* out, int32_t* status, hipStream_t s);
+int launch_expand_digests(const uint8_t* desc_digests, uint32_t n_desc, const uint32_t* idx, uint32_t n_req,
+                          uint8_t* out, int32_t* status, hipStream_t s);
 int launch_key_offsets(const int64_t* tok_off, uint32_t n_req, uint32_t block, int64_t* key_off, hipStream_t s);
 int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_off, uint32_t n_req,
                   const uint8_t* digests, uint32_t block, const int64_t* key_off, uint64_t n_keys,

@@ -2,17 +2,19 @@
 
 ``DeviceBatch`` marshals one batch onto the GPU once:
   * tokens and request offsets;
-  * a pool of canonical descriptor encodings, with per-request offsets and lengths.
+  * a pool of the canonical encodings of the batch's distinct descriptors, with their offsets and
+    lengths, and each request's descriptor index.
 It also preallocates every output.  One step then launches only library kernels:
-  key offsets -> descriptor digests -> chained keys -> longest-prefix lookup -> store of misses.
+  key offsets -> descriptor digests (one per distinct descriptor, then expanded per request) ->
+  chained keys -> longest-prefix lookup -> store of misses.
 """
 
 from __future__ import annotations
 
 import numpy as np
 
-from . import (Table, pkv_derive_keys, pkv_descriptor_encode, pkv_digest_batch, pkv_key_offsets,
-               pkv_lookup_prefix, pkv_store, pkv_table_export, pkv_table_rollback)
+from . import (Table, pkv_derive_keys, pkv_descriptor_encode, pkv_digest_batch, pkv_expand_digests,
+               pkv_key_offsets, pkv_lookup_prefix, pkv_store, pkv_table_export, pkv_table_rollback)
 
 
 class DeviceBatch:
@@ -40,9 +42,14 @@ class DeviceBatch:
             offs[1:] = np.cumsum([len(e) for e in padded])[:-1]
         pool = np.frombuffer(b"".join(padded) or b"\0", dtype=np.uint8)
         didx = np.asarray(desc_idx, dtype=np.int64)
+        if didx.shape[0] != self.n_req or (self.n_req and (didx.min() < 0 or didx.max() >= len(encs))):
+            raise ValueError("desc_idx must hold one descriptor index per request")
+        self.n_desc = len(encs)
         self.pool = torch.from_numpy(pool.copy()).to(device)
-        self.msg_off = torch.from_numpy(offs[didx].copy()).to(device)
-        self.msg_len = torch.from_numpy(lens[didx].astype(np.int32)).to(device)
+        self.msg_off = torch.from_numpy(offs).to(device)
+        self.msg_len = torch.from_numpy(lens.astype(np.int32)).to(device)
+        self.desc_idx = torch.from_numpy(didx.astype(np.int32)).to(device)
+        self.desc_digests = torch.empty((max(1, self.n_desc), 16), dtype=torch.uint8, device=device)
         self.digests = torch.empty((max(1, self.n_req), 16), dtype=torch.uint8, device=device)
         self.key_off = torch.empty(self.n_req + 1, dtype=torch.int64, device=device)
         self.status = torch.zeros(1, dtype=torch.int32, device=device)
@@ -69,7 +76,10 @@ class DeviceBatch:
         pkv_key_offsets(self.tok_off, self.block, self.key_off, stream)
 
     def digest(self, stream=None):
-        pkv_digest_batch(self.pool, self.msg_off, self.msg_len, self.digests[: self.n_req], self.status, stream)
+        """One digest per distinct descriptor, then one per request."""
+        pkv_digest_batch(self.pool, self.msg_off, self.msg_len, self.desc_digests[: self.n_desc], self.status, stream)
+        pkv_expand_digests(self.desc_digests[: self.n_desc], self.desc_idx, self.digests[: self.n_req], self.status,
+                           stream)
 
     def derive(self, stream=None):
         pkv_derive_keys(self.tokens, self.tok_off, self.digests[: max(1, self.n_req)], self.block, self.key_off,

@@ -52,6 +52,30 @@ def test_digest_batch_matches_oracle(pkv):
     assert (got == oracle.batch_digests(b)).all()
 
 
+def test_expand_digests(pkv):
+    """Per-request digests gathered from per-descriptor ones, including an index past the table
+    (PKV_ELAYOUT, that request's digest zeroed) and an empty batch."""
+    import torch
+    rng = np.random.default_rng(2)
+    table = rng.integers(0, 256, size=(37, 16), dtype=np.uint8)
+    idx = rng.integers(0, 37, size=1000).astype(np.int32)
+    d_tab = torch.from_numpy(table).cuda()
+    out = torch.full((1000, 16), 7, dtype=torch.uint8, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pkv.pkv_expand_digests(d_tab, torch.from_numpy(idx).cuda(), out, status)
+    assert int(status.item()) == 0
+    assert (out.cpu().numpy() == table[idx]).all()
+    bad = idx.copy()
+    bad[500] = 37
+    pkv.pkv_expand_digests(d_tab, torch.from_numpy(bad).cuda(), out, status)
+    got = out.cpu().numpy()
+    assert int(status.item()) == pkv.PKV_ELAYOUT
+    assert (got[500] == 0).all() and (np.delete(got, 500, 0) == np.delete(table[idx], 500, 0)).all()
+    status.zero_()
+    pkv.pkv_expand_digests(d_tab, torch.zeros(0, dtype=torch.int32, device="cuda"), out[:0], status)
+    assert int(status.item()) == 0
+
+
 def test_digest_batch_unaligned_pool(pkv):
     """Messages at odd byte offsets, one ending on the pool's last byte, and empty messages."""
     import torch
