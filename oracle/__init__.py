@@ -56,6 +56,7 @@ def lib():
         L.orc_derive.argtypes = [P, P, ctypes.c_uint32, P, ctypes.c_uint32, P, ctypes.c_int]
         L.orc_index_new.argtypes = [ctypes.c_uint64]
         L.orc_index_new.restype = P
+        L.orc_index_set_threads.argtypes = [P, ctypes.c_int]
         L.orc_index_free.argtypes = [P]
         L.orc_index_clone.argtypes = [P]
         L.orc_index_clone.restype = P
@@ -161,9 +162,13 @@ def batch_digests(batch) -> np.ndarray:
 class Index:
     """The oracle's index: a sorted set of (key, location) pairs with a capacity."""
 
-    def __init__(self, capacity: int, _handle=None):
+    def __init__(self, capacity: int, _handle=None, threads: int = 1):
+        """``threads``: how many threads the store's sort and the lookup may use (results do not
+        depend on it)."""
         self.capacity = capacity
         self._h = _handle if _handle is not None else lib().orc_index_new(capacity)
+        if _handle is None:
+            lib().orc_index_set_threads(self._h, int(threads))
 
     def clone(self) -> "Index":
         h = lib().orc_index_clone(self._h)

@@ -276,7 +276,8 @@ int orc_derive(const int32_t* tokens, const int64_t* tok_off, uint32_t n_req,
 
 typedef struct { uint8_t key[16]; uint64_t loc; uint32_t epoch; } entry;
 
-struct orc_index { uint64_t capacity, size; entry* e; };
+/* threads: how many threads the store's sort and the lookup may use (1 by default). */
+struct orc_index { uint64_t capacity, size; entry* e; int threads; };
 
 static int entry_cmp(const void* a, const void* b) {
     const entry* x = (const entry*)a; const entry* y = (const entry*)b;
@@ -285,11 +286,60 @@ static int entry_cmp(const void* a, const void* b) {
     return (x->loc > y->loc) - (x->loc < y->loc);
 }
 
+/* Sorting by entry_cmp on several threads: the array is cut into equal slices, each slice is sorted
+ * with qsort on a thread of its own, and neighbouring sorted runs are then merged pairwise (the
+ * left run wins ties) until one run is left.  The order is the one a single qsort gives. */
+typedef struct { entry* e; uint64_t n; } sort_job;
+
+static void* sort_worker(void* arg) {
+    sort_job* j = (sort_job*)arg;
+    qsort(j->e, j->n, sizeof(entry), entry_cmp);
+    return NULL;
+}
+
+static int sort_entries(entry* e, uint64_t n, int threads) {
+    if (threads > 64) threads = 64;
+    if (threads <= 1 || n < ((uint64_t)1 << 16)) {
+        qsort(e, n, sizeof(entry), entry_cmp);
+        return ORC_OK;
+    }
+    uint64_t cut[65];
+    for (int i = 0; i <= threads; ++i) cut[i] = n * (uint64_t)i / (uint64_t)threads;
+    pthread_t tid[64];
+    int running[64];
+    sort_job job[64];
+    for (int i = 0; i < threads; ++i) {
+        job[i].e = e + cut[i];
+        job[i].n = cut[i + 1] - cut[i];
+        running[i] = pthread_create(&tid[i], NULL, sort_worker, &job[i]) == 0;
+        if (!running[i]) sort_worker(&job[i]);           /* no thread: this slice is sorted here */
+    }
+    for (int i = 0; i < threads; ++i)
+        if (running[i]) pthread_join(tid[i], NULL);
+    entry* tmp = (entry*)malloc(n * sizeof(entry));
+    if (!tmp) return ORC_EINVAL;
+    for (int width = 1; width < threads; width *= 2) {
+        for (int i = 0; i + width < threads; i += 2 * width) {
+            uint64_t lo = cut[i], mid = cut[i + width], hi = cut[i + 2 * width < threads ? i + 2 * width : threads];
+            uint64_t a = lo, b = mid, o = 0;
+            while (a < mid || b < hi) {
+                if (b == hi || (a < mid && entry_cmp(&e[a], &e[b]) <= 0)) tmp[o++] = e[a++];
+                else tmp[o++] = e[b++];
+            }
+            memcpy(e + lo, tmp, (hi - lo) * sizeof(entry));
+        }
+    }
+    free(tmp);
+    return ORC_OK;
+}
+
 orc_index* orc_index_new(uint64_t capacity) {
     orc_index* t = (orc_index*)calloc(1, sizeof(orc_index));
-    if (t) t->capacity = capacity;
+    if (t) { t->capacity = capacity; t->threads = 1; }
     return t;
 }
+
+void orc_index_set_threads(orc_index* t, int threads) { t->threads = threads < 1 ? 1 : threads; }
 
 void orc_index_free(orc_index* t) {
     if (t) { free(t->e); free(t); }
@@ -298,6 +348,7 @@ void orc_index_free(orc_index* t) {
 orc_index* orc_index_clone(const orc_index* t) {
     orc_index* c = orc_index_new(t->capacity);
     if (!c) return NULL;
+    c->threads = t->threads;
     if (t->size) {
         c->e = (entry*)malloc(t->size * sizeof(entry));
         if (!c->e) { free(c); return NULL; }
@@ -334,14 +385,46 @@ static int64_t find(const orc_index* t, const uint8_t key[16]) {
 
 static int contains(const orc_index* t, const uint8_t key[16]) { return find(t, key) >= 0; }
 
-int orc_lookup(const orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
-               int32_t* hits) {
-    for (uint32_t r = 0; r < n_req; ++r) {
+/* Longest present prefix of requests r0 .. r1 - 1. */
+static void lookup_range(const orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t r0, uint32_t r1,
+                         int32_t* hits) {
+    for (uint32_t r = r0; r < r1; ++r) {
         int64_t n = key_off[r + 1] - key_off[r];
         int64_t h = 0;
         while (h < n && contains(t, keys + 16 * (key_off[r] + h))) ++h;
         hits[r] = (int32_t)h;
     }
+}
+
+typedef struct {
+    const orc_index* t; const uint8_t* keys; const int64_t* key_off; uint32_t r0, r1; int32_t* hits;
+} lookup_job;
+
+static void* lookup_worker(void* arg) {
+    lookup_job* j = (lookup_job*)arg;
+    lookup_range(j->t, j->keys, j->key_off, j->r0, j->r1, j->hits);
+    return NULL;
+}
+
+/* The index is only read, so requests are split statically over the index's threads. */
+int orc_lookup(const orc_index* t, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
+               int32_t* hits) {
+    int threads = t->threads > 64 ? 64 : t->threads;
+    if (threads <= 1 || n_req < 2) {
+        lookup_range(t, keys, key_off, 0, n_req, hits);
+        return ORC_OK;
+    }
+    pthread_t tid[64];
+    int running[64];
+    lookup_job job[64];
+    for (int i = 0; i < threads; ++i) {
+        job[i] = (lookup_job){t, keys, key_off, (uint32_t)((uint64_t)n_req * i / threads),
+                              (uint32_t)((uint64_t)n_req * (i + 1) / threads), hits};
+        running[i] = pthread_create(&tid[i], NULL, lookup_worker, &job[i]) == 0;
+        if (!running[i]) lookup_worker(&job[i]);         /* no thread: this slice runs here */
+    }
+    for (int i = 0; i < threads; ++i)
+        if (running[i]) pthread_join(tid[i], NULL);
     return ORC_OK;
 }
 
@@ -379,7 +462,7 @@ static int store_impl(orc_index* t, const uint8_t* keys, const int64_t* key_off,
         }
     }
     /* sort by (key, loc): the first of each run of equal keys carries the smallest location */
-    qsort(s, ns, sizeof(entry), entry_cmp);
+    if (sort_entries(s, ns, t->threads) != ORC_OK) { free(s); return ORC_EINVAL; }
     uint64_t n_new = 0;
     for (uint64_t i = 0; i < ns; ++i) {
         if (i > 0 && memcmp(s[i].key, s[i - 1].key, 16) == 0) continue;

@@ -72,7 +72,10 @@ typedef struct orc_index orc_index;
 
 orc_index* orc_index_new(uint64_t capacity);
 void orc_index_free(orc_index* t);
-/* An independent copy of t (same capacity and pairs); NULL if out of memory. */
+/* Threads the index's store (its sort) and lookup may use; 1 by default.  Results do not depend
+ * on it. */
+void orc_index_set_threads(orc_index* t, int threads);
+/* An independent copy of t (same capacity, pairs and thread count); NULL if out of memory. */
 orc_index* orc_index_clone(const orc_index* t);
 uint64_t orc_index_size(const orc_index* t);
 /* Copies the pairs out in ascending key order (byte-wise unsigned comparison). */

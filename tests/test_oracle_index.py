@@ -179,3 +179,42 @@ def test_clone_is_an_independent_copy():
     assert len(c) == 10 and len(idx) == 6
     a2, b2 = idx.dump()
     assert (a0 == a2).all() and (b0 == b2).all()
+
+
+@pytest.mark.parametrize("threads", [3, 17])
+def test_threaded_store_and_lookup_match_brute_force(threads):
+    """The index's store sorts its candidates on several threads and its lookup splits requests over
+    threads: on batches large enough for the threaded sort (2^16 candidates and more), with
+    duplicates spread across the slices, the dump equals a Python dict model (smallest location per
+    new key, present keys untouched) and the hits equal a brute-force set scan, for every thread
+    count."""
+    rng = np.random.default_rng(900 + threads)
+    pool = rng.integers(0, 256, size=(60000, 16), dtype=np.uint8)
+    model = {}
+    idx = oracle.Index(1 << 20, threads=threads)
+    for rnd in range(3):
+        n_req = 700
+        lens = rng.integers(0, 200, size=n_req)
+        ko = np.zeros(n_req + 1, np.int64)
+        ko[1:] = np.cumsum(lens)
+        keys = pool[rng.integers(0, pool.shape[0], size=int(ko[-1]))]
+        locs = rng.permutation(1 << 24)[: keys.shape[0]].astype(np.uint64)
+        hits = idx.lookup(keys, ko)
+        want = []
+        for r in range(n_req):
+            h = 0
+            while h < lens[r] and bytes(keys[ko[r] + h]) in model:
+                h += 1
+            want.append(h)
+        assert hits.tolist() == want, rnd
+        new = {}
+        for r in range(n_req):
+            for j in range(int(hits[r]), int(lens[r])):
+                k = bytes(keys[ko[r] + j])
+                if k not in model:
+                    new[k] = min(new.get(k, 1 << 63), int(locs[ko[r] + j]))
+        assert idx.store(keys, ko, hits, locs) == 0
+        model.update(new)
+        gk, gl = idx.dump()
+        assert [bytes(x) for x in gk] == sorted(model)
+        assert gl.tolist() == [model[k] for k in sorted(model)]
