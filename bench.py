@@ -6,11 +6,12 @@ HBM: key offsets -> descriptor digests -> chained block keys -> longest-prefix l
 the misses (then the step's new entries are rolled back so that every step meets the same
 index).  Consecutive steps run on two streams: the derive of step k+1 overlaps the index work of
 step k, which stays in step order on its own stream.  A serial run of the same steps is reported
-beside it.  The default workload is 1024 requests x 2048 tokens, block 16, against a 4M-slot index
-at load 0.5.
+beside it.  The default workload is the largest configuration: 16384 requests x 4096 tokens, block
+16, 20 registered dimensions, probing a 2^26-slot index that holds 2^25 entries (load 0.5).
 
 Prints one JSON line: Gkeys/s (keys derived and probed per second), the derive kernel's share of
-the int32 VALU roofline, and the CPU oracle timed on the host cores.
+the int32 VALU roofline, the lookup's and the store's share of HBM bandwidth, and the CPU oracle
+timed on the host cores.
 """
 
 from __future__ import annotations
@@ -52,27 +53,35 @@ WORKLOAD_TEXT = {
 
 
 DERIVE_SOURCES = ["paper_2609_38706_amd/csrc/k_derive.hip", "paper_2609_38706_amd/csrc/pkv_internal.h"]
-LOOKUP_SOURCES = ["paper_2609_38706_amd/csrc/k_table.hip", "paper_2609_38706_amd/csrc/pkv_internal.h"]
+TABLE_SOURCES = ["paper_2609_38706_amd/csrc/k_table.hip", "paper_2609_38706_amd/csrc/pkv_internal.h"]
 HBM_PEAK = 8.0e12             # MI355X HBM3E, bytes/s
 EVENT_STRIDE = 10             # derive launches of the timed region between two timed ones
 BYTES_PER_PROBE = 80          # the key bytes of one 4-slot bucket (64) + the 16-byte probe key
+# One insert of the store path: the 64 key bytes of the home bucket read, an 8-byte compare-and-swap,
+# the 16-byte key and 8-byte location written, and the 24 input bytes (key + location) read.
+BYTES_PER_INSERT = 120
 
 
-def measured_traffic(workload: str, kernel: str = "derive"):
-    """HBM bytes per launch of the derive (or lookup) kernel from the committed rocprofv3
-    FETCH_SIZE/WRITE_SIZE summary, or None when there is none for this workload or the kernel's
-    source has changed since it was taken."""
+def traffic_record(workload: str, kernel: str = "derive"):
+    """The committed rocprofv3 FETCH_SIZE/WRITE_SIZE record of a kernel (derive, lookup or store) on
+    a workload, or None when there is none or the kernel's source has changed since it was taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"{kernel}_traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
     h = hashlib.sha256()
-    for f in (DERIVE_SOURCES if kernel == "derive" else LOOKUP_SOURCES):
+    for f in (DERIVE_SOURCES if kernel == "derive" else TABLE_SOURCES):
         h.update(open(os.path.join(ROOT, f), "rb").read())
     if rec.get("source_sha256") != h.hexdigest():
         return None
-    return int(round(rec["bytes_per_launch"]))
+    return rec
+
+
+def measured_traffic(workload: str, kernel: str = "derive"):
+    """HBM bytes per launch from traffic_record, or None."""
+    rec = traffic_record(workload, kernel)
+    return None if rec is None else int(round(rec["bytes_per_launch"]))
 
 
 def compressions_per_key(block: int) -> int:
@@ -107,11 +116,12 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=3)
-    p.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_TEXT))
+    p.add_argument("--workload", default="c4", choices=sorted(WORKLOAD_TEXT))
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--classes", type=int, default=8, help="provenance classes of the budget workload")
     p.add_argument("--no-saturation", action="store_true", help="skip the derive-at-full-occupancy diagnostic")
-    p.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (0 = host cores, at most 16)")
+    p.add_argument("--cpu-threads", type=int, default=0,
+                   help="oracle threads (0 = the CPUs this process may run on, at most the 16 a one-GPU share has)")
     p.add_argument("--calib-copy", action="store_true", help="run only a plain 1 GiB device copy (counter calibration)")
     p.add_argument("--cold-reps", type=int, default=20,
                    help="reps of the cold-cache per-kernel measurement after the timed region (0 = skip)")
@@ -481,7 +491,7 @@ def budget_cpu_leg(args, g, target_s=10.0):
     empty index, until about `target_s` seconds; rate in keys per second."""
     import oracle
     from workloads import locations
-    threads = args.cpu_threads or max(1, min(16, len(os.sched_getaffinity(0))))
+    threads, _host = cpu_threads(args)
     batches = g["batches"]
     idx = oracle.Index(g["capacity"])
     total, keys_done, i = 0.0, 0, 0
@@ -505,7 +515,7 @@ def budget_cpu_leg(args, g, target_s=10.0):
 def omission_cpu_leg(args, case, n_keys, target_s=10.0):
     """The oracle's omission matrix on the same case, repeated until about `target_s` seconds."""
     from oracle.omission import omission_matrix
-    threads = args.cpu_threads or max(1, min(16, len(os.sched_getaffinity(0))))
+    threads, _host = cpu_threads(args)
     total, reps = 0.0, 0
     while total < target_s:
         t0 = time.perf_counter()
@@ -521,11 +531,13 @@ def omission_cpu_leg(args, case, n_keys, target_s=10.0):
 
 def cpu_leg(args, w, target_s=10.0, max_reps=2000):
     """The oracle as it stands, on the host cores: full steps of the same workload, each on a fresh
-    copy of the prepared index, repeated until about `target_s` seconds of timed CPU work."""
+    copy of the prepared index, repeated until about `target_s` seconds of timed CPU work.  Derive,
+    lookup (read-only) and the store's sort run on the same threads; the store's merge and the
+    descriptor digests on one."""
     import oracle
     from workloads import locations
-    threads = args.cpu_threads or max(1, min(16, len(os.sched_getaffinity(0))))
-    idx = oracle.Index(w.capacity)
+    threads, host = cpu_threads(args)
+    idx = oracle.Index(w.capacity, threads=threads)
     for pre in (w.fill, w.warmup):
         if pre is None:
             continue
@@ -533,6 +545,7 @@ def cpu_leg(args, w, target_s=10.0, max_reps=2000):
         keys = oracle.derive(pre.tokens, pre.tok_off, oracle.batch_digests(pre), pre.block, threads)
         hits = idx.lookup(keys, ko) if pre is w.warmup else np.zeros(pre.n_req, np.int32)
         assert idx.store(keys, ko, hits, locations(ko, pre.tag)) == 0
+        del keys
     b = w.batch
     locs = locations(oracle.key_offsets(b.tok_off, b.block), b.tag)
     total_s, total_keys, reps = 0.0, 0, 0
@@ -568,12 +581,23 @@ def cpu_leg(args, w, target_s=10.0, max_reps=2000):
     one_s = time.perf_counter() - t0
     return {"value": round(total_keys / total_s / 1e9, 6), "unit": "Gkeys/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} full steps of the same workload ({b.n_req} requests, {n_keys} keys each), each on a "
-                      f"fresh copy of the prepared index: digests, derive on {threads} threads, lookup and store "
-                      f"single-threaded; {total_s:.2f} s timed",
+                      f"fresh copy of the prepared index: digests, derive on {threads} threads, lookup on {threads} "
+                      f"threads (read-only), store with its sort on {threads} threads; {total_s:.2f} s timed",
+            "threads": threads, "host_cpus": host, "cpu_share": CPU_SHARE,
             "seconds": round(total_s, 3), "steps": reps, "cpu_model": cpu_model(),
             "phase_ms_per_step": {k: round(v / reps * 1e3, 3) for k, v in phase.items()},
             "derive_one_thread": {"requests": n_sub, "keys": int(ko[n_sub]), "seconds": round(one_s, 6),
                                   "gkeys_per_s": round(int(ko[n_sub]) / one_s / 1e9, 6)}}
+
+
+# The host CPUs one GPU's share of the box comes with; the oracle uses no more threads than that.
+CPU_SHARE = 16
+
+
+def cpu_threads(args):
+    """(threads the oracle uses, CPUs this process may run on)."""
+    host = len(os.sched_getaffinity(0))
+    return (args.cpu_threads or max(1, min(CPU_SHARE, host))), host
 
 
 def cpu_model() -> str:
@@ -694,6 +718,14 @@ def main():
                        "frac": round(lookup_bps / HBM_PEAK, 5), "traffic": measured_traffic(args.workload, "lookup"),
                        "kernel": "lookup (serial pass, events)", "probes": g["probes"],
                        "bytes_per_probe": BYTES_PER_PROBE}
+    store_bps = g["new_entries"] * BYTES_PER_INSERT / (ser["store_ms"] * 1e-3)
+    srec = traffic_record(args.workload, "store")
+    roofline_store = {"bound": "hbm", "achieved": round(store_bps / 1e9, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                      "frac": round(store_bps / HBM_PEAK, 5),
+                      "traffic": None if srec is None else int(round(srec["bytes_per_launch"])),
+                      "kernel": "store (k_store + fresh-bit finish; serial pass, events)",
+                      "inserts": g["new_entries"], "bytes_per_insert": BYTES_PER_INSERT,
+                      "atomics_per_insert": None if srec is None else srec.get("atomics_per_insert")}
     rates = {"derive_gkeys_per_s": round(g["n_keys"] / (g["derive_ms"] * 1e-3) / 1e9, 4),
              "lookup_gprobes_per_s": round(g["probes"] / (ser["lookup_ms"] * 1e-3) / 1e9, 4),
              "store_ginserts_per_s": round(g["new_entries"] / (ser["store_ms"] * 1e-3) / 1e9, 4)}
@@ -730,6 +762,7 @@ def main():
                      "hit_blocks": g["hit_blocks"], "new_entries": g["new_entries"]},
         "roofline": roofline,
         "roofline_lookup": roofline_lookup,
+        "roofline_store": roofline_store,
         "rates": rates,
         "cpu_baseline": cpu,
         "derive_fill": fill,

@@ -128,11 +128,24 @@ def export_sorted(table: Table):
     return sort_pairs(k, v)
 
 
+def key_order(keys: np.ndarray) -> np.ndarray:
+    """Permutation that sorts 16-byte keys by their bytes (unsigned, most significant first): an
+    argsort by the first 8 bytes, then runs that share them ordered by the last 8 bytes too."""
+    words = np.ascontiguousarray(keys).view(">u8").reshape(-1, 2)
+    order = np.argsort(words[:, 0])
+    first = words[order, 0]
+    tie = np.flatnonzero(first[1:] == first[:-1])
+    if tie.size:
+        pos = np.unique(np.concatenate([tie, tie + 1]))      # every position inside such a run
+        sub = order[pos]
+        order[pos] = sub[np.lexsort((words[sub, 1], words[sub, 0]))]
+    return order
+
+
 def sort_pairs(keys: np.ndarray, locs: np.ndarray):
     if keys.shape[0] == 0:
         return keys.reshape(0, 16), locs
-    words = np.ascontiguousarray(keys).view(">u8").reshape(-1, 2)
-    order = np.lexsort((words[:, 1], words[:, 0]))
+    order = key_order(keys)
     return keys[order], locs[order]
 
 

@@ -132,6 +132,11 @@ def check_structure(table):
             assert (dist_home < dist_empty).all(), "live slot not reachable from its home bucket"
         assert not ((claim == LO_EMPTY) | (claim == LO_REMOVED))[live].any(), "live slot with a free marker"
         w = np.ascontiguousarray(keys[live]).view(">u8").reshape(-1, 2)
-        w = w[np.lexsort((w[:, 1], w[:, 0]))]
-        assert not ((w[1:] == w[:-1]).all(axis=1)).any(), "duplicate key stored"
+        order = np.argsort(w[:, 0])
+        first = w[order, 0]
+        tie = np.flatnonzero(first[1:] == first[:-1])      # equal keys share their first 8 bytes
+        if tie.size:
+            sub = w[order[np.unique(np.concatenate([tie, tie + 1]))]]
+            sub = sub[np.lexsort((sub[:, 1], sub[:, 0]))]
+            assert not ((sub[1:] == sub[:-1]).all(axis=1)).any(), "duplicate key stored"
     return int(live.sum())

@@ -37,3 +37,24 @@ def test_more_than_one_gpu_exits_with_a_message():
                        text=True, timeout=300, cwd=ROOT)
     assert r.returncode != 0
     assert "one GPU" in (r.stdout + r.stderr)
+
+
+def test_default_workload_is_the_largest_configuration():
+    # 16384 requests x 4096 tokens against the 2^26-slot index is the largest specified shape
+    import argparse
+    old = sys.argv
+    try:
+        sys.argv = ["bench.py"]
+        args = bench.parse()
+    finally:
+        sys.argv = old
+    assert args.workload == "c4" and args.gpus == 1
+
+
+def test_cpu_threads_stay_within_the_one_gpu_share():
+    class A:
+        cpu_threads = 0
+    t, host = bench.cpu_threads(A())
+    assert 1 <= t <= bench.CPU_SHARE and t <= host == len(os.sched_getaffinity(0))
+    A.cpu_threads = 3
+    assert bench.cpu_threads(A())[0] == 3

@@ -170,3 +170,20 @@ def test_tree_work_area_holds_every_level(seed):
         nodes = _tree_nodes_per_level(lens.tolist())
         need = 8 * len(nodes) * (n + 1) + 32 * sum(nodes)
         assert pkv.lib().pkv_tree_work_bytes(n_bytes, n) >= need
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_sort_pairs_orders_keys_bytewise(seed):
+    """The host-side sort of exported (key, location) pairs orders keys by their bytes, also when many
+    keys share their first 8 bytes (the sort's tie-breaking path)."""
+    from paper_2609_38706_amd.pipeline import sort_pairs
+    rng = np.random.default_rng(seed)
+    for _ in range(100):
+        n = int(rng.integers(1, 300))
+        k = rng.integers(0, 3, size=(n, 16), dtype=np.uint8)
+        k[:, : int(rng.integers(0, 9))] = 0xFF
+        loc = np.arange(n, dtype=np.uint64)
+        sk, sl = sort_pairs(k, loc)
+        ref = sorted(range(n), key=lambda i: bytes(k[i]))
+        assert [bytes(x) for x in sk] == [bytes(k[i]) for i in ref]
+        assert [bytes(k[i]) for i in sl.tolist()] == [bytes(x) for x in sk]
