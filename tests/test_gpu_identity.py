@@ -35,7 +35,7 @@ def test_roots_at_every_edge(pkv):
         starts.append(pos)
         pos += (len(d) + 3) // 4 * 4
     # room at the end for the shared tensor below: the lengths may add up to the pool size at most
-    pool = np.zeros(pos + 64 + len(datas[9]), np.uint8)
+    pool = np.zeros(pos + 64 + (len(datas[9]) + 3) // 4 * 4, np.uint8)
     for st, d in zip(starts, datas):
         pool[st:st + len(d)] = np.frombuffer(d, np.uint8)
     # one more tensor sharing the bytes of tensor 9
