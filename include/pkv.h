@@ -249,6 +249,21 @@ int pkv_tensor_roots(const uint8_t* d_data, uint64_t n_bytes, const int64_t* d_t
 int pkv_content_identity(const pkv_tensor* tensors, uint32_t n_tensors, const pkv_field* config, size_t n_config,
                          uint8_t out[32]);
 
+/* pkv_tensor_roots for callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same roots, with the work area taken
+ * from a buffer of PKV_STATIC_TREE_WORK_BYTES that the library holds on each device it runs on
+ * until the process ends, so the caller passes only inputs and outputs.  The call allocates
+ * nothing (no hipMalloc, no hipFree).  Inputs whose work area, pkv_tree_work_bytes(n_bytes,
+ * n_tensors), exceeds PKV_STATIC_TREE_WORK_BYTES (about 250 MB of tensor bytes) are refused with
+ * PKV_EINVAL before anything is launched.  Every call on one device uses that device's one buffer:
+ * calls that overlap on one device (concurrent streams, or threads) race and give unspecified
+ * roots; calls ordered on one stream do not.  The first call on a device looks the buffer's address
+ * up there (and may return PKV_EHIP if that fails). */
+#define PKV_STATIC_TREE_WORK_BYTES (8u << 20)
+int pkv_tensor_roots_static(const uint8_t* d_data, uint64_t n_bytes, const int64_t* d_tensor_off,
+                            const int64_t* d_tensor_len, uint32_t n_tensors, uint8_t* d_roots, int32_t* d_status,
+                            hipStream_t stream);
+
 /* Text describing the last non-OK return on this thread. */
 const char* pkv_last_error(void);
 

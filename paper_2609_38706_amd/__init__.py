@@ -21,10 +21,12 @@ EXPORTED = ["pkv_descriptor_encode", "pkv_descriptor_digest", "pkv_digest_batch"
             "pkv_key_offsets",
             "pkv_derive_keys", "pkv_table_bytes", "pkv_table_init", "pkv_lookup_prefix", "pkv_store", "pkv_table_rollback",
             "pkv_table_export", "pkv_sum_hits", "pkv_lookup_prefix_touch", "pkv_store_touch",
-            "pkv_table_evict", "pkv_tree_work_bytes", "pkv_tensor_roots", "pkv_content_identity",
+            "pkv_table_evict", "pkv_tree_work_bytes", "pkv_tensor_roots", "pkv_tensor_roots_static",
+            "pkv_content_identity",
             "pkv_last_error", "pkv_version"]
 
 EVICT_WORK_BYTES = 3 * 2048 * 4 + 64   # PKV_EVICT_WORK_BYTES
+STATIC_TREE_WORK_BYTES = 8 << 20      # PKV_STATIC_TREE_WORK_BYTES
 
 
 class PkvError(RuntimeError):
@@ -70,6 +72,7 @@ def lib() -> ctypes.CDLL:
             "pkv_store_touch": [P, P, P, U32, U64, P, P, P, P, P, U32, P, P],
             "pkv_table_evict": [P, P, U64, P, P, P],
             "pkv_tensor_roots": [P, U64, P, P, U32, P, U64, P, P, P],
+            "pkv_tensor_roots_static": [P, U64, P, P, U32, P, P, P],
             "pkv_content_identity": [P, U32, P, ctypes.c_size_t, P],
         }
         for name, args in sig.items():
@@ -276,6 +279,14 @@ def pkv_tensor_roots(data, tensor_off, tensor_len, work, roots, status, stream=N
                                   _ptr(tensor_len, torch.int64), tensor_off.numel(), _ptr(work),
                                   work.numel() * work.element_size(), _ptr(roots, torch.uint8),
                                   _ptr(status, torch.int32), _stream(stream)))
+
+
+def pkv_tensor_roots_static(data, tensor_off, tensor_len, roots, status, stream=None):
+    """pkv_tensor_roots without a work area argument: the library's per-device buffer is used."""
+    import torch
+    _check(lib().pkv_tensor_roots_static(_ptr(data, torch.uint8), data.numel(), _ptr(tensor_off, torch.int64),
+                                         _ptr(tensor_len, torch.int64), tensor_off.numel(), _ptr(roots, torch.uint8),
+                                         _ptr(status, torch.int32), _stream(stream)))
 
 
 def pkv_content_identity(tensors, config=()) -> bytes:

@@ -371,6 +371,28 @@ int pkv_tensor_roots(const uint8_t* d_data, uint64_t n_bytes, const int64_t* d_t
                                d_roots, d_status, stream);
 }
 
+int pkv_tensor_roots_static(const uint8_t* d_data, uint64_t n_bytes, const int64_t* d_tensor_off,
+                            const int64_t* d_tensor_len, uint32_t n_tensors, uint8_t* d_roots, int32_t* d_status,
+                            hipStream_t stream) {
+    if (n_tensors == 0) return PKV_OK;
+    if ((!d_data && n_bytes) || !d_tensor_off || !d_tensor_len || !d_roots || !d_status)
+        return set_error(PKV_EINVAL, "pkv_tensor_roots_static: null argument");
+    if (n_bytes % 4 != 0 || !aligned(d_data, 4))
+        return set_error(PKV_EINVAL, "pkv_tensor_roots_static: data must be 4-byte aligned and a multiple of 4 bytes long");
+    if (!aligned(d_roots, 16)) return set_error(PKV_EINVAL, "pkv_tensor_roots_static: roots must be 16-byte aligned");
+    const uint64_t need = tree_layout(n_bytes, n_tensors).bytes;
+    if (need > PKV_STATIC_TREE_WORK_BYTES)
+        return set_error(PKV_EINVAL,
+                         "pkv_tensor_roots_static: %llu bytes of data in %u tensors need a %llu-byte work area, more "
+                         "than the %llu bytes this entry point holds; use pkv_tensor_roots",
+                         static_cast<unsigned long long>(n_bytes), n_tensors, static_cast<unsigned long long>(need),
+                         static_cast<unsigned long long>(PKV_STATIC_TREE_WORK_BYTES));
+    uint8_t* work = nullptr;
+    const int rc = static_tree_work(&work);
+    if (rc) return rc;
+    return launch_tensor_roots(d_data, n_bytes, d_tensor_off, d_tensor_len, n_tensors, work, d_roots, d_status, stream);
+}
+
 int pkv_content_identity(const pkv_tensor* tensors, uint32_t n, const pkv_field* config, size_t n_config,
                          uint8_t out[32]) {
     if ((!tensors && n) || (!config && n_config) || !out) return set_error(PKV_EINVAL, "pkv_content_identity: null argument");

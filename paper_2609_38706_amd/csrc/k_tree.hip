@@ -14,7 +14,14 @@
 // the next block while the current one compresses; other leaves take the byte-exact path.
 //
 // Work area (see tree_layout): the CSR of every level, then the digests of every level.
+#include <mutex>
+
 #include "pkv_internal.h"
+
+// Work area of pkv_tensor_roots_static: one copy per device, held until the process ends.  Host code
+// never passes this name to a kernel: it stands for a host-side shadow, not the device address;
+// static_tree_work() resolves the address per device.
+static __device__ __align__(256) uint8_t scratch[PKV_STATIC_TREE_WORK_BYTES];
 
 namespace pkv {
 namespace {
@@ -315,6 +322,27 @@ TreeLayout tree_layout(uint64_t n_bytes, uint32_t n) {
     }
     L.bytes = off;
     return L;
+}
+
+// Device address of `scratch` on the current device, looked up once per device (with that device
+// current) and kept.
+int static_tree_work(uint8_t** out) {
+    static std::mutex mu;
+    static void* addr[64] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return set_error(PKV_EHIP, "pkv_tensor_roots_static: hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= 64) return set_error(PKV_EINVAL, "pkv_tensor_roots_static: device %d out of range", dev);
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return set_error(PKV_EHIP, "pkv_tensor_roots_static: hipGetSymbolAddress: %s", hipGetErrorString(e));
+        addr[dev] = p;
+    }
+    *out = static_cast<uint8_t*>(addr[dev]);
+    return PKV_OK;
 }
 
 int launch_tensor_roots(const uint8_t* data, uint64_t n_bytes, const int64_t* tensor_off, const int64_t* tensor_len,

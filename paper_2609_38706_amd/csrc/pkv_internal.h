@@ -155,6 +155,7 @@ struct TreeLayout {
 TreeLayout tree_layout(uint64_t n_bytes, uint32_t n_tensors);
 int launch_tensor_roots(const uint8_t* data, uint64_t n_bytes, const int64_t* tensor_off, const int64_t* tensor_len,
                         uint32_t n, uint8_t* work, uint8_t* roots, int32_t* status, hipStream_t s);
+int static_tree_work(uint8_t** out);   // device address of the allocation-free entry point's work area
 int launch_export(const uint64_t* table, uint64_t capacity, uint8_t* out_keys, uint64_t* out_locs,
                   uint64_t* count, hipStream_t s);
 

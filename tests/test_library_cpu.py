@@ -33,7 +33,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 21
+    assert len(names) == 22
     lib = pkv.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -187,3 +187,17 @@ def test_sort_pairs_orders_keys_bytewise(seed):
         ref = sorted(range(n), key=lambda i: bytes(k[i]))
         assert [bytes(x) for x in sk] == [bytes(k[i]) for i in ref]
         assert [bytes(k[i]) for i in sl.tolist()] == [bytes(x) for x in sk]
+
+
+def test_static_tensor_roots_refuse_inputs_past_their_buffer():
+    """The allocation-free tensor-root call refuses, on the host and before anything is launched,
+    an input whose work area exceeds the library's per-device buffer."""
+    L = pkv.lib()
+    n_bytes = 1 << 28
+    assert L.pkv_tree_work_bytes(n_bytes, 1) > pkv.STATIC_TREE_WORK_BYTES
+    assert L.pkv_tree_work_bytes(1 << 20, 16) <= pkv.STATIC_TREE_WORK_BYTES
+    rc = L.pkv_tensor_roots_static(0x1000, n_bytes, 0x2000, 0x3000, 1, 0x4000, 0x5000, None)
+    assert rc == pkv.PKV_EINVAL
+    assert b"work area" in L.pkv_last_error()
+    assert L.pkv_tensor_roots_static(0x1000, 6, 0x2000, 0x3000, 1, 0x4000, 0x5000, None) == pkv.PKV_EINVAL
+    assert L.pkv_tensor_roots_static(0x1000, 64, 0x2000, 0x3000, 0, 0x4000, 0x5000, None) == pkv.PKV_OK
