@@ -723,7 +723,7 @@ def main():
     roofline_store = {"bound": "hbm", "achieved": round(store_bps / 1e9, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                       "frac": round(store_bps / HBM_PEAK, 5),
                       "traffic": None if srec is None else int(round(srec["bytes_per_launch"])),
-                      "kernel": "store (k_store + fresh-bit finish; serial pass, events)",
+                      "kernel": "store (k_store; serial pass, events)",
                       "inserts": g["new_entries"], "bytes_per_insert": BYTES_PER_INSERT,
                       "atomics_per_insert": None if srec is None else srec.get("atomics_per_insert")}
     rates = {"derive_gkeys_per_s": round(g["n_keys"] / (g["derive_ms"] * 1e-3) / 1e9, 4),

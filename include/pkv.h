@@ -78,10 +78,10 @@ typedef struct {
 } pkv_field;
 
 /* The shared-tier index (section 2.1 shared KV-cache tier): open addressing over buckets of four
- * slots, one 128-byte bucket per HBM line.  Bucket b covers slots 4b .. 4b + 3 and holds, in order:
- * the four slots' claim words (the first 8 key bytes, or a free-slot marker), four flag words, and
- * four 16-byte pairs {key bytes 8..15, location}.  A key's home bucket is its first 8 bytes
- * (little-endian) modulo the bucket count; probing is linear over slots.
+ * slots, one 128-byte bucket per HBM line.  Slot s is the 32-byte record at byte 32 s: its claim word
+ * (the first 8 key bytes, or a free-slot marker), a tag (the store call that inserted the entry, and
+ * which marker a substitute claim word stands for), key bytes 8..15 and the location.  A key's home
+ * bucket is its first 8 bytes (little-endian) modulo the bucket count; probing is linear over slots.
  *   slots    : pkv_table_bytes(capacity) bytes of device memory, 128-byte aligned.
  *   capacity : a power of two in [4, 2^56].
  * The struct itself is host memory; the buffer is device memory owned by the caller. */
@@ -158,8 +158,8 @@ int pkv_lookup_prefix(const pkv_table* table, const uint8_t* d_keys, const int64
  * d_n_new: one uint64 counter that the call increments by the number of new entries; the
  * caller zeroes it.  d_new_slots: NULL, or room for n_keys uint64: the slot index of each new
  * entry is appended at d_new_slots[old *d_n_new ...] (bit 63 marks a slot that was removed by
- * eviction before, bit 62 a key whose first 8 bytes equal one of the index's marker values,
- * stored with the substitute claim word).  No free slot for a new key sets PKV_EFULL. */
+ * eviction before).  No free slot for a new key sets PKV_EFULL.  Calls that store into one index
+ * must not overlap in time (order them on one stream). */
 int pkv_store(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off,
               uint32_t n_req, uint64_t n_keys, const int32_t* d_hit_blocks, const uint64_t* d_locs,
               uint64_t* d_new_slots, uint64_t* d_n_new, int32_t* d_status, hipStream_t stream);

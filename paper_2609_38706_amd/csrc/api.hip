@@ -3,9 +3,11 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <random>
 #include <vector>
 
 #include "pkv.h"
@@ -155,6 +157,17 @@ int set_error(int code, const char* fmt, ...) {
     std::vsnprintf(g_error, sizeof g_error, fmt, ap);
     va_end(ap);
     return code;
+}
+
+// Store-call generations: strictly increasing within the process, never 0, starting at a random
+// point of a 2^60 range so that two processes writing one index rarely share a generation.
+uint64_t next_generation() {
+    static std::atomic<uint64_t> counter{[] {
+        std::random_device rd;
+        const uint64_t seed = (static_cast<uint64_t>(rd()) << 32) ^ rd();
+        return (seed & ((1ull << 60) - 1)) | 1ull;
+    }()};
+    return counter.fetch_add(1, std::memory_order_relaxed) + 1;
 }
 
 int check_launch(const char* what) {

@@ -1,24 +1,24 @@
 // k_table.hip -- the shared-tier index in HBM: init, longest-prefix lookup, store of misses,
 // rollback, export and eviction to a budget, on gfx950.
 //
-// Layout (pkv_internal.h): 128-byte buckets of 4 slots.  A bucket holds the four slots' claim words
-// (each the first 8 bytes of the slot's key, or a marker), their flag words, and for each slot one
-// 16-byte pair {key bytes 8..15, location word}.  A key's home bucket is its first eight bytes
-// masked to the bucket count; probing is linear over slots, wrapping.  A fixed-budget tier adds
-// epochs[capacity] (uint32): the epoch of each entry's last use.
+// Layout (pkv_internal.h): one 32-byte record per slot {claim word, tag, key bytes 8..15, location},
+// four slots to a 128-byte bucket.  A key's home bucket is its first eight bytes masked to the bucket
+// count; probing is linear over slots, wrapping.  A fixed-budget tier adds epochs[capacity] (uint32):
+// the epoch of each entry's last use.
 //
 // Lookup reads whole buckets: a key is present iff some slot on its probe path holds it, and absent
 // once the path meets a never-used slot (removed slots have their own claim marker, so paths run
-// through them).  Store claims a slot with one 64-bit compare-and-swap on its claim word and then
-// writes the slot's {key bytes 8..15, location} pair with one 16-byte store, inside the same
-// 128-byte bucket (gfx950 has no 128-bit compare-and-swap):
+// through them).  Store claims a slot with one 64-bit compare-and-swap on its claim word, then writes
+// the slot's tag and, with one 16-byte store, its {key bytes 8..15, location} pair, all inside the
+// slot's own 32-byte sector (gfx950 has no 128-bit compare-and-swap):
 //   never used or removed --CAS claim word--> claimed, location kEmpty --16-byte store--> published
 // A lane first scans its key's path up to the first never-used slot, remembering the first removed
-// slot; it then claims that slot (or the never-used one).  A lane that meets a slot claimed with
-// its own claim word but not yet published re-reads it until it is, then compares the rest of the
-// key, so two lanes inserting one key always meet in the same slot.  A later equal key lowers a
-// fresh entry's location with atomic min; entries older than the batch carry no fresh bit and are
-// left untouched.  A final pass clears the fresh bits.
+// slot; it then claims that slot (or the never-used one).  A lane that meets a slot claimed with its
+// own claim word but not yet published re-reads it until it is, then compares the rest of the key, so
+// two lanes inserting one key always meet in the same slot.  Each store call carries its own
+// generation, written into the tag of every entry it inserts: a lane that finds its key inserted by
+// the same call lowers the location with atomic min (the smallest location of the batch wins), while
+// an entry of an earlier call is left untouched.  No pass after the store is needed.
 #include "pkv_internal.h"
 
 namespace pkv {
@@ -81,19 +81,18 @@ __device__ __forceinline__ void store_pair_coherent(uint64_t* p, uint64_t hi, ui
 }
 
 // ---- init -------------------------------------------------------------------------------------
-// Claim words all ones, flag words zero, pairs {all ones, kEmpty}.
+// Every slot {kLoEmpty, tag 0, key bytes all ones, kEmpty}: 16-byte units alternate {claim, tag} and
+// {key bytes 8..15, location}.
 __global__ __launch_bounds__(256) void k_init(uint4* t, uint64_t capacity) {
-    const uint64_t n = capacity * 2;                     // 16-byte units: 8 per bucket
+    const uint64_t n = capacity * 2;                     // 16-byte units: 2 per slot
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
-    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
-        const bool flags = (i & 7) == 2 || (i & 7) == 3;
-        t[i] = flags ? make_uint4(0u, 0u, 0u, 0u) : make_uint4(~0u, ~0u, ~0u, ~0u);
-    }
+    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride)
+        t[i] = (i & 1) ? make_uint4(~0u, ~0u, ~0u, ~0u) : make_uint4(~0u, ~0u, 0u, 0u);
 }
 
 // ---- lookup: one wavefront per request --------------------------------------------------------
-// A request's keys are probed in windows, one lane per key; a lane loads its key's bucket (the
-// four claim words and the four pairs: six 16-byte loads issued together, 96 of its 128 bytes),
+// A request's keys are probed in windows, one lane per key; a lane loads its key's bucket (eight
+// 16-byte loads issued together: each slot's {claim word, tag} and {key bytes 8..15, location}),
 // and the next window's keys are fetched while the current window's buckets are in flight.  A
 // ballot finds the first absent key, which ends the request.  The first window holds
 // LOOKUP_FIRST keys and each later window twice as many, up to 64: probes past a request's first
@@ -106,16 +105,17 @@ constexpr int kLookupWaves = 4;
 constexpr uint32_t kFirstWindow = PKV_LOOKUP_FIRST;
 
 struct Bucket {
-    uint4 c[2];      // claim words 0-1, 2-3
-    uint4 p[4];      // pair j: {key bytes 8..15, location}
+    uint4 c[4];      // slot j: {claim word, tag}
+    uint4 p[4];      // slot j: {key bytes 8..15, location}
 };
 
 __device__ __forceinline__ void load_bucket(const uint4* __restrict__ t, uint64_t b, Bucket& bk) {
     const uint4* q = t + b * (kBucketWords / 2);
-    bk.c[0] = q[0];
-    bk.c[1] = q[1];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bk.p[j] = q[4 + j];
+    for (int j = 0; j < 4; ++j) {
+        bk.c[j] = q[2 * j];
+        bk.p[j] = q[2 * j + 1];
+    }
 }
 
 // Probe of one key (lane-private) whose home bucket is already loaded in bk.  Returns the slot
@@ -123,21 +123,18 @@ __device__ __forceinline__ void load_bucket(const uint4* __restrict__ t, uint64_
 // matches nor holds a never-used slot.
 __device__ __forceinline__ int64_t probe_key(const uint4* __restrict__ t, uint64_t capacity, uint64_t bmask,
                                              const uint4& key, uint64_t b, Bucket& bk) {
-    const uint64_t* w = reinterpret_cast<const uint64_t*>(t);
     const KeyWords kw = key_words(key);
     const uint64_t n_buckets = bmask + 1;
     for (uint64_t it = 0; it < n_buckets; ++it) {
         bool empty = false;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint4 cw = bk.c[j >> 1];
-            const uint64_t claim = (j & 1) ? ((static_cast<uint64_t>(cw.w) << 32) | cw.z)
-                                           : ((static_cast<uint64_t>(cw.y) << 32) | cw.x);
+            const uint64_t claim = (static_cast<uint64_t>(bk.c[j].y) << 32) | bk.c[j].x;
+            const uint32_t flag = bk.c[j].z & 3u;
             const uint64_t hi = (static_cast<uint64_t>(bk.p[j].y) << 32) | bk.p[j].x;
             const uint64_t loc = (static_cast<uint64_t>(bk.p[j].w) << 32) | bk.p[j].z;
             const uint64_t s = b * kSlotsPerBucket + j;
-            if (claim == kw.claim && hi == kw.hi && loc != kEmpty &&
-                (kw.claim != kLoSub || w[b * kBucketWords + 4 + j] == kw.flag))
+            if (claim == kw.claim && hi == kw.hi && loc != kEmpty && (kw.claim != kLoSub || flag == kw.flag))
                 return static_cast<int64_t>(s);
             empty |= claim == kLoEmpty;
         }
@@ -224,6 +221,7 @@ struct StoreArgs {
     uint64_t* n_new;
     uint32_t* epochs;          // null unless the store refreshes epochs
     uint32_t epoch;
+    uint64_t generation;       // this call's generation (tags of the entries it inserts)
     int32_t* status;
 };
 
@@ -278,14 +276,12 @@ __device__ __forceinline__ void read_published_pair(const uint64_t* p, uint64_t&
     }
 }
 
-// Publishes a claimed slot: a substitute claim word first gets its flag word (complete before the
-// pair is written, so a lane that sees the published location reads the final flag), then the
-// pair {key bytes 8..15, location} is written with one 16-byte store.
-__device__ __forceinline__ void publish_slot(const Tab& t, uint64_t s, const KeyWords& kw, uint64_t v) {
-    if (kw.flag) {
-        store_relaxed(t.flag(s), kw.flag);
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    }
+// Publishes a claimed slot: its tag (generation and substitute flag), then {key bytes 8..15,
+// location} with one 16-byte store.  The two stores may land in either order: a reader that sees
+// the location published and the tag still 0 waits for the tag.
+__device__ __forceinline__ void publish_slot(const Tab& t, uint64_t s, const KeyWords& kw, uint64_t generation,
+                                             uint64_t v) {
+    store_relaxed(t.tag(s), make_tag(generation, kw.flag));
     store_pair_coherent(t.pair(s), kw.hi, v);
 }
 
@@ -309,7 +305,7 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
             report(a.status, PKV_ERESERVED);
             active = false;
         }
-        want = loc | kFresh;
+        want = loc;
         key = a.keys[k];
     }
     bool claimed = false;
@@ -336,10 +332,10 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
                 }
                 if (claim) {
                     if (cas_relaxed(t.lo(s), c, kw.claim)) {
-                        publish_slot(t, s, kw, want);
+                        publish_slot(t, s, kw, a.generation, want);
                         if (a.epochs) a.epochs[s] = a.epoch;
                         claimed = true;
-                        my_slot = s | (c == kLoRemoved ? kFromRemoved : 0) | (kw.claim == kLoSub ? kSubLogged : 0);
+                        my_slot = s | (c == kLoRemoved ? kFromRemoved : 0);
                         break;
                     }
                     continue;                        // lost the race: read the slot again
@@ -352,10 +348,20 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
                     if (++waits >= kWaitLimit) { report(a.status, PKV_ESTALL); break; }
                     continue;
                 }
-                if (hi == kw.hi && (kw.claim != kLoSub || load_relaxed(t.flag(s)) == kw.flag)) {
-                    if (loc & kFresh) min_relaxed(t.pair(s) + 1, want);
-                    if (a.epochs) a.epochs[s] = a.epoch;
-                    break;
+                if (hi == kw.hi) {
+                    // the tag tells a substitute claim word's key apart and whether this call
+                    // inserted the entry; it is only needed for those two questions
+                    const bool need_tag = kw.claim == kLoSub || want < loc;
+                    const uint64_t tag = need_tag ? load_relaxed(t.tag(s)) : 0;
+                    if (need_tag && tag == 0) {          // published, tag not landed yet: read it again
+                        if (++waits >= kWaitLimit) { report(a.status, PKV_ESTALL); break; }
+                        continue;
+                    }
+                    if (kw.claim != kLoSub || (tag & 3) == kw.flag) {
+                        if (want < loc && (tag >> 2) == a.generation) min_relaxed(t.loc(s), want);
+                        if (a.epochs) a.epochs[s] = a.epoch;
+                        break;
+                    }
                 }
             }
             s = (s + 1) & slot_mask;
@@ -394,56 +400,12 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
     }
 }
 
-// Clears the fresh bit of the slots the store logged (the index is quiescent: plain accesses).
-__global__ __launch_bounds__(256) void k_store_finish_log(Tab t, const uint64_t* slots, const uint64_t* n_slots,
-                                                          uint64_t max_slots) {
-    uint64_t n = *n_slots;
-    if (n > max_slots) n = max_slots;
-    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
-    for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
-        const uint64_t s = slots[i] & ~kLogFlags;
-        if (s >= t.capacity) continue;
-        uint64_t* p = t.loc(s);
-        const uint64_t l = *p;
-        if (l != kEmpty && (l & kFresh)) *p = l & ~kFresh;
-    }
-}
-
-// Without a slot log: re-finds every candidate's slot and clears its fresh bit.
-__global__ __launch_bounds__(kStoreThreads) void k_store_finish_probe(StoreArgs a) {
-    const uint64_t wave_base = wave_base_of(kStoreThreads);
-    const uint64_t k = wave_base + lane_id();
-    const int64_t total = a.key_off[a.n_req];
-    if (total < 0 || static_cast<uint64_t>(total) > a.n_keys) return;
-    if (!candidate(a, wave_base, k, total)) return;
-    const Tab& t = a.t;
-    const uint4 key = a.keys[k];
-    const KeyWords kw = key_words(key);
-    const uint64_t slot_mask = t.capacity - 1;
-    uint64_t s = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
-    uint64_t probes = 0;
-    while (true) {
-        const uint64_t c = *t.lo(s);
-        if (c == kLoEmpty) return;                        // not stored (an error was reported)
-        if (c == kw.claim && t.pair(s)[0] == kw.hi && (kw.claim != kLoSub || *t.flag(s) == kw.flag)) break;
-        s = (s + 1) & slot_mask;
-        if (++probes >= t.capacity) return;
-    }
-    uint64_t* p = t.loc(s);
-    const uint64_t l = *p;
-    if (l != kEmpty && (l & kFresh)) *p = l & ~kFresh;
-}
-
 // ---- rollback and export ------------------------------------------------------------------------
-// A slot back to the state a store found it in: never used, or removed.  Only a substitute claim
-// word comes with a non-zero flag word.
-__device__ __forceinline__ void clear_slot(const Tab& t, uint64_t s, bool removed, bool sub) {
-    if (sub) *t.flag(s) = 0;
-    *t.lo(s) = removed ? kLoRemoved : kLoEmpty;
+// A slot back to a free state: never used, or removed (two 16-byte stores into its 32-byte record).
+__device__ __forceinline__ void clear_slot(const Tab& t, uint64_t s, bool removed) {
+    const uint32_t m = removed ? 0xFFFFFFFEu : 0xFFFFFFFFu;            // low word of the claim marker
+    *reinterpret_cast<uint4*>(t.lo(s)) = make_uint4(m, ~0u, 0u, 0u);   // claim marker, tag 0
     *reinterpret_cast<uint4*>(t.pair(s)) = make_uint4(~0u, ~0u, ~0u, ~0u);   // key bytes 8..15, kEmpty
-}
-__device__ __forceinline__ void free_slot(const Tab& t, uint64_t s, bool removed) {
-    clear_slot(t, s, removed, *t.lo(s) == kLoSub);
 }
 
 __global__ __launch_bounds__(256) void k_rollback(Tab t, const uint64_t* slots, const uint64_t* n_slots,
@@ -453,9 +415,9 @@ __global__ __launch_bounds__(256) void k_rollback(Tab t, const uint64_t* slots, 
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; i < n; i += stride) {
         const uint64_t e = slots[i];
-        const uint64_t s = e & ~kLogFlags;
+        const uint64_t s = e & ~kFromRemoved;
         if (s < t.capacity)                          // the log says how the slot was found: no read
-            clear_slot(t, s, (e & kFromRemoved) != 0, (e & kSubLogged) != 0);
+            clear_slot(t, s, (e & kFromRemoved) != 0);
     }
 }
 
@@ -469,7 +431,7 @@ __device__ __forceinline__ bool slot_entry(const Tab& t, uint64_t s, uint4& key,
     loc = p[1];
     if (loc == kEmpty) return false;
     if (c == kLoSub) {
-        const uint64_t f = *t.flag(s);
+        const uint64_t f = *t.tag(s) & 3;
         c = f == 1 ? kLoEmpty : (f == 2 ? kLoRemoved : kLoSub);
     }
     const uint64_t hi = p[0];
@@ -530,7 +492,7 @@ __device__ __forceinline__ EvictCtl* evict_ctl(uint32_t* work) {
 
 __device__ __forceinline__ bool live_slot(const Tab& t, uint64_t s) {
     const uint64_t c = *t.lo(s);
-    return c != kLoEmpty && c != kLoRemoved && t.pair(s)[1] != kEmpty;
+    return c != kLoEmpty && c != kLoRemoved && *t.loc(s) != kEmpty;
 }
 
 __global__ __launch_bounds__(256) void k_evict_clear(uint32_t* work, uint64_t* n_evicted) {
@@ -652,7 +614,7 @@ __global__ __launch_bounds__(256) void k_evict_apply(Tab t, const uint32_t* epoc
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t s = blockIdx.x * static_cast<uint64_t>(blockDim.x) + threadIdx.x; s < t.capacity; s += stride) {
         if (!live_slot(t, s) || epochs[s] >= cut) continue;
-        free_slot(t, s, true);
+        clear_slot(t, s, true);
     }
 }
 
@@ -735,21 +697,13 @@ int launch_store(uint64_t* table, uint64_t capacity, const uint8_t* keys, const 
                  uint64_t n_keys, const int32_t* hits, const uint64_t* locs, uint64_t* new_slots, uint64_t* n_new,
                  uint32_t* epochs, uint32_t epoch, int32_t* status, hipStream_t s) {
     if (n_req == 0 || n_keys == 0) return PKV_OK;
-    StoreArgs a{Tab{table, capacity}, reinterpret_cast<const uint4*>(keys), key_off, n_req, n_keys, hits, locs,
-                new_slots, n_new, epochs, epoch, status};
     const uint64_t blocks = (n_keys + kStoreThreads - 1) / kStoreThreads;
     if (blocks > 0x7fffffffull) return set_error(PKV_EINVAL, "pkv_store: too many keys (%llu)",
                                                  static_cast<unsigned long long>(n_keys));
+    StoreArgs a{Tab{table, capacity}, reinterpret_cast<const uint4*>(keys), key_off, n_req, n_keys, hits, locs,
+                new_slots, n_new, epochs, epoch, next_generation(), status};
     hipLaunchKernelGGL(k_store, dim3(static_cast<unsigned>(blocks)), dim3(kStoreThreads), 0, s, a);
-    int rc = check_launch("pkv_store");
-    if (rc) return rc;
-    if (new_slots) {
-        hipLaunchKernelGGL(k_store_finish_log, dim3(grid_for(n_keys, 256, 4096)), dim3(256), 0, s, a.t, new_slots,
-                           n_new, n_keys);
-    } else {
-        hipLaunchKernelGGL(k_store_finish_probe, dim3(static_cast<unsigned>(blocks)), dim3(kStoreThreads), 0, s, a);
-    }
-    return check_launch("pkv_store (finish)");
+    return check_launch("pkv_store");
 }
 
 int launch_rollback(uint64_t* table, uint64_t capacity, const uint64_t* slots, const uint64_t* n_slots,

@@ -22,41 +22,43 @@ static constexpr uint32_t kRoundK[64] = {
 static constexpr uint32_t kInitH[8] = {0x6a09e667u, 0xbb67ae85u, 0x3c6ef372u, 0xa54ff53au,
                                       0x510e527fu, 0x9b05688cu, 0x1f83d9abu, 0x5be0cd19u};
 
-// Index layout.  The table is one array of 128-byte buckets of 4 slots:
-//   bucket word  0..3  claim word of slot j: the key's first 8 bytes (little-endian), or a marker;
-//   bucket word  4..7  flag word of slot j: which key prefix a substitute claim word stands for;
-//   bucket word  8..15 {key bytes 8..15, location word} of slot j, one 16-byte pair per slot.
+// Index layout.  One 32-byte record per slot, four consecutive slots to a 128-byte bucket (one HBM
+// line), so every access to one slot stays inside one 32-byte sector:
+//   word 0  claim word: the key's first 8 bytes (little-endian), or a marker;
+//   word 1  tag: (generation << 2) | flag.  The generation is the store call that inserted the
+//           entry (every call takes a new one, never 0); the flag says which marker a substitute
+//           claim word stands for (1: kLoEmpty, 2: kLoRemoved; 0 for every other key);
+//   word 2  key bytes 8..15;
+//   word 3  location word.
 // Claim word:
 //   kLoEmpty    -- never used; ends every probe path through it;
 //   kLoRemoved  -- removed by eviction: free for a new key, probe paths continue through it;
 //   other       -- claimed by the key whose first 8 bytes it holds.  A key whose first 8 bytes
-//                  equal one of the two markers claims with kLoSub instead, and its slot's flag
-//                  word says which (1: kLoEmpty, 2: kLoRemoved; 0 for every other key).
-// Location word: kEmpty until the claiming lane publishes the entry, then the location; bit 63
-// (kFresh) marks an entry inserted by the running store batch, whose location may still be
-// lowered to the batch minimum.  Valid caller locations are < 2^62.  Every 128-bit value is an
+//                  equal one of the two markers claims with kLoSub instead (and its tag's flag).
+// A free slot holds tag 0, key bytes all ones and location kEmpty.  A claimed slot is published
+// when its location word (written together with key bytes 8..15 by one 16-byte store) leaves
+// kEmpty; its tag is written by a separate store, so a published slot whose tag still reads 0 is
+// one whose tag has not landed yet.  Valid caller locations are < 2^62.  Every 128-bit value is an
 // ordinary key: the markers live only in claim words, never in key bytes.
 static constexpr uint64_t kLoEmpty = ~0ull;
 static constexpr uint64_t kLoRemoved = ~0ull - 1;
 static constexpr uint64_t kLoSub = ~0ull - 2;
 static constexpr uint64_t kEmpty = ~0ull;
-static constexpr uint64_t kFresh = 1ull << 63;
 static constexpr uint64_t kFromRemoved = 1ull << 63;   // slot-log flag: the claimed slot was a removed entry
-static constexpr uint64_t kSubLogged = 1ull << 62;     // slot-log flag: the slot's claim word is the substitute
-static constexpr uint64_t kLogFlags = kFromRemoved | kSubLogged;
 static constexpr uint32_t kSlotsPerBucket = 4;
+static constexpr uint64_t kSlotWords = 4;           // 32 bytes
 static constexpr uint64_t kBucketWords = 16;        // 128 bytes
+
+__host__ __device__ constexpr uint64_t make_tag(uint64_t generation, uint64_t flag) { return (generation << 2) | flag; }
 
 // Word addresses of slot s (< capacity).
 struct Tab {
     uint64_t* w;
     uint64_t capacity;
-    __device__ __forceinline__ uint64_t* lo(uint64_t s) const { return w + (s >> 2) * kBucketWords + (s & 3); }
-    __device__ __forceinline__ uint64_t* flag(uint64_t s) const { return w + (s >> 2) * kBucketWords + 4 + (s & 3); }
-    __device__ __forceinline__ uint64_t* pair(uint64_t s) const {
-        return w + (s >> 2) * kBucketWords + 8 + 2 * (s & 3);
-    }
-    __device__ __forceinline__ uint64_t* loc(uint64_t s) const { return pair(s) + 1; }
+    __device__ __forceinline__ uint64_t* lo(uint64_t s) const { return w + s * kSlotWords; }
+    __device__ __forceinline__ uint64_t* tag(uint64_t s) const { return w + s * kSlotWords + 1; }
+    __device__ __forceinline__ uint64_t* pair(uint64_t s) const { return w + s * kSlotWords + 2; }
+    __device__ __forceinline__ uint64_t* loc(uint64_t s) const { return w + s * kSlotWords + 3; }
 };
 
 namespace dev {
@@ -139,6 +141,7 @@ int launch_lookup(const uint64_t* table, uint64_t capacity, const uint8_t* keys,
 int launch_store(uint64_t* table, uint64_t capacity, const uint8_t* keys, const int64_t* key_off, uint32_t n_req,
                  uint64_t n_keys, const int32_t* hits, const uint64_t* locs, uint64_t* new_slots, uint64_t* n_new,
                  uint32_t* epochs, uint32_t epoch, int32_t* status, hipStream_t s);
+uint64_t next_generation();   // a fresh store-call generation (api.hip)
 int launch_evict(uint64_t* table, uint64_t capacity, const uint32_t* epochs, uint64_t budget, uint32_t* work,
                  uint64_t* n_evicted, hipStream_t s);
 int launch_rollback(uint64_t* table, uint64_t capacity, const uint64_t* slots, const uint64_t* n_slots,

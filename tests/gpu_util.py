@@ -61,7 +61,6 @@ def gpu_fill(table, batch):
 EMPTY = np.uint64(0xFFFFFFFFFFFFFFFF)
 PENDING = np.uint64(0xFFFFFFFFFFFFFFFE)
 TOMB = np.uint64(0xFFFFFFFFFFFFFFFD)
-FRESH = np.uint64(1 << 63)
 TOMB_KEY = np.array([0xFF] * 15 + [0xFE], np.uint8)
 
 
@@ -70,27 +69,30 @@ LO_REMOVED = np.uint64(0xFFFFFFFFFFFFFFFE)
 LO_SUB = np.uint64(0xFFFFFFFFFFFFFFFD)
 
 
+def raw_slots(table):
+    """The index's slot records as uint64 [capacity, 4]: claim word, tag, key bytes 8..15, location."""
+    cap = table.capacity
+    w = table.slots.cpu().numpy().view(np.uint64)
+    assert w.shape[0] == cap * 4, "index buffer is not 32 bytes per slot"
+    return w.reshape(cap, 4)
+
+
 def raw_table(table):
     """The index decoded slot by slot (include/pkv.h layout) into (keys uint8 [capacity, 16], locs
     uint64 [capacity]): a never-used slot reads as the all-0xFF key with location EMPTY, a removed
     slot as TOMB_KEY with location TOMB, a claimed but unpublished slot with location PENDING (these
     key values only stand in for free slots here; a live slot may hold any key).  Also checks the
-    layout's own invariants (free slots hold no key bytes, flags or location; flag words appear only
+    layout's own invariants (free slots hold no key bytes, tag or location; a tag's flag appears only
     with the substitute claim word)."""
-    cap = table.capacity
-    w = table.slots.cpu().numpy().view(np.uint64)
-    assert w.shape[0] == cap * 4, "index buffer is not 32 bytes per slot"
-    b = w.reshape(cap // 4, 16)
-    claim = b[:, 0:4].reshape(-1)
-    flag = b[:, 4:8].reshape(-1)
-    hi = b[:, 8:16:2].reshape(-1)
-    loc = b[:, 9:16:2].reshape(-1)
+    r = raw_slots(table)
+    claim, tag, hi, loc = r[:, 0], r[:, 1], r[:, 2], r[:, 3]
+    flag = tag & np.uint64(3)
     free = (claim == LO_EMPTY) | (claim == LO_REMOVED)
-    assert (flag[free] == 0).all() and (hi[free] == EMPTY).all() and (loc[free] == EMPTY).all(), \
+    assert (tag[free] == 0).all() and (hi[free] == EMPTY).all() and (loc[free] == EMPTY).all(), \
         "free slot with contents"
-    assert ((flag == 0) | (claim == LO_SUB)).all(), "flag word without the substitute claim word"
-    assert (flag <= 2).all(), "unknown flag word"
-    lo = np.where(flag == 1, LO_EMPTY, np.where(flag == 2, LO_REMOVED, claim))
+    assert ((flag == 0) | (claim == LO_SUB)).all(), "substitute flag without the substitute claim word"
+    assert (flag <= 2).all(), "unknown substitute flag"
+    lo = np.where(claim == LO_SUB, np.where(flag == 1, LO_EMPTY, np.where(flag == 2, LO_REMOVED, claim)), claim)
     keys = np.concatenate([lo.view(np.uint8).reshape(-1, 8), hi.view(np.uint8).reshape(-1, 8)], axis=1)
     locs = np.where(loc == EMPTY, PENDING, loc)
     keys[claim == LO_EMPTY] = 0xFF
@@ -103,8 +105,8 @@ def raw_table(table):
 def check_structure(table):
     """Index invariants: every live slot is reachable from its home bucket with no empty slot in
     between (removed slots do not break paths); no claimed-but-unpublished or batch-marked slot
-    survives a store; empty slots hold no key bytes and removed slots the removed placeholder; no key
-    is stored twice.  Returns the number of entries (live slots)."""
+    survives a store and every live slot carries the generation of the store that inserted it;
+    empty slots hold no key bytes and removed slots the removed placeholder; no key is stored twice.  Returns the number of entries (live slots)."""
     keys, locs = raw_table(table)
     cap = table.capacity
     assert locs.shape[0] == cap
@@ -112,11 +114,13 @@ def check_structure(table):
     tomb = locs == TOMB
     live = occ & ~tomb
     assert not (locs == PENDING).any(), "pending slot left behind"
-    assert not (locs[live] & FRESH).any(), "fresh bit left behind"
+    assert not (locs[live] >= np.uint64(1 << 62)).any(), "location outside the caller's range"
+    tags = raw_slots(table)[:, 1]
+    assert ((tags[live] >> np.uint64(2)) != 0).all(), "live slot without the generation of its store"
     assert (keys[~occ] == 0xFF).all(), "empty slot with key bytes"
     assert (keys[tomb] == TOMB_KEY[None, :]).all(), "removed slot without the removed placeholder"
     if live.any():
-        claim = table.slots.cpu().numpy().view(np.uint64).reshape(cap // 4, 16)[:, 0:4].reshape(-1)
+        claim = raw_slots(table)[:, 0]
         lo = keys[:, :8].copy().view("<u8").reshape(-1)
         home = (lo & np.uint64(cap // 4 - 1)).astype(np.int64) * 4
         idx = np.arange(cap, dtype=np.int64)

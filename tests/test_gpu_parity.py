@@ -256,6 +256,37 @@ def test_store_with_skewed_request_lengths(pkv, shape):
     assert int(n_new.item()) == len(idx)
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_earlier_entries_keep_their_location(pkv, seed):
+    """Each store call lowers only the locations of the entries it inserts itself: rounds whose
+    locations are smaller than every earlier round's, over keys that repeat within a batch and across
+    batches (marker-like keys included), give the oracle's index after every round (section 3.4:
+    an entry already present is never replaced; the smallest location of a batch wins)."""
+    import torch
+    from paper_2609_38706_amd.pipeline import export_sorted
+    rng = np.random.default_rng(700 + seed)
+    pool = np.concatenate([_marker_prefixed_pool(rng), rng.integers(0, 256, size=(30, 16), dtype=np.uint8)])
+    capacity = 256
+    idx = oracle.Index(capacity)
+    table = pkv.Table(capacity)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for rnd in range(4):
+        n_req = int(rng.integers(20, 60))
+        keys, ko = _key_batch(rng, pool, n_req, 6)
+        locs = rng.permutation(1 << 16)[: keys.shape[0]].astype(np.uint64) + np.uint64((3 - rnd) << 40)
+        zero = np.zeros(n_req, np.int32)
+        assert idx.store(keys, ko, zero, locs) == 0
+        n_new = torch.zeros(1, dtype=torch.int64, device="cuda")
+        pkv.pkv_store(table, _dev(keys, torch.uint8).reshape(-1, 16), _dev(ko, torch.int64), _dev(zero, torch.int32),
+                      _dev(locs, torch.int64), n_new, status)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        gk, gl = export_sorted(table)
+        ok, ol = idx.dump()
+        assert gk.shape == ok.shape and (gk == ok).all() and (gl == ol).all(), rnd
+        assert check_structure(table) == len(idx)
+
+
 def _marker_prefixed_pool(rng):
     """Keys whose first 8 bytes (the slot claim word, little-endian) equal the never-used marker
     (all 0xFF), the removed marker (0xFE then 0xFF) or the substitute claim word (0xFD then 0xFF),
@@ -284,7 +315,7 @@ def _marker_prefixed_pool(rng):
 @pytest.mark.parametrize("capacity", [32, 256])
 def test_marker_prefixed_keys(pkv, seed, capacity):
     """Claim-word edge cases: keys that claim with the substitute word keep their own identity
-    (flag words), equal keys still merge, lookups find exactly the stored ones, and a rollback
+    (their tags' flags), equal keys still merge, lookups find exactly the stored ones, and a rollback
     restores the index."""
     import torch
     from paper_2609_38706_amd.pipeline import export_sorted
