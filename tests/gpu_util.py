@@ -85,7 +85,7 @@ def raw_table(table):
     layout's own invariants (free slots hold no key bytes, tag or location; a tag's flag appears only
     with the substitute claim word)."""
     r = raw_slots(table)
-    claim, tag, hi, loc = r[:, 0], r[:, 1], r[:, 2], r[:, 3]
+    claim, tag, hi, loc = (np.ascontiguousarray(r[:, i]) for i in range(4))
     flag = tag & np.uint64(3)
     free = (claim == LO_EMPTY) | (claim == LO_REMOVED)
     assert (tag[free] == 0).all() and (hi[free] == EMPTY).all() and (loc[free] == EMPTY).all(), \
@@ -115,12 +115,12 @@ def check_structure(table):
     live = occ & ~tomb
     assert not (locs == PENDING).any(), "pending slot left behind"
     assert not (locs[live] >= np.uint64(1 << 62)).any(), "location outside the caller's range"
-    tags = raw_slots(table)[:, 1]
+    tags = np.ascontiguousarray(raw_slots(table)[:, 1])
     assert ((tags[live] >> np.uint64(2)) != 0).all(), "live slot without the generation of its store"
     assert (keys[~occ] == 0xFF).all(), "empty slot with key bytes"
     assert (keys[tomb] == TOMB_KEY[None, :]).all(), "removed slot without the removed placeholder"
     if live.any():
-        claim = raw_slots(table)[:, 0]
+        claim = np.ascontiguousarray(raw_slots(table)[:, 0])
         lo = keys[:, :8].copy().view("<u8").reshape(-1)
         home = (lo & np.uint64(cap // 4 - 1)).astype(np.int64) * 4
         idx = np.arange(cap, dtype=np.int64)
