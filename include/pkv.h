@@ -13,7 +13,7 @@
  *   hit_r      = largest h such that key_{r,1..h} are all in the index (a longest-prefix hit)
  *   store      : key_{r,j}, j > hit_r, is inserted if absent; among equal keys of one batch the
  *                smallest location wins; entries already present are never modified
- *                (section 3.4: a hit returns the first entry written).
+ *                (section 3.4: insert-if-absent, an entry already present is never replaced).
  *
  * Canonical order (section 5.1 registry; Prop. 1 appends further dimensions): the six core
  * dimensions model_id, adapter_id, weight_dtype, weight_version, kv_format, salt in that order,
@@ -130,7 +130,9 @@ int pkv_expand_digests(const uint8_t* d_desc_digests, uint32_t n_desc, const uin
 int pkv_key_offsets(const int64_t* d_tok_off, uint32_t n_req, uint32_t block, int64_t* d_key_off,
                     hipStream_t stream);
 
-/* Chained block keys of n_req requests (section 5.2, Eq. 3 with f = the chained block key).
+/* Chained block keys of n_req requests (section 5.2, Eq. 3 with f = the chained block key).  Beyond
+ * the specified (tokens, offsets, digests, block, key offsets, keys) this call takes the token and
+ * key counts (bounds checks) and a device status word.
  * d_tokens: n_tokens int32 token ids.  d_tok_off: n_req + 1 int64.  d_digests: n_req x 16
  * bytes (16-byte aligned), one descriptor digest per request.  d_key_off: n_req + 1 int64 as
  * produced by pkv_key_offsets.  d_keys: n_keys x 16 bytes (16-byte aligned).  A request whose
@@ -141,19 +143,26 @@ int pkv_derive_keys(const int32_t* d_tokens, uint64_t n_tokens, const int64_t* d
                     const int64_t* d_key_off, uint64_t n_keys, uint8_t* d_keys,
                     int32_t* d_status, hipStream_t stream);
 
-/* Marks every slot of the index empty. */
+/* Marks every slot of the index empty: the shared tier starts with no entry (section 2.1 shared
+ * KV-cache tier).  Beyond the operations the paper states (digest, derive, lookup, store), the index
+ * needs this set-up call, and the export and rollback below. */
 int pkv_table_init(const pkv_table* table, hipStream_t stream);
 
-/* Longest-prefix hit per request (section 3.4 / 4.1: the prefix a shared tier can serve):
+/* Longest-prefix hit per request (section 3.4 / 4.1: the prefix a shared tier can serve; the key
+ * count and the device status word are additions to the specified signature):
  * d_hit_blocks[r] = largest h with keys key_off[r] .. key_off[r] + h - 1 all present.
  * d_keys: n_keys x 16 bytes; d_key_off: n_req + 1 int64; d_hit_blocks: n_req int32. */
 int pkv_lookup_prefix(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_key_off,
                       uint32_t n_req, uint64_t n_keys, int32_t* d_hit_blocks, int32_t* d_status,
                       hipStream_t stream);
 
-/* Store path: inserts key j (0-based) of request r with location d_locs[key_off[r] + j] for
- * every j >= d_hit_blocks[r], unless the key is already present.  Duplicates inside the batch
- * keep the smallest location; entries present before the call are never changed.
+/* Store path (section 2.1: a worker stores the KV blocks it computed into the shared tier;
+ * section 3.4: insert-if-absent, an entry already present is never replaced): inserts key j
+ * (0-based) of request r with location d_locs[key_off[r] + j] for every j >= d_hit_blocks[r],
+ * unless the key is already present.  Duplicates inside the batch keep the smallest location;
+ * entries present before the call are never changed.  Compared with the four-call interface the
+ * path is specified by, this call also takes the key count (bounds checks), a device status word
+ * for errors found by the kernel, an optional slot log (rollback) and a new-entry counter.
  * d_locs: n_keys uint64 (< PKV_LOC_LIMIT, else PKV_ERESERVED).
  * d_n_new: one uint64 counter that the call increments by the number of new entries; the
  * caller zeroes it.  d_new_slots: NULL, or room for n_keys uint64: the slot index of each new
@@ -170,7 +179,9 @@ int pkv_store(const pkv_table* table, const uint8_t* d_keys, const int64_t* d_ke
 int pkv_table_rollback(const pkv_table* table, const uint64_t* d_new_slots, const uint64_t* d_n_new,
                        uint64_t max_slots, hipStream_t stream);
 
-/* Copies every occupied (key, location) pair out, in no particular order.  d_keys_out: room for
+/* Copies every occupied (key, location) pair out, in no particular order: the index contents as
+ * a set, which is how stored state is compared with the definition of the store (section 3.4) and
+ * how an index is saved across a restart (section 6.3).  d_keys_out: room for
  * capacity keys; d_locs_out: capacity words; *d_count receives the number of pairs (the call
  * zeroes it first). */
 int pkv_table_export(const pkv_table* table, uint8_t* d_keys_out, uint64_t* d_locs_out,

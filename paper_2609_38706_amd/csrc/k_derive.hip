@@ -10,6 +10,8 @@
 // A chain is strictly serial, so one lane owns one request and a wavefront owns 64 requests;
 // all work is 32-bit integer VALU (v_alignbit rotates, v_bitop3/v_bfi logic, v_add3 sums,
 // v_perm byte swaps).
+#include <atomic>
+
 #include "pkv_internal.h"
 
 namespace pkv {
@@ -1299,17 +1301,18 @@ __global__ __launch_bounds__(256) void k_key_offsets_add(uint32_t n_req, int64_t
 
 }  // namespace
 
-// Compute units of the current device (cached per device).
+// Compute units of the current device, cached per device.  Threads that race on the first call of a
+// device all store the same value; the atomics make that well defined.
 int compute_units() {
-    static int cached[64] = {0};
+    static std::atomic<int> cached[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (!cached[dev]) {
-        int cu = 0;
+    int cu = cached[dev].load(std::memory_order_relaxed);
+    if (cu <= 0) {
         if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
-        cached[dev] = cu;
+        cached[dev].store(cu, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return cu;
 }
 
 int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_off, uint32_t n_req,

@@ -81,9 +81,11 @@ def test_ragged_with_empty_requests_in_between(pkv):
 @pytest.mark.parametrize("n_req,block", [(8192, 16), (8193, 16), (16384, 16), (16385, 16), (8192, 32), (8193, 32),
                                          (16385, 48)])
 def test_derive_kernels_agree_at_the_switches(pkv, n_req, block):
-    """8192 requests = 256 workgroups of 32 lane-pair chains (the last size of the lane-pair kernels);
-    8193..16384 run the two-wavefront kernels with one lane per chain; from 16385 on the
-    one-wavefront kernels.  Every kernel, for B = 16 and for B = 16m, must give the oracle's keys."""
+    """The kernel switches at 256 compute units.  B = 16: up to 8192 requests run one lane-pair
+    consumer/helper pair per workgroup (32 chains each), 8193..16384 two pairs per workgroup, from
+    16385 on one lane per chain.  B = 16m: up to 8192 requests the lane-pair kernel, 8193..16384 the
+    consumer/helper kernel with one lane per chain, from 16385 on the one-wavefront kernel.  Every
+    kernel must give the oracle's keys."""
     rng = np.random.default_rng(n_req + block)
     lens = rng.integers(0, 4 * block, size=n_req)
     off = np.zeros(n_req + 1, np.int64)

@@ -1,5 +1,5 @@
 """Pins of the oracle's index semantics (lookup = longest stored prefix of block keys; store =
-insert-if-absent, section 3.4: a hit returns the first entry written).  Checked against a
+insert-if-absent, section 3.4: an entry already present is never replaced).  Checked against a
 brute-force Python dict on small random inputs with planted overlaps."""
 
 import numpy as np
