@@ -1216,7 +1216,7 @@ __global__ __launch_bounds__(256) void k_expand_digests(const uint4* desc_digest
 // chunk's offset (the final value at its start) to the rest of the chunk.  The chunk ends double as
 // the scratch, so the call needs no memory beyond its output.
 constexpr int kScanThreads = 1024;
-constexpr int kScanPerThread = 8;
+constexpr int kScanPerThread = 16;
 constexpr uint32_t kScanChunk = kScanThreads * kScanPerThread;
 
 // Inclusive scan of per-thread sums across the workgroup: returns this thread's exclusive prefix;

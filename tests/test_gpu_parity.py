@@ -615,9 +615,9 @@ def test_workload_c4(pkv):
     assert check_structure(table) == len(idx)
 
 
-@pytest.mark.parametrize("n_req", [1, 8191, 8192, 8193, 3 * 8192 + 5, 100000])
+@pytest.mark.parametrize("n_req", [1, 8192, 16383, 16384, 16385, 3 * 16384 + 5, 100000])
 def test_key_offsets_across_scan_chunks(pkv, n_req):
-    """The key-offset scan works in chunks of 8192 requests; sizes around and across chunk ends must
+    """The key-offset scan works in chunks of 16384 requests; sizes around and across chunk ends must
     give the oracle's prefix sums of floor(len / B)."""
     import torch
     rng = np.random.default_rng(n_req)
