@@ -81,7 +81,10 @@ typedef struct {
  * slots, one 128-byte bucket per HBM line.  Slot s is the 32-byte record at byte 32 s: its claim word
  * (the first 8 key bytes, or a free-slot marker), a tag (the store call that inserted the entry, and
  * which marker a substitute claim word stands for), key bytes 8..15 and the location.  A key's home
- * bucket is its first 8 bytes (little-endian) modulo the bucket count; probing is linear over slots.
+ * bucket is its first 8 bytes (little-endian) modulo the bucket count; its probe path visits the
+ * home bucket and then the following buckets (wrapping), the slots of each bucket in the order
+ * r, r + 1, r + 2, r + 3 (mod 4) with r = key byte 8 mod 4, and a key sits at or before the first
+ * never-used slot of its path.
  *   slots    : pkv_table_bytes(capacity) bytes of device memory, 128-byte aligned.
  *   capacity : a power of two in [4, 2^56].
  * The struct itself is host memory; the buffer is device memory owned by the caller. */

@@ -3,7 +3,7 @@
 //
 // Layout (pkv_internal.h): one 32-byte record per slot {claim word, tag, key bytes 8..15, location},
 // four slots to a 128-byte bucket.  A key's home bucket is its first eight bytes masked to the bucket
-// count; probing is linear over slots, wrapping.  A fixed-budget tier adds epochs[capacity] (uint32):
+// count; probing continues over the following buckets, wrapping.  A fixed-budget tier adds epochs[capacity] (uint32):
 // the epoch of each entry's last use.
 //
 // Lookup reads whole buckets: a key is present iff some slot on its probe path holds it, and absent
@@ -12,8 +12,10 @@
 // the slot's tag and, with one 16-byte store, its {key bytes 8..15, location} pair, all inside the
 // slot's own 32-byte sector (gfx950 has no 128-bit compare-and-swap):
 //   never used or removed --CAS claim word--> claimed, location kEmpty --16-byte store--> published
-// A lane first scans its key's path up to the first never-used slot, remembering the first removed
-// slot; it then claims that slot (or the never-used one).  A lane that meets a slot claimed with its
+// A key's path starts in its home bucket at a slot chosen by two bits of the key and continues over
+// the bucket's other slots and then the following buckets.  A lane first scans its key's path up to
+// the first never-used slot, remembering the first removed slot; it then claims that slot (or the
+// never-used one).  A lane that meets a slot claimed with its
 // own claim word but not yet published re-reads it until it is, then compares the rest of the key, so
 // two lanes inserting one key always meet in the same slot.  Each store call carries its own
 // generation, written into the tag of every entry it inserts: a lane that finds its key inserted by
@@ -60,6 +62,15 @@ __device__ __forceinline__ KeyWords key_words(const uint4& k) {
     w.claim = w.flag ? kLoSub : w.lo;
     return w;
 }
+
+// A key's probe path visits its home bucket and then the following buckets (wrapping), each bucket's
+// four slots in the order rot, rot + 1, rot + 2, rot + 3 (mod 4), where rot is two bits of the key's
+// second half (independent of the home bucket, which the first half gives).  Keys of one bucket so
+// spread their first choices over its four slots, and a store's scan meets a free slot after fewer
+// reads than when every key starts at the bucket's first slot.  Position p counts along the path
+// from the home bucket's first position; path_slot gives the slot at p.
+__device__ __forceinline__ uint64_t path_rotation(const KeyWords& kw) { return kw.hi & 3; }
+__device__ __forceinline__ uint64_t path_slot(uint64_t p, uint64_t rot) { return (p & ~3ull) | ((p + rot) & 3); }
 
 // Device-coherent 16-byte access to a slot's {key bytes 8..15, location} pair.  The sc1 bit gives
 // the same agent-scope coherence that the compiler uses for relaxed agent-scope atomics (the
@@ -313,11 +324,13 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
     if (active) {
         const KeyWords kw = key_words(key);
         const uint64_t slot_mask = t.capacity - 1;
-        uint64_t s = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
-        uint64_t steps = 0, first_free = ~0ull;  // slots passed in the current phase; first removed slot
+        const uint64_t rot = path_rotation(kw);
+        uint64_t p = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;   // path position
+        uint64_t steps = 0, first_free = ~0ull;  // slots passed in the current phase; first removed slot's position
         uint32_t waits = 0;
         bool scanning = true;                    // phase 1: the key may still sit further along
         while (true) {
+            const uint64_t s = path_slot(p, rot);
             const uint64_t c = load_relaxed(t.lo(s));
             if (c == kLoEmpty || c == kLoRemoved) {
                 bool claim = !scanning;
@@ -325,7 +338,7 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
                     scanning = false;
                     steps = 0;
                     if (first_free != ~0ull) {       // claim the first removed slot on the path instead
-                        s = first_free;
+                        p = first_free;
                         continue;
                     }
                     claim = true;
@@ -340,7 +353,7 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
                     }
                     continue;                        // lost the race: read the slot again
                 }
-                if (first_free == ~0ull) first_free = s;   // a removed slot met while scanning
+                if (first_free == ~0ull) first_free = p;   // a removed slot met while scanning
             } else if (c == kw.claim) {
                 uint64_t hi, loc;
                 read_published_pair(t.pair(s), hi, loc);
@@ -364,12 +377,12 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
                     }
                 }
             }
-            s = (s + 1) & slot_mask;
+            p = (p + 1) & slot_mask;
             if (++steps >= t.capacity) {         // a whole cycle
                 if (scanning && first_free != ~0ull) {
                     scanning = false;
                     steps = 0;
-                    s = first_free;
+                    p = first_free;
                     continue;
                 }
                 report(a.status, PKV_EFULL);

@@ -103,8 +103,8 @@ def raw_table(table):
 
 
 def check_structure(table):
-    """Index invariants: every live slot is reachable from its home bucket with no empty slot in
-    between (removed slots do not break paths); no claimed-but-unpublished or batch-marked slot
+    """Index invariants: every live slot lies on its key's probe path (include/pkv.h) with no
+    never-used slot before it on the path (removed slots do not break paths); no claimed-but-unpublished or batch-marked slot
     survives a store and every live slot carries the generation of the store that inserted it;
     empty slots hold no key bytes and removed slots the removed placeholder; no key is stored twice.  Returns the number of entries (live slots)."""
     keys, locs = raw_table(table)
@@ -122,18 +122,28 @@ def check_structure(table):
     if live.any():
         claim = np.ascontiguousarray(raw_slots(table)[:, 0])
         lo = keys[:, :8].copy().view("<u8").reshape(-1)
-        home = (lo & np.uint64(cap // 4 - 1)).astype(np.int64) * 4
-        idx = np.arange(cap, dtype=np.int64)
-        # last empty position at or before each index, cyclically
-        last = np.where(~occ, idx, -1)
-        last = np.maximum.accumulate(last)
-        if (~occ).any():
-            wrap_last = int(idx[~occ][-1]) - cap
+        n_b = cap // 4
+        s = np.flatnonzero(live).astype(np.int64)
+        home = (lo[s] & np.uint64(n_b - 1)).astype(np.int64)
+        rot = (keys[s, 8] & 3).astype(np.int64)            # the path's first slot in each bucket
+        b_s, j_s = s // 4, s % 4
+        # buckets from the home bucket up to the slot's own: none may hold a never-used slot
+        has_empty = (~occ).reshape(n_b, 4).any(axis=1)
+        bidx = np.arange(n_b, dtype=np.int64)
+        last = np.maximum.accumulate(np.where(has_empty, bidx, -1))     # last such bucket at or before b
+        if has_empty.any():
+            wrap_last = int(bidx[has_empty][-1]) - n_b
             last = np.where(last < 0, wrap_last, last)
-            s = idx[live]
-            dist_home = (s - home[live]) % cap
-            dist_empty = s - last[live]
-            assert (dist_home < dist_empty).all(), "live slot not reachable from its home bucket"
+            before = np.where(b_s > 0, last[b_s - 1], wrap_last)          # strictly before b_s, cyclically
+            dist_home = (b_s - home) % n_b
+            dist_empty = b_s - before
+            assert (dist_home < dist_empty).all(), "live slot behind a bucket with a never-used slot"
+        # inside its bucket: the slots that come before it on the path are not never-used
+        pos = (j_s - rot) & 3
+        for i in range(3):
+            earlier = b_s * 4 + ((rot + i) & 3)
+            bad = (i < pos) & ~occ[earlier]
+            assert not bad.any(), "live slot behind a never-used slot of its bucket"
         assert not ((claim == LO_EMPTY) | (claim == LO_REMOVED))[live].any(), "live slot with a free marker"
         w = np.ascontiguousarray(keys[live]).view(">u8").reshape(-1, 2)
         order = np.argsort(w[:, 0])

@@ -615,6 +615,25 @@ def test_workload_c4(pkv):
     assert check_structure(table) == len(idx)
 
 
+@pytest.mark.gpu
+def test_key_offsets_long_requests_and_block_sizes(pkv):
+    """Lengths beyond 2^32 tokens and block sizes that are and are not powers of two give the oracle's
+    floor(len / B) sums (only the offsets are read, so no tokens are allocated)."""
+    import torch
+    rng = np.random.default_rng(44)
+    n_req = 3000
+    lens = rng.integers(0, 1 << 12, size=n_req)
+    big = rng.random(n_req) < 0.1
+    lens[big] = rng.integers(1 << 31, 1 << 40, size=int(big.sum()))
+    off = np.zeros(n_req + 1, np.int64)
+    off[1:] = np.cumsum(lens)
+    for block in (1, 2, 7, 16, 1000, 1 << 20, 3000000019, 0xFFFFFFFF):
+        tok_off = torch.from_numpy(off).cuda()
+        key_off = torch.full((n_req + 1,), -5, dtype=torch.int64, device="cuda")
+        pkv.pkv_key_offsets(tok_off, block, key_off)
+        assert (key_off.cpu().numpy() == oracle.key_offsets(off, block)).all(), block
+
+
 @pytest.mark.parametrize("n_req", [1, 8192, 16383, 16384, 16385, 3 * 16384 + 5, 100000])
 def test_key_offsets_across_scan_chunks(pkv, n_req):
     """The key-offset scan works in chunks of 16384 requests; sizes around and across chunk ends must
