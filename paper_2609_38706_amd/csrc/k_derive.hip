@@ -1137,63 +1137,191 @@ __device__ __forceinline__ uint32_t msg_word_bytes(const uint8_t* p, uint64_t L,
     return v;
 }
 
-// The same word from an aligned message whose rounded-up length lies inside the pool: the dword
-// is loaded unconditionally (index clamped to the message's last word) and padded with selects,
-// so loads of a whole block can be issued together.
-__device__ __forceinline__ uint32_t msg_word_fast(const uint32_t* p4, uint64_t L, uint64_t q) {
-    const uint64_t last = (L - 1) >> 2;                  // L > 0 on this path
-    const uint32_t be = bswap(p4[q < last ? q : last]);
-    const int64_t r = static_cast<int64_t>(L) - static_cast<int64_t>(4 * q);   // message bytes in this word
-    const uint32_t keep = r >= 4 ? 0xFFFFFFFFu : (r <= 0 ? 0u : (0xFFFFFFFFu << (8 * (4 - r))));
-    const uint32_t pad = (r >= 0 && r < 4) ? (0x80u << (8 * (3 - r))) : 0u;
-    return (be & keep) | pad;
+
+// One message per lane pair, with the derive's paired rounds (the e lane holds e, f, g, h, the a
+// lane a, b, c, d).  Both lanes read the block's 16 words; the pair splits the block's schedule
+// (even words on the e lane, odd ones on the a lane, pair_schedule_step), and each odd K + W word
+// is swapped over to the e lane, which forms Q.  A wavefront holds 32 messages and runs as many
+// blocks as its longest message; a pair past its message's last block keeps its state.
+//
+// The message words come from LDS: the workgroup first copies the byte span of the pool that its
+// messages occupy (whole dwords, when it fits the stage) with coalesced loads, so each block costs
+// LDS reads instead of a round trip to memory (with one, a block took about 4.5 µs whatever its
+// arithmetic).  A word at any byte alignment is two stage dwords and one byte-aligned funnel shift.
+// Spans larger than the stage read the pool directly, one block ahead.
+constexpr uint32_t kDigestPairs = 32;
+constexpr uint32_t kDigestStageWords = 8192;          // 32 KiB
+
+// A message word, big-endian, from its 4 bytes in memory order (le) and the message bytes r it
+// holds, clamped to [-1, 4]: 4 keeps it whole, 0..3 keep r bytes and put the 0x80 padding byte
+// after them, -1 (past the padding byte) gives 0.
+__device__ __forceinline__ uint32_t pad_word(uint32_t le, int32_t r) {
+    const uint32_t keep = static_cast<uint32_t>(0xFFFFFFFFull << (8 * (4 - (r > 0 ? r : 0))));
+    const uint32_t pad = r >= 0 ? static_cast<uint32_t>(0x80000000ull >> (8 * r)) : 0u;
+    return (bswap(le) & keep) | pad;
 }
 
-__global__ __launch_bounds__(64) void k_digest(const uint8_t* bytes, uint64_t n_bytes, const int64_t* off,
-                                               const uint32_t* len, uint32_t n, uint8_t* out, int32_t* status) {
-    const uint32_t i = blockIdx.x * 64 + threadIdx.x;
-    if (i >= n) return;
-    const int64_t o = off[i];
-    const uint64_t L = len[i];
-    if (o < 0 || static_cast<uint64_t>(o) > n_bytes || L > n_bytes - static_cast<uint64_t>(o)) {
-        dev::report(status, PKV_ELAYOUT);
-        return;
+__global__ __launch_bounds__(64) void k_digest_pp(const uint8_t* bytes, uint64_t n_bytes, const int64_t* off,
+                                                  const uint32_t* len, uint32_t n, uint8_t* out, int32_t* status) {
+    __shared__ uint32_t stage[kDigestStageWords + 17];   // 17 words of slack: a block's reads are never clamped
+    const uint32_t lane = threadIdx.x;
+    const uint32_t c = pair_chain(lane);
+    const bool odd = pair_is_a(lane);
+    const uint32_t i = blockIdx.x * kDigestPairs + c;
+    bool valid = i < n;
+    int64_t o = 0;
+    uint64_t L = 0;
+    if (valid) {
+        o = off[i];
+        L = len[i];
+        if (o < 0 || static_cast<uint64_t>(o) > n_bytes || L > n_bytes - static_cast<uint64_t>(o)) {
+            dev::report(status, PKV_ELAYOUT);
+            valid = false;
+        }
     }
+    if (!valid) {
+        o = 0;
+        L = 0;
+    }
+    const int64_t n_blocks = valid ? static_cast<int64_t>((L + 9 + 63) / 64) : 0;
+    const int64_t max_blocks = wave_max(n_blocks);
+    const uint64_t bitlen = L * 8;
+
+    // the workgroup's messages as one byte span [lo, hi) of the pool, widened to whole dwords
+    const int64_t lo = -wave_max(valid ? -o : -INT64_MAX);
+    const int64_t hi = wave_max(valid ? o + static_cast<int64_t>(L) : 0);
+    const uintptr_t b0 = reinterpret_cast<uintptr_t>(bytes), pool_end = b0 + n_bytes;
+    const uintptr_t s0 = (b0 + static_cast<uintptr_t>(lo)) & ~static_cast<uintptr_t>(3);
+    const uint64_t nw = hi > lo ? ((b0 + static_cast<uintptr_t>(hi) + 3) - s0) / 4 : 0;
+    const bool staged = nw > 0 && nw <= kDigestStageWords;       // the same on every lane
+    if (staged) {
+        // Dwords [k_in0, k_in1) lie wholly inside the pool and are copied with unconditional loads,
+        // 16 per lane at a time (the index clamped into the range); the span starts at most 3
+        // bytes before the pool and ends at most 3 bytes past it, so at most the first and the
+        // last dword are assembled from the pool's bytes.
+        const uint64_t k_in0 = s0 < b0 ? 1 : 0;
+        const uint64_t k_in1 = pool_end >= s0 + 4 ? ((pool_end - s0) / 4 < nw ? (pool_end - s0) / 4 : nw) : 0;
+        const uint32_t* s4 = reinterpret_cast<const uint32_t*>(s0);
+        if (k_in1 > k_in0) {
+            for (uint64_t k0 = k_in0 + lane; k0 < k_in1; k0 += 64 * 16) {
+                uint32_t v[16];
+#pragma unroll
+                for (int u = 0; u < 16; ++u) {
+                    const uint64_t k = k0 + 64 * u;
+                    v[u] = s4[k < k_in1 ? k : k_in1 - 1];
+                }
+#pragma unroll
+                for (int u = 0; u < 16; ++u) {
+                    const uint64_t k = k0 + 64 * u;
+                    if (k < k_in1) stage[k] = v[u];
+                }
+            }
+        }
+        const uint64_t edge = lane == 0 ? 0 : nw - 1;  // lane 0: the first dword, lane 1: the last
+        if (lane < 2 && (edge < k_in0 || edge >= k_in1)) {
+            const uintptr_t a = s0 + 4 * edge;
+            uint32_t v = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (a + j >= b0 && a + j < pool_end) v |= static_cast<uint32_t>(*reinterpret_cast<const uint8_t*>(a + j)) << (8 * j);
+            stage[edge] = v;
+        }
+        // one wavefront: its later LDS reads see these writes
+    }
+    const uint64_t sb = (b0 + static_cast<uintptr_t>(o)) - s0;    // the message's start in the stage (bytes)
+    const uint32_t sh = static_cast<uint32_t>(sb & 3);
+    const uint64_t sk = sb >> 2;
     const uint8_t* p = bytes + o;
     const bool fast = L > 0 && (reinterpret_cast<uintptr_t>(p) & 3) == 0 &&
                       static_cast<uint64_t>(o) + ((L + 3) & ~3ull) <= n_bytes;
     const uint32_t* p4 = reinterpret_cast<const uint32_t*>(p);
-    const uint64_t n_blocks = (L + 9 + 63) / 64;
-    const uint64_t bitlen = L * 8;
-    uint32_t s[8], nxt[16];
-    init_state(s);
-    if (fast) {
+
+    // A block's raw words are read one block ahead (into the same registers that the block before
+    // has just consumed), then assembled: from the stage, two dwords and a byte-aligned shift per
+    // word; from an aligned message, its dwords; otherwise byte by byte.
+    const uint64_t flast = fast ? (L - 1) >> 2 : 0;
+    PairLane pl;
+    pl.m = odd ? ~0u : 0u;
+    pl.nm = ~pl.m;
+    pl.r1 = odd ? 2u : 6u;
+    pl.r2 = odd ? 13u : 11u;
+    pl.r3 = odd ? 22u : 25u;
+    const PairK pk = make_pair_k(odd);
+    uint32_t x[4];
 #pragma unroll
-        for (int q = 0; q < 16; ++q) nxt[q] = msg_word_fast(p4, L, q);
-    } else {
+    for (int q = 0; q < 4; ++q) x[q] = odd ? kInitH[q] : kInitH[4 + q];
+#define PKV_DIGEST_READ_RAW(BLK)                                                                  \
+    do {                                                                                          \
+        if (staged) {                                                                             \
+            const uint64_t kb64 = sk + 16 * static_cast<uint64_t>(BLK);                           \
+            const uint32_t kb = kb64 < kDigestStageWords ? static_cast<uint32_t>(kb64) : kDigestStageWords; \
+            _Pragma("unroll") for (int qr = 0; qr < 17; ++qr) raw[qr] = stage[kb + qr];           \
+        } else if (fast) {                                                                        \
+            _Pragma("unroll") for (int qr = 0; qr < 16; ++qr) {                                   \
+                const uint64_t qq = 16 * static_cast<uint64_t>(BLK) + qr;                         \
+                raw[qr] = p4[qq < flast ? qq : flast];                                            \
+            }                                                                                     \
+        }                                                                                         \
+    } while (0)
+    uint32_t raw[17] = {};
+    PKV_DIGEST_READ_RAW(0);
+    for (int64_t blk = 0; blk < max_blocks; ++blk) {
+        uint32_t w[16], kw[64];
+        {
+            // message bytes from this block on, clamped: what each word keeps follows from it; a
+            // lane past its message (or without one) assembles words that it masks out
+            const int64_t rem64 = static_cast<int64_t>(L) - 64 * blk;
+            const int32_t rem = static_cast<int32_t>(rem64 < -1 ? -1 : (rem64 > 68 ? 68 : rem64));
+            if (staged || fast) {
 #pragma unroll
-        for (int q = 0; q < 16; ++q) nxt[q] = msg_word_bytes(p, L, q);
-    }
-    for (uint64_t c = 0; c < n_blocks; ++c) {
-        uint32_t w[16];
-#pragma unroll
-        for (int q = 0; q < 16; ++q) w[q] = nxt[q];
-        if (c + 1 < n_blocks) {                        // the next block's words load under this compression
-            if (fast) {
-#pragma unroll
-                for (int q = 0; q < 16; ++q) nxt[q] = msg_word_fast(p4, L, 16 * (c + 1) + q);
+                for (int q = 0; q < 16; ++q) {
+                    const uint32_t le = staged ? __builtin_amdgcn_alignbyte(raw[q + 1], raw[q], sh) : raw[q];
+                    const int32_t r = rem - 4 * q;
+                    w[q] = pad_word(le, r < -1 ? -1 : (r > 4 ? 4 : r));
+                }
             } else {
 #pragma unroll
-                for (int q = 0; q < 16; ++q) nxt[q] = msg_word_bytes(p, L, 16 * (c + 1) + q);
+                for (int q = 0; q < 16; ++q) w[q] = msg_word_bytes(p, L, 16 * static_cast<uint64_t>(blk) + q);
             }
-        } else {
-            w[14] = static_cast<uint32_t>(bitlen >> 32);
-            w[15] = static_cast<uint32_t>(bitlen);
+            if (blk + 1 == n_blocks) {                 // the last block ends with the bit length
+                w[14] = static_cast<uint32_t>(bitlen >> 32);
+                w[15] = static_cast<uint32_t>(bitlen);
+            }
         }
-        compress(s, w);
+        if (blk + 1 < max_blocks) PKV_DIGEST_READ_RAW(blk + 1);
+#pragma unroll
+        for (int t = 0; t < 16; ++t) kw[t] = w[t] + kRoundK[t];
+        uint32_t v[8];                                 // own words, newest first (a select per word, not an index)
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = bsel(pk.m, w[15 - 2 * k], w[14 - 2 * k]);
+        // the schedule's 16 words for rounds 16 (ph + 1) .. 16 (ph + 1) + 15 are made just before
+        // rounds 16 ph .. 16 ph + 15, which need the first of them, so only 32 K + W words are live
+        auto schedule16 = [&](int j0) {
+#pragma unroll
+            for (int j = j0; j < j0 + 8; ++j) {
+                uint32_t wk;
+                pair_schedule_step(v, pk.m, pk.k[j], wk);
+                kw[2 * j] = wk;                        // on the e lane: K + W of round 2j
+                kw[2 * j + 1] = lane_swap(wk);         // on the e lane: the a lane's K + W of round 2j + 1
+            }
+        };
+        uint32_t y[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) y[q] = x[q];
+        uint32_t q = (y[3] + kw[0]) & pl.nm;
+#pragma unroll
+        for (int ph = 0; ph < 4; ++ph) {
+            if (ph < 3) schedule16(8 + 8 * ph);
+            pair_rounds16_regs(y, q, pl, kw + 16 * ph, ph < 3 ? kw[16 * ph + 16] : 0u);
+        }
+        const bool act = blk < n_blocks;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) x[k] = act ? x[k] + y[k] : x[k];
     }
-    reinterpret_cast<uint4*>(out)[i] = make_uint4(bswap(s[0]), bswap(s[1]), bswap(s[2]), bswap(s[3]));
+    if (valid && odd)                                  // the a lane holds H0..H3
+        reinterpret_cast<uint4*>(out)[i] = make_uint4(bswap(x[0]), bswap(x[1]), bswap(x[2]), bswap(x[3]));
 }
+#undef PKV_DIGEST_READ_RAW
 
 // ---- per-request digests from per-descriptor digests: one lane per request -------------------
 __global__ __launch_bounds__(256) void k_expand_digests(const uint4* desc_digests, uint32_t n_desc, const uint32_t* idx,
@@ -1344,7 +1472,8 @@ int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_o
 int launch_digest_batch(const uint8_t* bytes, uint64_t n_bytes, const int64_t* off, const uint32_t* len, uint32_t n,
                         uint8_t* out, int32_t* status, hipStream_t s) {
     if (n == 0) return PKV_OK;
-    hipLaunchKernelGGL(k_digest, dim3((n + 63) / 64), dim3(64), 0, s, bytes, n_bytes, off, len, n, out, status);
+    hipLaunchKernelGGL(k_digest_pp, dim3((n + kDigestPairs - 1) / kDigestPairs), dim3(64), 0, s, bytes, n_bytes, off,
+                       len, n, out, status);
     return check_launch("pkv_digest_batch");
 }
 

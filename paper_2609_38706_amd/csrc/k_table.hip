@@ -106,14 +106,11 @@ __global__ __launch_bounds__(256) void k_init(uint4* t, uint64_t capacity) {
 // 16-byte loads issued together: each slot's {claim word, tag} and {key bytes 8..15, location}),
 // and the next window's keys are fetched while the current window's buckets are in flight.  A
 // ballot finds the first absent key, which ends the request.  The first window holds
-// LOOKUP_FIRST keys and each later window twice as many, up to 64: probes past a request's first
+// kFirstWindow keys and each later window twice as many, up to 64: probes past a request's first
 // miss are wasted bandwidth, so short prefixes (and misses on the first key) probe few keys,
 // while long prefixes soon reach full 64-key windows.
-#ifndef PKV_LOOKUP_FIRST
-#define PKV_LOOKUP_FIRST 16
-#endif
 constexpr int kLookupWaves = 4;
-constexpr uint32_t kFirstWindow = PKV_LOOKUP_FIRST;
+constexpr uint32_t kFirstWindow = 16;
 
 struct Bucket {
     uint4 c[4];      // slot j: {claim word, tag}

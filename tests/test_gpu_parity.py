@@ -104,6 +104,34 @@ def test_digest_batch_unaligned_pool(pkv):
         assert got[i].tobytes() == oracle.sha256(e)[:16]
 
 
+@pytest.mark.gpu
+@pytest.mark.parametrize("shift", [0, 1, 3])
+def test_digest_batch_every_length(pkv, shift):
+    """Messages of every length 0..200 bytes (every padding case of one to four SHA-256 blocks:
+    55/56 and 119/120 bytes put the length in the same or the next block), 4-byte aligned
+    (shift 0) or not, in a pool whose last message ends on its last byte; 201 messages span
+    several workgroups and leave a partial one."""
+    import torch
+    rng = np.random.default_rng(100 + shift)
+    lens = list(range(201))
+    rng.shuffle(lens)
+    offs, pool = [], bytearray()
+    for n in lens:
+        pool += b"\0" * ((-len(pool)) % 4 + shift)            # the message starts `shift` past a word
+        offs.append(len(pool))
+        pool += rng.bytes(n)
+    d_pool = torch.from_numpy(np.frombuffer(bytes(pool), np.uint8).copy()).cuda()
+    d_off = torch.tensor(offs, dtype=torch.int64, device="cuda")
+    d_len = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    out = torch.zeros((len(lens), 16), dtype=torch.uint8, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pkv.pkv_digest_batch(d_pool, d_off, d_len, out, status)
+    got = out.cpu().numpy()
+    assert int(status.item()) == 0
+    for i, (o, n) in enumerate(zip(offs, lens)):
+        assert got[i].tobytes() == oracle.sha256(bytes(pool[o:o + n]))[:16], (n, shift)
+
+
 @pytest.mark.parametrize("block", [1, 2, 3, 7, 15, 16, 17, 31, 32, 48, 64, 100, 256, 257])
 def test_derive_matches_oracle_any_block(pkv, block):
     rng = np.random.default_rng(block)
