@@ -222,6 +222,43 @@ def serial_leg(args, table, run):
             "store_ms": float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))}
 
 
+def fused_leg(args, table, run):
+    """The same steps on one stream with keys and hit lengths from one call (pkv_derive_lookup: the
+    fused derive and lookup kernel for B = 16), the call bracketed by events.  Its hit lengths must
+    equal those of the separate derive and lookup kernels (the serial pass just before)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    want = run.host_hits()
+
+    def step(ev=None):
+        run.n_new.zero_()
+        run.key_offsets()
+        run.digest()
+        if ev is not None:
+            ev[0].record(stream)
+        run.derive_lookup(table)
+        if ev is not None:
+            ev[1].record(stream)
+        run.store(table)
+        run.rollback(table)
+
+    for _ in range(args.warmup):
+        step()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    if run.host_status() != 0:
+        raise RuntimeError(f"fused step failed: status {run.host_status()}")
+    if not (run.host_hits() == want).all():
+        raise RuntimeError("fused derive-and-lookup hit lengths differ from the lookup kernel's")
+    return {"ms": (t1 - t0) * 1e3 / args.steps,
+            "derive_lookup_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))}
+
+
 def cold_leg(args, table, run, reps):
     """Per-kernel times with cold caches, outside the timed region: before every rep (untimed) the
     index is restored from a pristine device copy and a 1 GiB scratch buffer is written, which
@@ -264,6 +301,7 @@ def gpu_leg(args, w):
     from paper_2609_38706_amd.pipeline import TwoStreamRunner
     pkv, table, runs, fill = setup_gpu(args, w)
     serial = serial_leg(args, table, runs[0])
+    fused = fused_leg(args, table, runs[0])
     runner = TwoStreamRunner(table)
     order = [runs[i % 2] for i in range(max(args.steps, args.warmup))]
     runner.run(order[: args.warmup], rollback=True)
@@ -290,7 +328,7 @@ def gpu_leg(args, w):
     new_entries = int(run.n_new.item())
     cold = cold_leg(args, table, run, args.cold_reps)
     return {"probes": probes, "ms": (t1 - t0) * 1e3 / args.steps, "derive_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in evs if e is not None])),
-            "derive_timed_launches": sum(e is not None for e in evs), "serial": serial, "n_keys": run.n_keys, "n_req": run.n_req, "hit_blocks": int(hits.sum()),
+            "derive_timed_launches": sum(e is not None for e in evs), "serial": serial, "fused": fused, "n_keys": run.n_keys, "n_req": run.n_req, "hit_blocks": int(hits.sum()),
             "new_entries": new_entries, "fill": fill, "cold": cold}
 
 
@@ -759,7 +797,11 @@ def main():
         "pipeline": {"streams": 2, "overlap": "derive of step k+1 with lookup/store/rollback of step k",
                      "serial_ms_per_step": round(g["serial"]["ms"], 4),
                      "serial_value": round(g["n_keys"] / (g["serial"]["ms"] * 1e-3) / 1e9, 6),
-                     "hit_blocks": g["hit_blocks"], "new_entries": g["new_entries"]},
+                     "hit_blocks": g["hit_blocks"], "new_entries": g["new_entries"],
+                     "fused_ms_per_step": round(g["fused"]["ms"], 4),
+                     "fused_derive_lookup_ms": round(g["fused"]["derive_lookup_ms"], 4),
+                     "fused": "one stream: key offsets, digests, keys and hit lengths in one call "
+                              "(pkv_derive_lookup), store, rollback"},
         "roofline": roofline,
         "roofline_lookup": roofline_lookup,
         "roofline_store": roofline_store,

@@ -146,6 +146,20 @@ int pkv_derive_keys(const int32_t* d_tokens, uint64_t n_tokens, const int64_t* d
                     const int64_t* d_key_off, uint64_t n_keys, uint8_t* d_keys,
                     int32_t* d_status, hipStream_t stream);
 
+/* Chained block keys and their longest-prefix hits in one call (section 5.2, Eq. 3 for the keys;
+ * section 3.4 / 4.1 for the hit): the results of pkv_derive_keys followed by pkv_lookup_prefix on
+ * the keys it wrote, with the arguments, layouts and errors of those two calls (a request whose
+ * offsets are inconsistent gets no key and hit length 0).  For B = 16 and up to two lane-pair
+ * workgroups of chains per compute unit (16384 requests on 256 compute units) one kernel does both:
+ * each chain's keys are probed while its later keys are still being hashed, so the probes' memory
+ * latency hides under the hashing and no key is read back for a separate lookup pass.  Other
+ * shapes run the two kernels one after the other.  The index is only read: no store into it may
+ * overlap this call (order them on one stream). */
+int pkv_derive_lookup(const int32_t* d_tokens, uint64_t n_tokens, const int64_t* d_tok_off, uint32_t n_req,
+                      const uint8_t* d_digests, uint32_t block, const int64_t* d_key_off, uint64_t n_keys,
+                      uint8_t* d_keys, const pkv_table* table, int32_t* d_hit_blocks, int32_t* d_status,
+                      hipStream_t stream);
+
 /* Marks every slot of the index empty: the shared tier starts with no entry (section 2.1 shared
  * KV-cache tier).  Beyond the operations the paper states (digest, derive, lookup, store), the index
  * needs this set-up call, and the export and rollback below. */

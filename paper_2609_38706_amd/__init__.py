@@ -19,7 +19,7 @@ ERROR_NAMES = {0: "PKV_OK", -1: "PKV_EINVAL", -2: "PKV_EDUPDIM", -3: "PKV_ERESER
 
 EXPORTED = ["pkv_descriptor_encode", "pkv_descriptor_digest", "pkv_digest_batch", "pkv_expand_digests",
             "pkv_key_offsets",
-            "pkv_derive_keys", "pkv_table_bytes", "pkv_table_init", "pkv_lookup_prefix", "pkv_store", "pkv_table_rollback",
+            "pkv_derive_keys", "pkv_derive_lookup", "pkv_table_bytes", "pkv_table_init", "pkv_lookup_prefix", "pkv_store", "pkv_table_rollback",
             "pkv_table_export", "pkv_sum_hits", "pkv_lookup_prefix_touch", "pkv_store_touch",
             "pkv_table_evict", "pkv_tree_work_bytes", "pkv_tensor_roots", "pkv_tensor_roots_static",
             "pkv_content_identity",
@@ -62,6 +62,7 @@ def lib() -> ctypes.CDLL:
             "pkv_key_offsets": [P, U32, U32, P, P],
             "pkv_expand_digests": [P, U32, P, U32, P, P, P],
             "pkv_derive_keys": [P, U64, P, U32, P, U32, P, U64, P, P, P],
+            "pkv_derive_lookup": [P, U64, P, U32, P, U32, P, U64, P, P, P, P, P],
             "pkv_table_init": [P, P],
             "pkv_lookup_prefix": [P, P, P, U32, U64, P, P, P],
             "pkv_store": [P, P, P, U32, U64, P, P, P, P, P, P],
@@ -212,6 +213,16 @@ def pkv_lookup_prefix(table: Table, keys, key_off, hits, status, stream=None):
     _check(lib().pkv_lookup_prefix(ctypes.byref(t), _ptr(keys, torch.uint8), _ptr(key_off, torch.int64),
                                    key_off.numel() - 1, keys.numel() // 16, _ptr(hits, torch.int32),
                                    _ptr(status, torch.int32), _stream(stream)))
+
+
+def pkv_derive_lookup(tokens, tok_off, digests, block, key_off, keys, table: Table, hits, status, stream=None):
+    import torch
+    t = table.struct()
+    _check(lib().pkv_derive_lookup(_ptr(tokens, torch.int32), tokens.numel(), _ptr(tok_off, torch.int64),
+                                   tok_off.numel() - 1, _ptr(digests, torch.uint8), block,
+                                   _ptr(key_off, torch.int64), keys.numel() // 16, _ptr(keys, torch.uint8),
+                                   ctypes.byref(t), _ptr(hits, torch.int32), _ptr(status, torch.int32),
+                                   _stream(stream)))
 
 
 def pkv_store(table: Table, keys, key_off, hits, locs, n_new, status, new_slots=None, stream=None):

@@ -266,6 +266,24 @@ int pkv_derive_keys(const int32_t* d_tokens, uint64_t n_tokens, const int64_t* d
                          stream);
 }
 
+int pkv_derive_lookup(const int32_t* d_tokens, uint64_t n_tokens, const int64_t* d_tok_off, uint32_t n_req,
+                      const uint8_t* d_digests, uint32_t block, const int64_t* d_key_off, uint64_t n_keys,
+                      uint8_t* d_keys, const pkv_table* table, int32_t* d_hit_blocks, int32_t* d_status,
+                      hipStream_t stream) {
+    int rc = check_table(table, "pkv_derive_lookup");
+    if (rc) return rc;
+    if (block == 0) return set_error(PKV_EINVAL, "pkv_derive_lookup: block size 0");
+    if (n_req == 0) return PKV_OK;
+    if ((!d_tokens && n_tokens) || !d_tok_off || !d_digests || !d_key_off || (!d_keys && n_keys) || !d_hit_blocks ||
+        !d_status)
+        return set_error(PKV_EINVAL, "pkv_derive_lookup: null argument");
+    if (!aligned(d_digests, 16) || !aligned(d_keys, 16))
+        return set_error(PKV_EINVAL, "pkv_derive_lookup: digests and keys must be 16-byte aligned");
+    if (!aligned(d_tokens, 4)) return set_error(PKV_EINVAL, "pkv_derive_lookup: tokens not 4-byte aligned");
+    return launch_derive_lookup(d_tokens, n_tokens, d_tok_off, n_req, d_digests, block, d_key_off, n_keys, d_keys,
+                                table_words(table), table->capacity, d_hit_blocks, d_status, stream);
+}
+
 uint64_t pkv_table_bytes(uint64_t capacity) {
     if (!pow2(capacity) || capacity < kSlotsPerBucket || capacity > (1ull << 56)) return 0;
     return capacity * 32;

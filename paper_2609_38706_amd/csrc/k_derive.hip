@@ -34,6 +34,11 @@ struct ChainArgs {
     uint64_t n_keys;
     uint8_t* keys;
     int32_t* status;
+    // fused derive and lookup only (else null / 0): the index buckets, the bucket count - 1 and
+    // the per-request hit lengths
+    const uint4* table;
+    uint64_t bucket_mask;
+    int32_t* hits;
 };
 
 // Loads request r's bounds and checks them against the buffers; false = skip this request.
@@ -462,10 +467,88 @@ __device__ __forceinline__ void produce_key_pair(PpShared& sh, uint32_t chain, b
     pair_schedule8<24, 0>(v, pk, col);
 }
 
+// ---- fused derive and lookup: the helper probes the index while the consumer hashes ------------
+// The longest-prefix hit (section 3.4 / 4.1; the hit pkv_lookup_prefix returns) of a chain is
+// found by the helper wavefront from the keys the consumer has already produced, so no key makes
+// a second trip through HBM and every probe's memory latency hides under the rounds of later keys.
+// The two lanes of a chain's pair share the probes: the e lane probes positions 0, 2, 4, .. and
+// the a lane positions 1, 3, 5, ..  Once per key period (at the start of the long last phase) a
+// lane checks the bucket it loaded one period earlier and then loads the next one: the bucket that
+// follows when the checked one is full and neither holds the key nor a never-used slot, else the
+// home bucket of its next key.  Two lanes resolve up to two keys per period while the consumer
+// produces one, so a chain catches up after probes that continued into a following bucket.  A
+// lane stops at its first absent key, and as soon as its partner has found an absent key at a
+// smaller position; the hit length is the smaller of the two first absent positions (or the key
+// count).  The index is only read, so the caller must not store into it while this runs.
+struct PairProbe {
+    int64_t next;          // position of the lane's next unresolved key
+    int64_t miss;          // position of the lane's first absent key, else the chain's key count
+    uint64_t bucket;       // bucket of the probe in flight
+    uint64_t visited;      // buckets the probe in flight has checked
+    uint4 key;             // key of the probe in flight
+    uint4 c[4], p[4];      // its bucket: each slot's {claim word, tag} and {key bytes 8..15, location}
+    bool pend;             // a probe is in flight
+};
+
+__device__ __forceinline__ void probe_load(const ChainArgs& a, PairProbe& pr) {
+    const uint4* q = a.table + pr.bucket * (kBucketWords / 2);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        pr.c[j] = q[2 * j];
+        pr.p[j] = q[2 * j + 1];
+    }
+}
+
+// The first absent position known to the pair (every lane of the wavefront calls this together).
+__device__ __forceinline__ int64_t pair_miss(const PairProbe& pr) {
+    const uint64_t m = static_cast<uint64_t>(pr.miss);
+    const uint64_t other = (static_cast<uint64_t>(lane_swap(static_cast<uint32_t>(m >> 32))) << 32) |
+                           lane_swap(static_cast<uint32_t>(m));
+    const int64_t o = static_cast<int64_t>(other);
+    return o < pr.miss ? o : pr.miss;
+}
+
+// One probe point.  Keys 0 .. avail - 1 of the chain exist; `newest` is key period - 1 (the one
+// the helper read from LDS this period), every older key is read back from the key array, which
+// the consumer wrote at least one workgroup barrier earlier.
+__device__ __forceinline__ void probe_point(const ChainArgs& a, PairProbe& pr, int64_t k0, int64_t avail,
+                                            int64_t period, uint4 newest) {
+    if (pr.pend) {
+        const dev::KeyWords kw = dev::key_words(pr.key);
+        bool hit = false, empty = false;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            hit |= dev::slot_holds(pr.c[j], pr.p[j], kw);
+            empty |= dev::slot_never_used(pr.c[j]);
+        }
+        ++pr.visited;
+        if (hit) {
+            pr.next += 2;
+            pr.pend = false;
+        } else if (empty || pr.visited > a.bucket_mask) {    // a never-used slot, or every bucket checked
+            pr.miss = pr.next;
+            pr.pend = false;
+        } else {
+            pr.bucket = (pr.bucket + 1) & a.bucket_mask;
+            probe_load(a, pr);
+        }
+    }
+    const int64_t lim = pair_miss(pr);
+    if (!pr.pend && pr.next < lim && pr.next < avail) {
+        uint4 k = newest;
+        if (pr.next != period - 1) k = reinterpret_cast<const uint4*>(a.keys)[k0 + pr.next];
+        pr.key = k;
+        pr.bucket = dev::home_bucket(pr.key, a.bucket_mask);
+        pr.visited = 0;
+        probe_load(a, pr);
+        pr.pend = true;
+    }
+}
+
 // P consumer/helper pairs per workgroup (P = 2 puts two consumers on one compute unit, each on its
 // own SIMD, when there are enough chains for that); every barrier is workgroup-wide, so all pairs
-// run the same number of keys.
-template <int P>
+// run the same number of keys.  FUSED: the helper also finds each chain's hit length (above).
+template <int P, bool FUSED>
 __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
     __shared__ PpShared sh_pairs[P];
     __shared__ int64_t pair_n[2 * P];
@@ -551,6 +634,12 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
         uint32_t* kw1hi_col = reinterpret_cast<uint32_t*>(&sh.kw1hi[0][c]) + (odd ? 1 : 0);
         const PairK pk = make_pair_k(odd);
         uint32_t tk[8], pre[8];
+        PairProbe pr;
+        if (FUSED) {
+            pr.next = odd ? 1 : 0;
+            pr.miss = n;
+            pr.pend = false;
+        }
         load_tokens_pair(tp, 0, n, odd, tk);
         load_tokens_pair(tp, 1, n, odd, pre);
         produce_key_pair(sh, c, odd, pk, 0, tk);
@@ -574,11 +663,23 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             __syncthreads();
             pair_schedule8<24>(v, pk, kw1hi_col);
             __syncthreads();
+            if (FUSED) {                                       // keys 0 .. i - 1 exist; pv is key i - 1
+                const uint4 newest = make_uint4(bswap(pv[0]), bswap(pv[1]), bswap(pv[2]), bswap(pv[3]));
+                probe_point(a, pr, k0, i < n ? i : n, i, newest);
+            }
 #pragma unroll
             for (int q = 0; q < 8; ++q) tk[q] = pre[q];        // the next key's token-only data
             load_tokens_pair(tp, i + 2, n, odd, pre);
             produce_key_pair(sh, c, odd, pk, buf ^ 1, tk);
             __syncthreads();                                   // end of key
+        }
+        if (FUSED) {
+            // every key exists now; finish the probes still open (the exit test is wave-wide, as
+            // each probe point exchanges values between the lanes of a pair)
+            const uint4 none = make_uint4(0u, 0u, 0u, 0u);
+            while (__ballot(pr.pend || pr.next < pair_miss(pr)) != 0) probe_point(a, pr, k0, n, nmax + 1, none);
+            const int64_t h = pair_miss(pr);
+            if (odd && r < a.n_req) a.hits[r] = static_cast<int32_t>(h);
         }
     }
 }
@@ -1452,9 +1553,9 @@ int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_o
     const unsigned pp_grid = (n_req + kPpChains - 1) / kPpChains;
     const unsigned pp2_grid = (n_req + 2 * kPpChains - 1) / (2 * kPpChains);
     if (block == 16 && pp_grid <= static_cast<unsigned>(compute_units())) {
-        hipLaunchKernelGGL(k_derive_b16_pp<1>, dim3(pp_grid), dim3(kPcThreads), 0, s, a);
+        hipLaunchKernelGGL((k_derive_b16_pp<1, false>), dim3(pp_grid), dim3(kPcThreads), 0, s, a);
     } else if (block == 16 && pp2_grid <= static_cast<unsigned>(compute_units())) {
-        hipLaunchKernelGGL(k_derive_b16_pp<2>, dim3(pp2_grid), dim3(2 * kPcThreads), 0, s, a);
+        hipLaunchKernelGGL((k_derive_b16_pp<2, false>), dim3(pp2_grid), dim3(2 * kPcThreads), 0, s, a);
     } else if (block == 16) {
         hipLaunchKernelGGL(k_derive_b16, grid, dim3(kDeriveThreads), 0, s, a);
     } else if (block % 16 == 0 && pp_grid <= static_cast<unsigned>(compute_units())) {
@@ -1467,6 +1568,31 @@ int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_o
         hipLaunchKernelGGL(k_derive_any, grid, dim3(kDeriveThreads), 0, s, a);
     }
     return check_launch("pkv_derive_keys");
+}
+
+// Keys and hit lengths in one kernel where the lane-pair kernel runs the chains (B = 16, at most two
+// lane-pair workgroups' chains per compute unit); otherwise the derive and the lookup kernels one
+// after the other on the stream.
+int launch_derive_lookup(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_off, uint32_t n_req,
+                         const uint8_t* digests, uint32_t block, const int64_t* key_off, uint64_t n_keys,
+                         uint8_t* keys, const uint64_t* table, uint64_t capacity, int32_t* hits, int32_t* status,
+                         hipStream_t s) {
+    if (n_req == 0) return PKV_OK;
+    const unsigned pp_grid = (n_req + kPpChains - 1) / kPpChains;
+    const unsigned pp2_grid = (n_req + 2 * kPpChains - 1) / (2 * kPpChains);
+    const unsigned cus = static_cast<unsigned>(compute_units());
+    if (block != 16 || pp2_grid > cus) {
+        const int rc = launch_derive(tokens, n_tokens, tok_off, n_req, digests, block, key_off, n_keys, keys, status, s);
+        if (rc) return rc;
+        return launch_lookup(table, capacity, keys, key_off, n_req, n_keys, hits, nullptr, 0, status, s);
+    }
+    ChainArgs a{tokens, n_tokens, tok_off, n_req, digests, block, key_off, n_keys, keys, status,
+                reinterpret_cast<const uint4*>(table), capacity / kSlotsPerBucket - 1, hits};
+    if (pp_grid <= cus)
+        hipLaunchKernelGGL((k_derive_b16_pp<1, true>), dim3(pp_grid), dim3(kPcThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL((k_derive_b16_pp<2, true>), dim3(pp2_grid), dim3(2 * kPcThreads), 0, s, a);
+    return check_launch("pkv_derive_lookup");
 }
 
 int launch_digest_batch(const uint8_t* bytes, uint64_t n_bytes, const int64_t* off, const uint32_t* len, uint32_t n,

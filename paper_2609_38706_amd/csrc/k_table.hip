@@ -28,7 +28,11 @@ namespace {
 
 using dev::eq4;
 using dev::home_bucket;
+using dev::key_words;
+using dev::KeyWords;
 using dev::report;
+using dev::slot_holds;
+using dev::slot_never_used;
 
 constexpr uint32_t kWaitLimit = 1u << 20;      // re-reads of one claimed slot before giving up
 
@@ -47,21 +51,6 @@ __device__ __forceinline__ void store_relaxed(uint64_t* p, uint64_t v) {
 }
 
 __device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
-
-// The two 8-byte halves of a key as little-endian words, and the claim and flag words that stand
-// for its first half in a slot.
-struct KeyWords {
-    uint64_t lo, hi;
-    uint64_t claim, flag;
-};
-__device__ __forceinline__ KeyWords key_words(const uint4& k) {
-    KeyWords w;
-    w.lo = (static_cast<uint64_t>(k.y) << 32) | k.x;
-    w.hi = (static_cast<uint64_t>(k.w) << 32) | k.z;
-    w.flag = w.lo == kLoEmpty ? 1u : (w.lo == kLoRemoved ? 2u : 0u);
-    w.claim = w.flag ? kLoSub : w.lo;
-    return w;
-}
 
 // A key's probe path visits its home bucket and then the following buckets (wrapping), each bucket's
 // four slots in the order rot, rot + 1, rot + 2, rot + 3 (mod 4), where rot is two bits of the key's
@@ -142,14 +131,8 @@ __device__ __forceinline__ int64_t probe_key(const uint4* __restrict__ t, uint64
         bool empty = false;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint64_t claim = (static_cast<uint64_t>(bk.c[j].y) << 32) | bk.c[j].x;
-            const uint32_t flag = bk.c[j].z & 3u;
-            const uint64_t hi = (static_cast<uint64_t>(bk.p[j].y) << 32) | bk.p[j].x;
-            const uint64_t loc = (static_cast<uint64_t>(bk.p[j].w) << 32) | bk.p[j].z;
-            const uint64_t s = b * kSlotsPerBucket + j;
-            if (claim == kw.claim && hi == kw.hi && loc != kEmpty && (kw.claim != kLoSub || flag == kw.flag))
-                return static_cast<int64_t>(s);
-            empty |= claim == kLoEmpty;
+            if (slot_holds(bk.c[j], bk.p[j], kw)) return static_cast<int64_t>(b * kSlotsPerBucket + j);
+            empty |= slot_never_used(bk.c[j]);
         }
         if (empty) return -1;
         b = (b + 1) & bmask;

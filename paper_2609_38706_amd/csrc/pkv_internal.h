@@ -123,6 +123,34 @@ __device__ __forceinline__ uint64_t home_bucket(const uint4& k, uint64_t bucket_
     return ((static_cast<uint64_t>(k.y) << 32) | k.x) & bucket_mask;
 }
 
+// The two 8-byte halves of a key as little-endian words, and the claim and flag words that stand
+// for its first half in a slot.
+struct KeyWords {
+    uint64_t lo, hi;
+    uint64_t claim, flag;
+};
+__device__ __forceinline__ KeyWords key_words(const uint4& k) {
+    KeyWords w;
+    w.lo = (static_cast<uint64_t>(k.y) << 32) | k.x;
+    w.hi = (static_cast<uint64_t>(k.w) << 32) | k.z;
+    w.flag = w.lo == kLoEmpty ? 1u : (w.lo == kLoRemoved ? 2u : 0u);
+    w.claim = w.flag ? kLoSub : w.lo;
+    return w;
+}
+
+// Slot j (0..3) of a bucket as read by a lookup: its {claim word, tag} and {key bytes 8..15,
+// location} halves.  The key is in the slot when the claim word (and, under a substitute claim
+// word, the flag) and key bytes 8..15 agree and the location is published.
+__device__ __forceinline__ bool slot_holds(const uint4& ct, const uint4& pr, const KeyWords& kw) {
+    const uint64_t claim = (static_cast<uint64_t>(ct.y) << 32) | ct.x;
+    const uint64_t hi = (static_cast<uint64_t>(pr.y) << 32) | pr.x;
+    const uint64_t loc = (static_cast<uint64_t>(pr.w) << 32) | pr.z;
+    return claim == kw.claim && hi == kw.hi && loc != kEmpty && (kw.claim != kLoSub || (ct.z & 3u) == kw.flag);
+}
+__device__ __forceinline__ bool slot_never_used(const uint4& ct) {
+    return ((static_cast<uint64_t>(ct.y) << 32) | ct.x) == kLoEmpty;
+}
+
 }  // namespace dev
 
 // ---- launchers (defined next to their kernels; return a PKV_* code) ------------------------
@@ -135,6 +163,10 @@ int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_o
                   const uint8_t* digests, uint32_t block, const int64_t* key_off, uint64_t n_keys,
                   uint8_t* keys, int32_t* status, hipStream_t s);
 int launch_table_init(uint64_t* table, uint64_t capacity, hipStream_t s);
+int launch_derive_lookup(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_off, uint32_t n_req,
+                         const uint8_t* digests, uint32_t block, const int64_t* key_off, uint64_t n_keys,
+                         uint8_t* keys, const uint64_t* table, uint64_t capacity, int32_t* hits, int32_t* status,
+                         hipStream_t s);
 int launch_lookup(const uint64_t* table, uint64_t capacity, const uint8_t* keys, const int64_t* key_off,
                   uint32_t n_req, uint64_t n_keys, int32_t* hits, uint32_t* epochs, uint32_t epoch, int32_t* status,
                   hipStream_t s);

@@ -13,7 +13,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import (Table, pkv_derive_keys, pkv_descriptor_encode, pkv_digest_batch, pkv_expand_digests,
+from . import (Table, pkv_derive_keys, pkv_derive_lookup, pkv_descriptor_encode, pkv_digest_batch, pkv_expand_digests,
                pkv_key_offsets, pkv_lookup_prefix, pkv_store, pkv_table_export, pkv_table_rollback)
 
 
@@ -88,6 +88,11 @@ class DeviceBatch:
     def lookup(self, table: Table, stream=None):
         pkv_lookup_prefix(table, self.keys, self.key_off, self.hits[: max(1, self.n_req)], self.status, stream)
 
+    def derive_lookup(self, table: Table, stream=None):
+        """Keys and hit lengths in one call (the fused kernel where it applies)."""
+        pkv_derive_lookup(self.tokens, self.tok_off, self.digests[: max(1, self.n_req)], self.block, self.key_off,
+                          self.keys, table, self.hits[: max(1, self.n_req)], self.status, stream)
+
     def store(self, table: Table, stream=None, log=True):
         pkv_store(table, self.keys, self.key_off, self.hits[: max(1, self.n_req)], self.locs, self.n_new,
                   self.status, self.new_slots if log else None, stream)
@@ -101,6 +106,13 @@ class DeviceBatch:
         self.digest(stream)
         self.derive(stream)
         self.lookup(table, stream)
+        self.store(table, stream)
+
+    def step_fused(self, table: Table, stream=None):
+        """The same pass with keys and hit lengths from one call."""
+        self.key_offsets(stream)
+        self.digest(stream)
+        self.derive_lookup(table, stream)
         self.store(table, stream)
 
     # ---- host views (synchronizing) ----------------------------------------------------------
