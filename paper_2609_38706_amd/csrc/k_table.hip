@@ -202,9 +202,13 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
 }
 
 // ---- store ------------------------------------------------------------------------------------
-// One lane per key of the batch; candidate = key j of request r with j >= hits[r].  A wavefront
-// covers 64 consecutive keys: one (wave-uniform) binary search finds the request of its first
-// key, and each lane walks forward over the few request boundaries inside the wavefront.
+// One lane per candidate key at a time (candidate = key j of request r with j >= hits[r]).  A
+// wavefront owns kStoreKeysPerLane x 64 consecutive keys, lane l the keys l, l + 64, l + 128, ..
+// of them, and a lane moves on to its next candidate as soon as the current one is inserted or
+// found.  One key per lane measured fastest (c4 store alone 0.302 ms against 0.318 / 0.347 ms with
+// two / four): fewer, longer wavefronts lose more beside the derive than their busier lanes gain.
+// One (wave-uniform) search finds the request of the wavefront's first key, and each lane walks
+// forward over the request boundaries it meets.
 struct StoreArgs {
     Tab t;
     const uint4* keys;
@@ -221,10 +225,14 @@ struct StoreArgs {
     int32_t* status;
 };
 
-__device__ __forceinline__ bool candidate(const StoreArgs& a, uint64_t wave_base, uint64_t k, int64_t total) {
-    // largest r < n_req with key_off[r] <= wave_base: start where equal-length requests would put
-    // it, widen by doubling steps until [lo, hi) brackets it, then bisect (a batch of equal
-    // lengths needs two loads instead of log2(n_req)); key_off[0] = 0 <= wave_base always
+constexpr uint32_t kStoreThreads = 256;
+constexpr uint32_t kStoreKeysPerLane = 1;
+constexpr uint32_t kStoreWaveKeys = 64 * kStoreKeysPerLane;
+
+// The largest r < n_req with key_off[r] <= wave_base (key_off[0] = 0 <= wave_base always): start
+// where equal-length requests would put it, widen by doubling steps until [lo, hi) brackets it, then
+// bisect (a batch of equal lengths needs two loads instead of log2(n_req)).
+__device__ __forceinline__ uint32_t first_request(const StoreArgs& a, uint64_t wave_base, int64_t total) {
     const int64_t wb = static_cast<int64_t>(wave_base);
     const uint64_t n = a.n_req;
     uint64_t lo = 0, hi = n;
@@ -247,18 +255,69 @@ __device__ __forceinline__ bool candidate(const StoreArgs& a, uint64_t wave_base
         const uint64_t mid = (lo + hi) >> 1;
         if (a.key_off[mid] <= wb) lo = mid; else hi = mid;
     }
-    if (static_cast<int64_t>(k) >= total) return false;
-    uint32_t r = static_cast<uint32_t>(lo);
-    while (r + 1 < a.n_req && a.key_off[r + 1] <= static_cast<int64_t>(k)) ++r;
-    const int64_t j = static_cast<int64_t>(k) - a.key_off[r];
-    int64_t h = a.hits[r];
-    if (h < 0) h = 0;
-    return j >= h;
+    return static_cast<uint32_t>(lo);
 }
 
-__device__ __forceinline__ uint64_t wave_base_of(uint32_t block_threads) {
-    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    return static_cast<uint64_t>(blockIdx.x) * block_threads + wave * 64ull;
+// The probe of a lane's current candidate.
+struct StoreProbe {
+    KeyWords kw;
+    uint64_t want;             // its location
+    uint64_t rot;              // path rotation inside each bucket
+    uint64_t p;                // path position
+    uint64_t steps;            // slots passed in the current phase
+    uint64_t first_free;       // position of the first removed slot met while scanning, or ~0
+    uint32_t waits;
+    bool scanning;             // phase 1: the key may still sit further along its path
+};
+
+// Which of the lane's keys (bit q: key wave_base + 64 q + lane) are candidates.  Computed before
+// the probe loop, so that no load in the loop waits for anything but the last memory operation.
+__device__ __forceinline__ uint32_t lane_candidates(const StoreArgs& a, uint64_t wave_base, int64_t total,
+                                                    uint32_t lane) {
+    if (static_cast<int64_t>(wave_base) >= total) return 0;
+    uint32_t r = first_request(a, wave_base, total);
+    uint32_t mask = 0;
+#pragma unroll
+    for (uint32_t q = 0; q < kStoreKeysPerLane; ++q) {
+        const uint64_t k = wave_base + 64ull * q + lane;
+        if (static_cast<int64_t>(k) >= total) break;
+        while (r + 1 < a.n_req && a.key_off[r + 1] <= static_cast<int64_t>(k)) ++r;
+        const int64_t j = static_cast<int64_t>(k) - a.key_off[r];
+        int64_t h = a.hits[r];
+        if (h < 0) h = 0;
+        if (j >= h) mask |= 1u << q;
+    }
+    return mask;
+}
+
+// Moves the lane to its next candidate (the lowest bit of *cands, which it clears); true with the
+// probe set up at the key's home bucket, false when none is left.  The key and its location are
+// loaded together and both waited for at once: the wait then covers every memory operation in
+// flight, which the publication store that may precede it requires.
+__device__ __forceinline__ bool next_candidate(const StoreArgs& a, uint64_t wave_base, uint32_t lane, uint32_t& cands,
+                                               StoreProbe& st) {
+    while (cands) {
+        const uint32_t q = __builtin_ctz(cands);
+        cands &= cands - 1;
+        const uint64_t k = wave_base + 64ull * q + lane;
+        const uint64_t loc = a.locs[k];
+        const uint4 key = a.keys[k];
+        asm volatile("" : : "v"(loc), "v"(key.x), "v"(key.y), "v"(key.z), "v"(key.w));
+        if (loc >= PKV_LOC_LIMIT) {
+            report(a.status, PKV_ERESERVED);
+            continue;
+        }
+        st.kw = key_words(key);
+        st.want = loc;
+        st.rot = path_rotation(st.kw);
+        st.p = home_bucket(key, (a.t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
+        st.steps = 0;
+        st.first_free = ~0ull;
+        st.waits = 0;
+        st.scanning = true;
+        return true;
+    }
+    return false;
 }
 
 // The pair of a slot whose claim word matched and whose location word is published.  The pair is
@@ -281,120 +340,111 @@ __device__ __forceinline__ void publish_slot(const Tab& t, uint64_t s, const Key
     store_pair_coherent(t.pair(s), kw.hi, v);
 }
 
-constexpr uint32_t kStoreThreads = 256;
-
 __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
-    const uint64_t wave_base = wave_base_of(kStoreThreads);
-    const uint64_t k = wave_base + lane_id();
+    __shared__ uint64_t log_slots[kStoreThreads * kStoreKeysPerLane];   // the workgroup's new slots
+    __shared__ uint32_t log_n, waves_done;
+    const uint32_t lane = lane_id();
+    const uint64_t wave_base = static_cast<uint64_t>(blockIdx.x) * (kStoreThreads * kStoreKeysPerLane) +
+                               __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * static_cast<uint64_t>(kStoreWaveKeys);
     const int64_t total = a.key_off[a.n_req];
     if (total < 0 || static_cast<uint64_t>(total) > a.n_keys) {
-        if (k == 0) report(a.status, PKV_ELAYOUT);
+        if (blockIdx.x == 0 && threadIdx.x == 0) report(a.status, PKV_ELAYOUT);
         return;
     }
-    const Tab& t = a.t;
-    bool active = candidate(a, wave_base, k, total);
-    uint64_t want = 0;
-    uint4 key = make_uint4(0, 0, 0, 0);
-    if (active) {
-        const uint64_t loc = a.locs[k];
-        if (loc >= PKV_LOC_LIMIT) {
-            report(a.status, PKV_ERESERVED);
-            active = false;
-        }
-        want = loc;
-        key = a.keys[k];
-    }
-    bool claimed = false;
-    uint64_t my_slot = 0;
-    if (active) {
-        const KeyWords kw = key_words(key);
-        const uint64_t slot_mask = t.capacity - 1;
-        const uint64_t rot = path_rotation(kw);
-        uint64_t p = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;   // path position
-        uint64_t steps = 0, first_free = ~0ull;  // slots passed in the current phase; first removed slot's position
-        uint32_t waits = 0;
-        bool scanning = true;                    // phase 1: the key may still sit further along
-        while (true) {
-            const uint64_t s = path_slot(p, rot);
-            const uint64_t c = load_relaxed(t.lo(s));
-            if (c == kLoEmpty || c == kLoRemoved) {
-                bool claim = !scanning;
-                if (scanning && c == kLoEmpty) {     // a never-used slot ends the path: the key is absent
-                    scanning = false;
-                    steps = 0;
-                    if (first_free != ~0ull) {       // claim the first removed slot on the path instead
-                        p = first_free;
-                        continue;
-                    }
-                    claim = true;
-                }
-                if (claim) {
-                    if (cas_relaxed(t.lo(s), c, kw.claim)) {
-                        publish_slot(t, s, kw, a.generation, want);
-                        if (a.epochs) a.epochs[s] = a.epoch;
-                        claimed = true;
-                        my_slot = s | (c == kLoRemoved ? kFromRemoved : 0);
-                        break;
-                    }
-                    continue;                        // lost the race: read the slot again
-                }
-                if (first_free == ~0ull) first_free = p;   // a removed slot met while scanning
-            } else if (c == kw.claim) {
-                uint64_t hi, loc;
-                read_published_pair(t.pair(s), hi, loc);
-                if (loc == kEmpty) {                 // claimed, not yet published: read it again
-                    if (++waits >= kWaitLimit) { report(a.status, PKV_ESTALL); break; }
-                    continue;
-                }
-                if (hi == kw.hi) {
-                    // the tag tells a substitute claim word's key apart and whether this call
-                    // inserted the entry; it is only needed for those two questions
-                    const bool need_tag = kw.claim == kLoSub || want < loc;
-                    const uint64_t tag = need_tag ? load_relaxed(t.tag(s)) : 0;
-                    if (need_tag && tag == 0) {          // published, tag not landed yet: read it again
-                        if (++waits >= kWaitLimit) { report(a.status, PKV_ESTALL); break; }
-                        continue;
-                    }
-                    if (kw.claim != kLoSub || (tag & 3) == kw.flag) {
-                        if (want < loc && (tag >> 2) == a.generation) min_relaxed(t.loc(s), want);
-                        if (a.epochs) a.epochs[s] = a.epoch;
-                        break;
-                    }
-                }
-            }
-            p = (p + 1) & slot_mask;
-            if (++steps >= t.capacity) {         // a whole cycle
-                if (scanning && first_free != ~0ull) {
-                    scanning = false;
-                    steps = 0;
-                    p = first_free;
-                    continue;
-                }
-                report(a.status, PKV_EFULL);
-                break;
-            }
-        }
-    }
-    // one counter update per workgroup (every lane of the workgroup gets here); slot log in lane order
-    __shared__ uint32_t wave_claims[kStoreThreads / 64];
-    __shared__ uint64_t group_base;
-    const uint64_t mask = __ballot(claimed);
-    const uint32_t lane = lane_id(), wave = threadIdx.x >> 6;
-    if (lane == 0) wave_claims[wave] = static_cast<uint32_t>(__popcll(mask));
-    __syncthreads();
     if (threadIdx.x == 0) {
-        uint64_t total_claims = 0;
-        for (uint32_t w = 0; w < kStoreThreads / 64; ++w) total_claims += wave_claims[w];
-        group_base = total_claims ? __hip_atomic_fetch_add(a.n_new, total_claims, __ATOMIC_RELAXED,
-                                                           __HIP_MEMORY_SCOPE_AGENT)
-                                  : 0;
+        log_n = 0;
+        waves_done = 0;
     }
     __syncthreads();
-    if (claimed && a.new_slots) {
-        uint64_t pos = group_base + __popcll(mask & ((1ull << lane) - 1));
-        for (uint32_t w = 0; w < wave; ++w) pos += wave_claims[w];
-        if (pos < a.n_keys) a.new_slots[pos] = my_slot;
-        else report(a.status, PKV_ELAYOUT);
+    const Tab& t = a.t;
+    const uint64_t slot_mask = t.capacity - 1;
+    uint32_t cands = lane_candidates(a, wave_base, total, lane);
+    StoreProbe st;
+    bool live = next_candidate(a, wave_base, lane, cands, st);
+    while (live) {
+        const uint64_t s = path_slot(st.p, st.rot);
+        const uint64_t c = load_relaxed(t.lo(s));
+        bool advance = false, done = false, fail = false;
+        if (c == kLoEmpty || c == kLoRemoved) {
+            bool try_claim = !st.scanning;
+            if (st.scanning && c == kLoEmpty) {            // a never-used slot ends the path: the key is absent
+                st.scanning = false;
+                st.steps = 0;
+                if (st.first_free != ~0ull) st.p = st.first_free;   // claim the first removed slot on the path instead
+                else try_claim = true;
+            } else if (st.scanning) {                       // a removed slot met while scanning
+                if (st.first_free == ~0ull) st.first_free = st.p;
+                advance = true;
+            }
+            if (try_claim && cas_relaxed(t.lo(s), c, st.kw.claim)) {
+                publish_slot(t, s, st.kw, a.generation, st.want);
+                if (a.epochs) a.epochs[s] = a.epoch;
+                log_slots[atomicAdd(&log_n, 1u)] = s | (c == kLoRemoved ? kFromRemoved : 0);
+                done = true;
+            }                                               // a lost race reads the slot again
+        } else if (c == st.kw.claim) {
+            uint64_t hi, loc;
+            read_published_pair(t.pair(s), hi, loc);
+            if (loc == kEmpty) {                            // claimed, not yet published: read it again
+                if (++st.waits >= kWaitLimit) { report(a.status, PKV_ESTALL); fail = true; }
+            } else if (hi == st.kw.hi) {
+                // the tag tells a substitute claim word's key apart and whether this call inserted
+                // the entry; it is only needed for those two questions
+                const bool need_tag = st.kw.claim == kLoSub || st.want < loc;
+                const uint64_t tag = need_tag ? load_relaxed(t.tag(s)) : 0;
+                if (need_tag && tag == 0) {                 // published, tag not landed yet: read it again
+                    if (++st.waits >= kWaitLimit) { report(a.status, PKV_ESTALL); fail = true; }
+                } else if (st.kw.claim != kLoSub || (tag & 3) == st.kw.flag) {
+                    if (st.want < loc && (tag >> 2) == a.generation) min_relaxed(t.loc(s), st.want);
+                    if (a.epochs) a.epochs[s] = a.epoch;
+                    done = true;
+                } else {
+                    advance = true;
+                }
+            } else {
+                advance = true;
+            }
+        } else {
+            advance = true;                                 // another key
+        }
+        if (advance) {
+            st.p = (st.p + 1) & slot_mask;
+            if (++st.steps >= t.capacity) {                 // a whole cycle
+                if (st.scanning && st.first_free != ~0ull) {
+                    st.scanning = false;
+                    st.steps = 0;
+                    st.p = st.first_free;
+                } else {
+                    report(a.status, PKV_EFULL);
+                    fail = true;
+                }
+            }
+        }
+        if (fail) {
+            live = false;                                   // the call has failed: this lane stops
+        } else if (done) {
+            live = next_candidate(a, wave_base, lane, cands, st);
+        }
+    }
+    // One counter update per workgroup, by its last wavefront to finish: the others leave at once
+    // instead of waiting at a barrier (beside other kernels, a workgroup's wavefronts can finish far
+    // apart).  The slot log goes out in the order the lanes claimed.
+    uint32_t rank = 0;
+    if (lane == 0)
+        rank = __hip_atomic_fetch_add(&waves_done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+    rank = __shfl(rank, 0);
+    if (rank != kStoreThreads / 64 - 1) return;
+    const uint32_t n_log = __hip_atomic_load(&log_n, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    uint64_t base = 0;
+    if (lane == 0 && n_log)
+        base = __hip_atomic_fetch_add(a.n_new, static_cast<uint64_t>(n_log), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    base = __shfl(base, 0);
+    if (a.new_slots) {
+        for (uint32_t i = lane; i < n_log; i += 64) {
+            const uint64_t pos = base + i;
+            if (pos < a.n_keys) a.new_slots[pos] = log_slots[i];
+            else report(a.status, PKV_ELAYOUT);
+        }
     }
 }
 
@@ -695,7 +745,7 @@ int launch_store(uint64_t* table, uint64_t capacity, const uint8_t* keys, const 
                  uint64_t n_keys, const int32_t* hits, const uint64_t* locs, uint64_t* new_slots, uint64_t* n_new,
                  uint32_t* epochs, uint32_t epoch, int32_t* status, hipStream_t s) {
     if (n_req == 0 || n_keys == 0) return PKV_OK;
-    const uint64_t blocks = (n_keys + kStoreThreads - 1) / kStoreThreads;
+    const uint64_t blocks = (n_keys + kStoreThreads * kStoreKeysPerLane - 1) / (kStoreThreads * kStoreKeysPerLane);
     if (blocks > 0x7fffffffull) return set_error(PKV_EINVAL, "pkv_store: too many keys (%llu)",
                                                  static_cast<unsigned long long>(n_keys));
     StoreArgs a{Tab{table, capacity}, reinterpret_cast<const uint4*>(keys), key_off, n_req, n_keys, hits, locs,
