@@ -1469,20 +1469,31 @@ __device__ __forceinline__ int64_t block_exclusive(int64_t mine, int64_t* wave_s
     return wave_base + incl - mine;
 }
 
+// len / block rounded toward zero, as C's integer division gives it; a power-of-two block (shift >=
+// 0 is its log2) takes a shift of the magnitude instead of a 64-bit division.
+__device__ __forceinline__ int64_t blocks_of(int64_t len, uint32_t block, int shift) {
+    if (shift < 0) return len / block;
+    const uint64_t m = len < 0 ? 0ull - static_cast<uint64_t>(len) : static_cast<uint64_t>(len);
+    const int64_t q = static_cast<int64_t>(m >> shift);
+    return len < 0 ? -q : q;
+}
+
 // Chunk blockIdx.x: key_off[r + 1] = sum of floor(len_q / B) over the chunk's requests q <= r.
 __global__ __launch_bounds__(kScanThreads) void k_key_offsets(const int64_t* tok_off, uint32_t n_req, uint32_t block,
-                                                             int64_t* key_off) {
+                                                             int shift, int64_t* key_off) {
     __shared__ int64_t wave_sum[kScanThreads / 64];
     const uint32_t tid = threadIdx.x;
     if (blockIdx.x == 0 && tid == 0) key_off[0] = 0;
     const uint64_t base = static_cast<uint64_t>(blockIdx.x) * kScanChunk;
+    const uint64_t r0 = base + static_cast<uint64_t>(tid) * kScanPerThread;
+    int64_t t[kScanPerThread + 1];               // the thread's request boundaries, all loaded at once
+#pragma unroll
+    for (int j = 0; j <= kScanPerThread; ++j) t[j] = r0 + j <= n_req ? tok_off[r0 + j] : 0;
     int64_t v[kScanPerThread];
     int64_t mine = 0;
 #pragma unroll
     for (int j = 0; j < kScanPerThread; ++j) {
-        const uint64_t r = base + static_cast<uint64_t>(tid) * kScanPerThread + j;
-        int64_t c = 0;
-        if (r < n_req) c = (tok_off[r + 1] - tok_off[r]) / block;
+        const int64_t c = r0 + j < n_req ? blocks_of(t[j + 1] - t[j], block, shift) : 0;
         v[j] = c;
         mine += c;
     }
@@ -1614,8 +1625,9 @@ int launch_expand_digests(const uint8_t* desc_digests, uint32_t n_desc, const ui
 
 int launch_key_offsets(const int64_t* tok_off, uint32_t n_req, uint32_t block, int64_t* key_off, hipStream_t s) {
     const uint64_t n_chunks = (static_cast<uint64_t>(n_req) + kScanChunk - 1) / kScanChunk;
+    const int shift = (block & (block - 1)) == 0 ? __builtin_ctz(block) : -1;
     hipLaunchKernelGGL(k_key_offsets, dim3(n_chunks ? static_cast<unsigned>(n_chunks) : 1u), dim3(kScanThreads), 0, s,
-                       tok_off, n_req, block, key_off);
+                       tok_off, n_req, block, shift, key_off);
     if (n_chunks > 1) {
         hipLaunchKernelGGL(k_key_offsets_carry, dim3(1), dim3(kScanThreads), 0, s, n_req, key_off);
         hipLaunchKernelGGL(k_key_offsets_add, dim3(static_cast<unsigned>(n_chunks - 1)), dim3(256), 0, s, n_req,
