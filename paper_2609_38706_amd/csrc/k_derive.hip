@@ -1479,31 +1479,53 @@ __device__ __forceinline__ int64_t blocks_of(int64_t len, uint32_t block, int sh
 }
 
 // Chunk blockIdx.x: key_off[r + 1] = sum of floor(len_q / B) over the chunk's requests q <= r.
+// The chunk's requests are cut into runs of 64 consecutive ones (lane l takes request l of a run),
+// so every load and store of a run is one coalesced 512-byte access; each wavefront scans `runs`
+// consecutive runs (as few as cover the chunk, so a small batch spreads over the wavefronts
+// instead of queueing on one), chaining their totals, and the wavefronts' totals chain across the
+// workgroup.
 __global__ __launch_bounds__(kScanThreads) void k_key_offsets(const int64_t* tok_off, uint32_t n_req, uint32_t block,
                                                              int shift, int64_t* key_off) {
     __shared__ int64_t wave_sum[kScanThreads / 64];
-    const uint32_t tid = threadIdx.x;
+    const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     if (blockIdx.x == 0 && tid == 0) key_off[0] = 0;
-    const uint64_t base = static_cast<uint64_t>(blockIdx.x) * kScanChunk;
-    const uint64_t r0 = base + static_cast<uint64_t>(tid) * kScanPerThread;
-    int64_t t[kScanPerThread + 1];               // the thread's request boundaries, all loaded at once
+    const uint64_t c0 = static_cast<uint64_t>(blockIdx.x) * kScanChunk;
+    const uint64_t in_chunk = n_req - c0 < kScanChunk ? n_req - c0 : kScanChunk;
+    const uint32_t runs = static_cast<uint32_t>((in_chunk + 64 * (kScanThreads / 64) - 1) / (64 * (kScanThreads / 64)));
+    const uint64_t r0 = c0 + static_cast<uint64_t>(wave) * 64 * runs;
+    int64_t lo[kScanPerThread], hi[kScanPerThread];
 #pragma unroll
-    for (int j = 0; j <= kScanPerThread; ++j) t[j] = r0 + j <= n_req ? tok_off[r0 + j] : 0;
-    int64_t v[kScanPerThread];
-    int64_t mine = 0;
-#pragma unroll
-    for (int j = 0; j < kScanPerThread; ++j) {
-        const int64_t c = r0 + j < n_req ? blocks_of(t[j + 1] - t[j], block, shift) : 0;
-        v[j] = c;
-        mine += c;
+    for (int i = 0; i < kScanPerThread; ++i) {            // every boundary the wavefront needs, at once
+        const uint64_t r = r0 + 64ull * i + lane;
+        const bool in = static_cast<uint32_t>(i) < runs && r < n_req;
+        lo[i] = in ? tok_off[r] : 0;
+        hi[i] = in ? tok_off[r + 1] : 0;
     }
-    int64_t total;
-    int64_t run = block_exclusive(mine, wave_sum, &total);
+    int64_t incl[kScanPerThread];
+    int64_t run = 0;                                      // the wavefront's total so far
 #pragma unroll
-    for (int j = 0; j < kScanPerThread; ++j) {
-        const uint64_t r = base + static_cast<uint64_t>(tid) * kScanPerThread + j;
-        run += v[j];
-        if (r < n_req) key_off[r + 1] = run;
+    for (int i = 0; i < kScanPerThread; ++i) {
+        incl[i] = 0;
+        if (static_cast<uint32_t>(i) < runs) {            // uniform across the workgroup
+            const uint64_t r = r0 + 64ull * i + lane;
+            int64_t x = r < n_req ? blocks_of(hi[i] - lo[i], block, shift) : 0;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const int64_t y = __shfl_up(x, d, 64);
+                if (lane >= static_cast<uint32_t>(d)) x += y;
+            }
+            incl[i] = run + x;
+            run += __shfl(x, 63, 64);
+        }
+    }
+    if (lane == 0) wave_sum[wave] = run;
+    __syncthreads();
+    int64_t base = 0;
+    for (uint32_t q = 0; q < wave; ++q) base += wave_sum[q];
+#pragma unroll
+    for (int i = 0; i < kScanPerThread; ++i) {
+        const uint64_t r = r0 + 64ull * i + lane;
+        if (static_cast<uint32_t>(i) < runs && r < n_req) key_off[r + 1] = base + incl[i];
     }
 }
 
