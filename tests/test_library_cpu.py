@@ -118,6 +118,9 @@ def test_zero_block_rejected_on_host():
     L = pkv.lib()
     assert L.pkv_key_offsets(0x1000, 4, 0, 0x2000, None) == pkv.PKV_EINVAL
     assert L.pkv_derive_keys(0x1000, 16, 0x2000, 1, 0x3000, 0, 0x4000, 1, 0x5000, 0x6000, None) == pkv.PKV_EINVAL
+    t = _table(1024)
+    assert L.pkv_derive_lookup(0x1000, 16, 0x2000, 1, 0x3000, 0, 0x4000, 1, 0x5000, ctypes.byref(t), 0x7000,
+                               0x6000, None) == pkv.PKV_EINVAL
 
 
 def test_null_arguments_rejected_on_host():
@@ -126,6 +129,14 @@ def test_null_arguments_rejected_on_host():
     assert L.pkv_lookup_prefix(ctypes.byref(t), None, 0x2000, 3, 5, 0x3000, 0x4000, None) == pkv.PKV_EINVAL
     assert L.pkv_store(ctypes.byref(t), 0x1000, 0x2000, 3, 5, 0x3000, 0x4000, None, None, 0x5000, None) == pkv.PKV_EINVAL
     assert L.pkv_digest_batch(0x1000, 10, None, 0x2000, 3, 0x3000, 0x4000, None) == pkv.PKV_EINVAL
+    # keys and hits in one call: a missing hit array, unaligned keys, an index of bad capacity
+    assert L.pkv_derive_lookup(0x1000, 16, 0x2000, 1, 0x3000, 16, 0x4000, 1, 0x5000, ctypes.byref(t), None,
+                               0x6000, None) == pkv.PKV_EINVAL
+    assert L.pkv_derive_lookup(0x1000, 16, 0x2000, 1, 0x3000, 16, 0x4000, 1, 0x5008, ctypes.byref(t), 0x7000,
+                               0x6000, None) == pkv.PKV_EINVAL
+    bad = _table(1000)
+    assert L.pkv_derive_lookup(0x1000, 16, 0x2000, 1, 0x3000, 16, 0x4000, 1, 0x5000, ctypes.byref(bad), 0x7000,
+                               0x6000, None) == pkv.PKV_EINVAL
 
 
 def test_host_content_identity_matches_oracle():
