@@ -351,6 +351,19 @@ __device__ __forceinline__ uint32_t lane_swap(uint32_t v) {
     return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x128, 0xF, 0xF, false));
 }
 
+// out[j] = (the pair's other lane's v[j]) + k[j]: four DPP adds (row_ror:8).  v was written by
+// VALU instructions well before (a workgroup barrier lies between), and s_nop 1 covers the two wait
+// states a DPP read of a freshly written VGPR would need anyway.
+__device__ __forceinline__ void swap_add4(uint32_t out[4], const uint32_t v[4], const uint32_t k[4]) {
+    asm volatile("s_nop 1\n"
+                 "v_add_u32_dpp %0, %4, %8 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+                 "v_add_u32_dpp %1, %5, %9 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+                 "v_add_u32_dpp %2, %6, %10 row_ror:8 row_mask:0xf bank_mask:0xf\n"
+                 "v_add_u32_dpp %3, %7, %11 row_ror:8 row_mask:0xf bank_mask:0xf"
+                 : "=&v"(out[0]), "=&v"(out[1]), "=&v"(out[2]), "=&v"(out[3])
+                 : "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3]), "v"(k[0]), "v"(k[1]), "v"(k[2]), "v"(k[3]));
+}
+
 // Bitwise select m ? a : b in one instruction (v_bfi_b32), with the lane's parity mask m as an
 // ordinary register: no condition register to rebuild around each use.
 __device__ __forceinline__ uint32_t bsel(uint32_t m, uint32_t a, uint32_t b) {
@@ -589,14 +602,23 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
         }
         // K + W of rounds 0..3 of the next key (W0..W3 = previous key, held by the a lane and
         // swapped over to the e lane, the only lane whose Q uses it)
-        uint32_t kwp[4];
+        uint32_t kwp[4], kk[4], key[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) kwp[j] = kRoundK[j];
+        for (int j = 0; j < 4; ++j) kwp[j] = kk[j] = kRoundK[j];
         if (odd) sh.prev[c] = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();                                       // prologue
         for (int64_t i = 0; i < nmax; ++i) {
             const int buf = static_cast<int>(i & 1);
             uint32_t x[4], kw[16], kw2[64], hmid[4], q;
+            if (i > 0) {
+                // the previous key, after the barrier that handed it to the helper (its critical
+                // path runs from that barrier, this wavefront waits for it at the next one): the e
+                // lane's K + W of rounds 0..3, and the key into the key array
+                swap_add4(kwp, key, kk);
+                if (odd && i - 1 < n)
+                    reinterpret_cast<uint4*>(a.keys)[k0 + i - 1] =
+                        make_uint4(bswap(key[0]), bswap(key[1]), bswap(key[2]), bswap(key[3]));
+            }
 #pragma unroll
             for (int j = 0; j < 4; ++j) { kw[j] = kwp[j]; kw[4 + j] = dgk[j]; }
             get4(&sh.kw1tok[buf][0][c], kw + 8);
@@ -612,19 +634,15 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
 #pragma unroll
             for (int ph = 0; ph < 4; ++ph)                     // compression 2
                 pair_rounds16_regs(x, q, pl, kw2 + 16 * ph, ph < 3 ? kw2[16 * ph + 16] : 0u);
-            uint32_t key[4];                                   // the key on the a lane
 #pragma unroll
-            for (int j = 0; j < 4; ++j) key[j] = x[j] + hmid[j];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) kwp[j] = lane_swap(key[j]) + kRoundK[j];
-            if (odd) {
-                if (i < n)
-                    reinterpret_cast<uint4*>(a.keys)[k0 + i] =
-                        make_uint4(bswap(key[0]), bswap(key[1]), bswap(key[2]), bswap(key[3]));
-                put4(&sh.prev[c], key);
-            }
+            for (int j = 0; j < 4; ++j) key[j] = x[j] + hmid[j];   // the key on the a lane
+            if (odd) put4(&sh.prev[c], key);
             __syncthreads();                                   // end of key
         }
+        if (odd && nmax > 0 && nmax - 1 < n)                   // the last key of a chain of nmax keys
+            reinterpret_cast<uint4*>(a.keys)[k0 + nmax - 1] =
+                make_uint4(bswap(key[0]), bswap(key[1]), bswap(key[2]), bswap(key[3]));
+        __syncthreads();                                       // every key is in the key array
     } else {
         // ---------------- helper: lane pair per chain ----------------
         const int32_t* tp = a.tokens + t0;
@@ -673,6 +691,7 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             produce_key_pair(sh, c, odd, pk, buf ^ 1, tk);
             __syncthreads();                                   // end of key
         }
+        __syncthreads();                                       // every key is in the key array
         if (FUSED) {
             // every key exists now; finish the probes still open (the exit test is wave-wide, as
             // each probe point exchanges values between the lanes of a pair)
