@@ -202,13 +202,10 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
 }
 
 // ---- store ------------------------------------------------------------------------------------
-// One lane per candidate key at a time (candidate = key j of request r with j >= hits[r]).  A
-// wavefront owns kStoreKeysPerLane x 64 consecutive keys, lane l the keys l, l + 64, l + 128, ..
-// of them, and a lane moves on to its next candidate as soon as the current one is inserted or
-// found.  One key per lane measured fastest (c4 store alone 0.302 ms against 0.318 / 0.347 ms with
-// two / four): fewer, longer wavefronts lose more beside the derive than their busier lanes gain.
-// One (wave-uniform) search finds the request of the wavefront's first key, and each lane walks
-// forward over the request boundaries it meets.
+// One lane per key of the batch; candidate = key j of request r with j >= hits[r].  A wavefront
+// covers 64 consecutive keys: one (wave-uniform) search finds the request of its first key, and
+// each lane walks forward over the few request boundaries inside the wavefront.  The key and its
+// location are loaded before that search, so their round trip overlaps it.
 struct StoreArgs {
     Tab t;
     const uint4* keys;
@@ -226,8 +223,6 @@ struct StoreArgs {
 };
 
 constexpr uint32_t kStoreThreads = 256;
-constexpr uint32_t kStoreKeysPerLane = 1;
-constexpr uint32_t kStoreWaveKeys = 64 * kStoreKeysPerLane;
 
 // The largest r < n_req with key_off[r] <= wave_base (key_off[0] = 0 <= wave_base always): start
 // where equal-length requests would put it, widen by doubling steps until [lo, hi) brackets it, then
@@ -237,8 +232,9 @@ __device__ __forceinline__ uint32_t first_request(const StoreArgs& a, uint64_t w
     const uint64_t n = a.n_req;
     uint64_t lo = 0, hi = n;
     if (total > 0 && n > 2) {
-        uint64_t g = static_cast<uint64_t>(static_cast<double>(wave_base) * static_cast<double>(n) /
-                                           static_cast<double>(total));
+        // single precision is close enough for a guess: the doubling steps correct it
+        uint64_t g = static_cast<uint64_t>(static_cast<float>(wave_base) *
+                                           (static_cast<float>(n) / static_cast<float>(total)));
         if (g >= n) g = n - 1;
         uint64_t step = 1;
         if (a.key_off[g] <= wb) {
@@ -270,56 +266,6 @@ struct StoreProbe {
     bool scanning;             // phase 1: the key may still sit further along its path
 };
 
-// Which of the lane's keys (bit q: key wave_base + 64 q + lane) are candidates.  Computed before
-// the probe loop, so that no load in the loop waits for anything but the last memory operation.
-__device__ __forceinline__ uint32_t lane_candidates(const StoreArgs& a, uint64_t wave_base, int64_t total,
-                                                    uint32_t lane) {
-    if (static_cast<int64_t>(wave_base) >= total) return 0;
-    uint32_t r = first_request(a, wave_base, total);
-    uint32_t mask = 0;
-#pragma unroll
-    for (uint32_t q = 0; q < kStoreKeysPerLane; ++q) {
-        const uint64_t k = wave_base + 64ull * q + lane;
-        if (static_cast<int64_t>(k) >= total) break;
-        while (r + 1 < a.n_req && a.key_off[r + 1] <= static_cast<int64_t>(k)) ++r;
-        const int64_t j = static_cast<int64_t>(k) - a.key_off[r];
-        int64_t h = a.hits[r];
-        if (h < 0) h = 0;
-        if (j >= h) mask |= 1u << q;
-    }
-    return mask;
-}
-
-// Moves the lane to its next candidate (the lowest bit of *cands, which it clears); true with the
-// probe set up at the key's home bucket, false when none is left.  The key and its location are
-// loaded together and both waited for at once: the wait then covers every memory operation in
-// flight, which the publication store that may precede it requires.
-__device__ __forceinline__ bool next_candidate(const StoreArgs& a, uint64_t wave_base, uint32_t lane, uint32_t& cands,
-                                               StoreProbe& st) {
-    while (cands) {
-        const uint32_t q = __builtin_ctz(cands);
-        cands &= cands - 1;
-        const uint64_t k = wave_base + 64ull * q + lane;
-        const uint64_t loc = a.locs[k];
-        const uint4 key = a.keys[k];
-        asm volatile("" : : "v"(loc), "v"(key.x), "v"(key.y), "v"(key.z), "v"(key.w));
-        if (loc >= PKV_LOC_LIMIT) {
-            report(a.status, PKV_ERESERVED);
-            continue;
-        }
-        st.kw = key_words(key);
-        st.want = loc;
-        st.rot = path_rotation(st.kw);
-        st.p = home_bucket(key, (a.t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
-        st.steps = 0;
-        st.first_free = ~0ull;
-        st.waits = 0;
-        st.scanning = true;
-        return true;
-    }
-    return false;
-}
-
 // The pair of a slot whose claim word matched and whose location word is published.  The pair is
 // written by one 16-byte store after the claim; a first half that still reads as the value every
 // free slot holds (all ones) is re-read after an acquire fence, in case the read was stale.
@@ -341,11 +287,11 @@ __device__ __forceinline__ void publish_slot(const Tab& t, uint64_t s, const Key
 }
 
 __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
-    __shared__ uint64_t log_slots[kStoreThreads * kStoreKeysPerLane];   // the workgroup's new slots
+    __shared__ uint64_t log_slots[kStoreThreads];       // the workgroup's new slots
     __shared__ uint32_t log_n, waves_done;
     const uint32_t lane = lane_id();
-    const uint64_t wave_base = static_cast<uint64_t>(blockIdx.x) * (kStoreThreads * kStoreKeysPerLane) +
-                               __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * static_cast<uint64_t>(kStoreWaveKeys);
+    const uint64_t wave_base = static_cast<uint64_t>(blockIdx.x) * kStoreThreads +
+                               __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * 64ull;
     const int64_t total = a.key_off[a.n_req];
     if (total < 0 || static_cast<uint64_t>(total) > a.n_keys) {
         if (blockIdx.x == 0 && threadIdx.x == 0) report(a.status, PKV_ELAYOUT);
@@ -358,9 +304,40 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
     __syncthreads();
     const Tab& t = a.t;
     const uint64_t slot_mask = t.capacity - 1;
-    uint32_t cands = lane_candidates(a, wave_base, total, lane);
+    const uint64_t k = wave_base + lane;
+    const bool in_batch = static_cast<int64_t>(k) < total;
+    uint4 key = make_uint4(0u, 0u, 0u, 0u);
+    uint64_t want = 0;
+    if (in_batch) {                                         // issued before the request search
+        key = a.keys[k];
+        want = a.locs[k];
+    }
+    bool live = false;
+    if (static_cast<int64_t>(wave_base) < total) {
+        uint32_t r = first_request(a, wave_base, total);
+        if (in_batch) {
+            while (r + 1 < a.n_req && a.key_off[r + 1] <= static_cast<int64_t>(k)) ++r;
+            const int64_t j = static_cast<int64_t>(k) - a.key_off[r];
+            int64_t h = a.hits[r];
+            if (h < 0) h = 0;
+            live = j >= h;
+        }
+    }
+    if (live && want >= PKV_LOC_LIMIT) {
+        report(a.status, PKV_ERESERVED);
+        live = false;
+    }
     StoreProbe st;
-    bool live = next_candidate(a, wave_base, lane, cands, st);
+    if (live) {
+        st.kw = key_words(key);
+        st.want = want;
+        st.rot = path_rotation(st.kw);
+        st.p = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
+        st.steps = 0;
+        st.first_free = ~0ull;
+        st.waits = 0;
+        st.scanning = true;
+    }
     while (live) {
         const uint64_t s = path_slot(st.p, st.rot);
         const uint64_t c = load_relaxed(t.lo(s));
@@ -420,11 +397,7 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
                 }
             }
         }
-        if (fail) {
-            live = false;                                   // the call has failed: this lane stops
-        } else if (done) {
-            live = next_candidate(a, wave_base, lane, cands, st);
-        }
+        if (fail || done) live = false;
     }
     // One counter update per workgroup, by its last wavefront to finish: the others leave at once
     // instead of waiting at a barrier (beside other kernels, a workgroup's wavefronts can finish far
@@ -745,7 +718,7 @@ int launch_store(uint64_t* table, uint64_t capacity, const uint8_t* keys, const 
                  uint64_t n_keys, const int32_t* hits, const uint64_t* locs, uint64_t* new_slots, uint64_t* n_new,
                  uint32_t* epochs, uint32_t epoch, int32_t* status, hipStream_t s) {
     if (n_req == 0 || n_keys == 0) return PKV_OK;
-    const uint64_t blocks = (n_keys + kStoreThreads * kStoreKeysPerLane - 1) / (kStoreThreads * kStoreKeysPerLane);
+    const uint64_t blocks = (n_keys + kStoreThreads - 1) / kStoreThreads;
     if (blocks > 0x7fffffffull) return set_error(PKV_EINVAL, "pkv_store: too many keys (%llu)",
                                                  static_cast<unsigned long long>(n_keys));
     StoreArgs a{Tab{table, capacity}, reinterpret_cast<const uint4*>(keys), key_off, n_req, n_keys, hits, locs,
