@@ -218,3 +218,34 @@ def test_fused_step_c2(pkv):
     assert (db.host_hits() == ohits).all()
     _compare_dump(table, idx)
     check_structure(table)
+
+
+def test_fused_through_removed_slots(pkv):
+    """An index whose eviction left removed slots on probe paths (the fixed-budget tier): the fused
+    probes run through them as the lookup does, and give the oracle's hit lengths."""
+    import torch
+    from tests.test_gpu_pipeline import _batches
+    cap, budget = 1024, 300
+    table = pkv.Table(cap, epochs=True)
+    idx = oracle.Index(cap)
+    n_ev = torch.zeros(1, dtype=torch.int64, device="cuda")
+    batches = _batches(10, seed=77, n_req=20)
+    for epoch, b in enumerate(batches[:8], start=1):
+        db = gpu_batch(b)
+        db.digest()
+        db.derive()
+        db.n_new.zero_()
+        pkv.pkv_lookup_prefix_touch(table, db.keys, db.key_off, epoch, db.hits[: max(1, db.n_req)], db.status)
+        pkv.pkv_store_touch(table, db.keys, db.key_off, db.hits[: max(1, db.n_req)], db.locs, db.n_new, db.status,
+                            epoch, db.new_slots)
+        k, ko = oracle_keys(b)
+        hits = idx.lookup_touch(k, ko, epoch)
+        assert idx.store_touch(k, ko, hits, locations(ko, b.tag), epoch) == 0
+        pkv.pkv_table_evict(table, budget, n_ev)
+        assert int(n_ev.item()) == idx.evict(budget)
+        assert db.host_status() == 0
+    from tests.gpu_util import TOMB, raw_table
+    assert (raw_table(table)[1] == TOMB).sum() > 0           # removed slots exist
+    for b in batches:                                        # evicted, kept and never stored prefixes
+        ohits = _check_fused(pkv, b, idx, table)
+        assert ohits.shape[0] == b.n_req

@@ -611,7 +611,8 @@ def test_workload_c5(pkv):
 def test_workload_c4(pkv):
     """Full-size lookup-heavy run: a 2^25-entry fill of a 2^26-slot index, then 16384 x 256 probe keys
     derived, looked up and stored.  Every key, every hit length and the whole index after the store
-    (sorted (key, location) pairs and their count) equal the oracle's; the hit lengths also follow
+    (sorted (key, location) pairs and their count) equal the oracle's, and so do the keys and hit
+    lengths of the fused derive-and-lookup call on the same index; the hit lengths also follow
     the recipe's closed form (the stored prefix under a matching descriptor, 0 under a descriptor
     that differs in one dimension)."""
     w = make_workload("c4")
@@ -622,6 +623,9 @@ def test_workload_c4(pkv):
     assert int(fill.n_new.item()) == w.meta["fill_entries"]
     del fill
     db = gpu_batch(w.batch)
+    db.digest()
+    db.derive_lookup(table)                                  # keys and hits in one call, as well
+    fkeys, fhits = db.host_keys(), db.host_hits()
     db.step(table)
     gkeys, hits = db.host_keys(), db.host_hits()
     assert db.host_status() == 0
@@ -632,10 +636,10 @@ def test_workload_c4(pkv):
     oracle_fill(idx, w.fill)
     assert len(idx) == w.meta["fill_entries"]
     okeys, ko = oracle_keys(w.batch)
-    assert (gkeys == okeys).all()
-    del gkeys
+    assert (gkeys == okeys).all() and (fkeys == okeys).all()
+    del gkeys, fkeys
     ohits = idx.lookup(okeys, ko)
-    assert (hits == ohits).all()
+    assert (hits == ohits).all() and (fhits == ohits).all()
     assert idx.store(okeys, ko, ohits, locations(ko, w.batch.tag)) == 0
     assert int(db.n_new.item()) == len(idx) - w.meta["fill_entries"]
     announce("workload c4: index dump")
