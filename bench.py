@@ -123,7 +123,7 @@ def parse():
     p.add_argument("--cpu-threads", type=int, default=0,
                    help="oracle threads (0 = the CPUs this process may run on, at most the 16 a one-GPU share has)")
     p.add_argument("--calib-copy", action="store_true", help="run only a plain 1 GiB device copy (counter calibration)")
-    p.add_argument("--cold-reps", type=int, default=20,
+    p.add_argument("--cold-reps", type=int, default=50,
                    help="reps of the cold-cache per-kernel measurement after the timed region (0 = skip)")
     p.add_argument("--quiet", action="store_true")
     return p.parse_args()
