@@ -176,6 +176,15 @@ __device__ __forceinline__ int64_t wave_max(int64_t v) {
     return v;
 }
 
+// A value equal on every lane, moved to scalar registers (a loop bounded by it then runs as a
+// scalar loop instead of an exec-mask loop).
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+    const uint64_t u = static_cast<uint64_t>(v);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u >> 32));
+    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
 // ---- B = 16, each chain on a lane pair (used while chains are very scarce) ---------------------
 // Within one SHA-256 round the e-half (Sigma1, Ch, h + K_t + W_t) and the a-half (Sigma0, Maj) are
 // independent until the final sums.  The consumer wavefront gives each chain two lanes, lane i and
@@ -201,12 +210,16 @@ __device__ __forceinline__ int64_t wave_max(int64_t v) {
 // same way.
 constexpr uint32_t kPpChains = 32;
 
+// K + W words the consumer reads are split by parity: [p][r][chain] holds the words
+// t = t0 + 8r + p + 2j (j = 0..3) for the lane of parity p (0: e lane, 1: a lane), so each lane
+// reads four words of its own parity with one 16-byte load, and a round takes its Q word from its
+// own lane or, for odd t, from the partner lane by DPP.
 struct PpShared {
-    uint4 kw2[2][16][kPpChains];      // K_t + W_t of compression 2, two keys
-    uint4 w1tok[2][2][kPpChains];     // W8..W15 of compression 1, two keys
-    uint4 kw1tok[2][2][kPpChains];    // K_t + W_t, t = 8..15 of compression 1, two keys
-    uint4 kw1hi[12][kPpChains];       // K_t + W_t, t = 16..63 of compression 1 (current key)
-    uint4 prev[kPpChains];            // previous key words
+    uint4 kw2[2][2][8][kPpChains];    // K_t + W_t of compression 2 (t0 = 0), two keys; word 0 + h0
+    uint4 w1tok[2][2][kPpChains];     // W8..W15 of compression 1, two keys (helper only)
+    uint4 kw1tok[2][2][kPpChains];    // K_t + W_t, t = 8..15 of compression 1 (t0 = 8), two keys
+    uint4 kw1hi[2][6][kPpChains];     // K_t + W_t, t = 16..63 of compression 1 (t0 = 16), current key
+    uint4 prev[2][kPpChains];         // [1]: previous key words (a lanes); [0]: the e lanes' unused copy
 };
 
 struct PairLane {
@@ -240,13 +253,6 @@ __device__ __forceinline__ bool pair_is_a(uint32_t lane) { return (lane & 8u) !=
     "v_add_u32_dpp %[" #X3 "], %[" #X3 "], %[t0] row_ror:8 row_mask:0xf bank_mask:0x3\n"          \
     "v_add_u32_dpp %[q], %[" #X2 "], %[" #KWN "] quad_perm:[0,1,2,3] row_mask:0xf bank_mask:0x3\n" \
     "v_add_u32_dpp %[" #X3 "], %[t0], %[t0] row_ror:8 row_mask:0xf bank_mask:0xc\n"
-// Without forming the next round's Q (the caller forms it from K + W words that are still
-// arriving); one wait state more covers the a lane's DPP read of Y.
-#define PKV_PAIR_ROUND_LAST(X0, X1, X2, X3)                                                          \
-    PKV_ROUND_HEAD(X0, X1, X2)                                                                    \
-    "v_add_u32_dpp %[" #X3 "], %[" #X3 "], %[t0] row_ror:8 row_mask:0xf bank_mask:0x3\n"          \
-    "s_nop 0\n"                                                                                   \
-    "v_add_u32_dpp %[" #X3 "], %[t0], %[t0] row_ror:8 row_mask:0xf bank_mask:0xc\n"
 // gfx950 fetches 8-byte instructions (VOP3, DPP) that are not 8-byte aligned at about one cycle
 // more each: a run of the 10-instruction round placed 4 bytes off takes 50 cycles instead of 40.
 // The compiler puts 4-byte instructions (s_nop, VOP2) between asm statements, so each block of
@@ -265,14 +271,6 @@ __device__ __forceinline__ void pair_rounds4(uint32_t& x0, uint32_t& x1, uint32_
     uint32_t t0, t1, t2;
     asm volatile(PKV_ALIGN8 PKV_PAIR_ROUND(a, b, c, d, k1) PKV_PAIR_ROUND(d, a, b, c, k2) PKV_PAIR_ROUND(c, d, a, b, k3)
                      PKV_PAIR_ROUND(b, c, d, a, k4) PKV_ROUNDS4_OPERANDS, [k4] "v"(k4));
-}
-
-// Four paired rounds whose last one leaves Q of the following round to the caller.
-__device__ __forceinline__ void pair_rounds4_last(uint32_t& x0, uint32_t& x1, uint32_t& x2, uint32_t& x3, uint32_t q,
-                                                  const PairLane& pl, uint32_t k1, uint32_t k2, uint32_t k3) {
-    uint32_t t0, t1, t2;
-    asm volatile(PKV_ALIGN8 PKV_PAIR_ROUND(a, b, c, d, k1) PKV_PAIR_ROUND(d, a, b, c, k2) PKV_PAIR_ROUND(c, d, a, b, k3)
-                     PKV_PAIR_ROUND_LAST(b, c, d, a) PKV_ROUNDS4_OPERANDS);
 }
 
 // 16 paired rounds as one asm statement, for K + W words that are all in registers already (the
@@ -296,7 +294,6 @@ __device__ __forceinline__ void pair_rounds16_regs(uint32_t x[4], uint32_t& q, c
 #undef PKV_PAIR_ROUNDS4
 #undef PKV_ROUNDS4_OPERANDS
 #undef PKV_ALIGN8
-#undef PKV_PAIR_ROUND_LAST
 #undef PKV_PAIR_ROUND
 #undef PKV_ROUND_HEAD
 
@@ -310,59 +307,180 @@ __device__ __forceinline__ void pair_rounds16(uint32_t x[4], uint32_t& q, const 
     pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[13], kw[14], kw[15], after);
 }
 
-// Compression 1 of a key on the consumer: rounds 0..15 take K + W from kw (registers), the other
-// 48 rounds from the helper's rows (rows[4p + j][c] holds rounds 16 + 16p + 4j .. + 3).  The
-// barrier that makes a phase's rows visible sits four rounds before the phase starts, and the rows
-// are read right after it, so the last four rounds of the previous phase cover their LDS latency;
-// those four rounds leave Q of the phase's first round to be formed from the new words.
-__device__ __forceinline__ void pair_comp1(uint32_t x[4], const PairLane& pl, const uint32_t kw[16],
-                                           const uint4 (*rows)[kPpChains], uint32_t c) {
-    uint32_t ka[16], kb[16];
-    uint32_t q = (x[3] + kw[0]) & pl.nm;
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[1], kw[2], kw[3], kw[4]);
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[5], kw[6], kw[7], kw[8]);
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[9], kw[10], kw[11], kw[12]);      // rounds 0..11
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < 4; ++j) get4(&rows[j][c], ka + 4 * j);
-    pair_rounds4_last(x[0], x[1], x[2], x[3], q, pl, kw[13], kw[14], kw[15]);         // rounds 12..15
-    q = (x[3] + ka[0]) & pl.nm;
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, ka[1], ka[2], ka[3], ka[4]);
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, ka[5], ka[6], ka[7], ka[8]);
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, ka[9], ka[10], ka[11], ka[12]);      // rounds 16..27
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < 4; ++j) get4(&rows[4 + j][c], kb + 4 * j);
-    pair_rounds4_last(x[0], x[1], x[2], x[3], q, pl, ka[13], ka[14], ka[15]);         // rounds 28..31
-    q = (x[3] + kb[0]) & pl.nm;
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kb[1], kb[2], kb[3], kb[4]);
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kb[5], kb[6], kb[7], kb[8]);
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kb[9], kb[10], kb[11], kb[12]);      // rounds 32..43
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < 4; ++j) get4(&rows[8 + j][c], ka + 4 * j);
-    pair_rounds4_last(x[0], x[1], x[2], x[3], q, pl, kb[13], kb[14], kb[15]);         // rounds 44..47
-    q = (x[3] + ka[0]) & pl.nm;
-    pair_rounds16(x, q, pl, ka, 0u);                                                   // rounds 48..63
-}
-
 // v of the pair's other lane (DPP row_ror:8).
 __device__ __forceinline__ uint32_t lane_swap(uint32_t v) {
     return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x128, 0xF, 0xF, false));
 }
 
-// out[j] = (the pair's other lane's v[j]) + k[j]: four DPP adds (row_ror:8).  v was written by
-// VALU instructions well before (a workgroup barrier lies between), and s_nop 1 covers the two wait
-// states a DPP read of a freshly written VGPR would need anyway.
-__device__ __forceinline__ void swap_add4(uint32_t out[4], const uint32_t v[4], const uint32_t k[4]) {
-    asm volatile("s_nop 1\n"
-                 "v_add_u32_dpp %0, %4, %8 row_ror:8 row_mask:0xf bank_mask:0xf\n"
-                 "v_add_u32_dpp %1, %5, %9 row_ror:8 row_mask:0xf bank_mask:0xf\n"
-                 "v_add_u32_dpp %2, %6, %10 row_ror:8 row_mask:0xf bank_mask:0xf\n"
-                 "v_add_u32_dpp %3, %7, %11 row_ror:8 row_mask:0xf bank_mask:0xf"
-                 : "=&v"(out[0]), "=&v"(out[1]), "=&v"(out[2]), "=&v"(out[3])
-                 : "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3]), "v"(k[0]), "v"(k[1]), "v"(k[2]), "v"(k[3]));
+// ---- k_derive_b16_pp's consumer: rounds with K + W split over the lane pair ------------------
+// The e lane forms Q = h + K_t + W_t for the next round; K + W of even t sits in its own register,
+// of odd t in the same register of its partner (the a lane), read by DPP row_ror:8.  So each lane
+// holds half of a key's K + W words.  Every write of Q is masked to the e lanes (the a lanes' Q
+// stays zero).  A block of rounds may start from read-only input registers (the chaining value)
+// and write its first four new state words into fresh registers, which saves copying the input.
+// Operand roles and instruction forms are those of the rounds above (PKV_ROUND_HEAD).
+#define PKV_S_HEAD(X0, X1, X2)                                                                    \
+    "v_alignbit_b32 %[t0], %[" #X0 "], %[" #X0 "], %[r1]\n"                                       \
+    "v_alignbit_b32 %[t1], %[" #X0 "], %[" #X0 "], %[r2]\n"                                       \
+    "v_alignbit_b32 %[t2], %[" #X0 "], %[" #X0 "], %[r3]\n"                                       \
+    "v_bitop3_b32 %[t0], %[t0], %[t1], %[t2] bitop3:0x96\n"                                       \
+    "v_bitop3_b32 %[t1], %[" #X0 "], %[" #X1 "], %[m] bitop3:0xd2\n"                              \
+    "v_bitop3_b32 %[t1], %[t1], %[" #X1 "], %[" #X2 "] bitop3:0xca\n"                             \
+    "v_add3_u32 %[t0], %[t0], %[t1], %[q]\n"
+// next Q from the lane's own word / the partner's word / none (last round of a key)
+#define PKV_QO(X2, K) "v_add_u32_dpp %[q], %[" #X2 "], %[" #K "] quad_perm:[0,1,2,3] row_mask:0xf bank_mask:0x3\n"
+#define PKV_QP(X2, K) "v_add_u32_dpp %[q], %[" #K "], %[" #X2 "] row_ror:8 row_mask:0xf bank_mask:0x3\n"
+#define PKV_QN(X2, K) "s_nop 0\n"
+// one round: the new x0 goes to D (X3's register in place, or a fresh one)
+#define PKV_SR(X0, X1, X2, X3, D, QF, K)                                                          \
+    PKV_S_HEAD(X0, X1, X2)                                                                        \
+    "v_add_u32_dpp %[" #D "], %[" #X3 "], %[t0] row_ror:8 row_mask:0xf bank_mask:0x3\n"           \
+    QF(X2, K)                                                                                     \
+    "v_add_u32_dpp %[" #D "], %[t0], %[t0] row_ror:8 row_mask:0xf bank_mask:0xc\n"
+// in place, by position in the four-round cycle of roles
+#define PKV_R0(QF, K) PKV_SR(a, b, c, d, d, QF, K)
+#define PKV_R1(QF, K) PKV_SR(d, a, b, c, c, QF, K)
+#define PKV_R2(QF, K) PKV_SR(c, d, a, b, b, QF, K)
+#define PKV_R3(QF, K) PKV_SR(b, c, d, a, a, QF, K)
+// from inputs i0..i3 into fresh a..d; afterwards a..d hold the roles x0..x3
+#define PKV_F0(QF, K) PKV_SR(i0, i1, i2, i3, d, QF, K)
+#define PKV_F1(QF, K) PKV_SR(d, i0, i1, i2, c, QF, K)
+#define PKV_F2(QF, K) PKV_SR(c, d, i0, i1, b, QF, K)
+#define PKV_F3(QF, K) PKV_SR(b, c, d, i0, a, QF, K)
+// four rounds t0 + 4s .. of a phase whose own words are W[2s], W[2s+1] (K + W of t0 + 4s + 1 +
+// j: partner's W[2s], own W[2s+1], partner's W[2s+1], own W[2s+2] is the next block's)
+#define PKV_PH4(KA, KB) PKV_R0(PKV_QO, KA) PKV_R1(PKV_QP, KA) PKV_R2(PKV_QO, KB) PKV_R3(PKV_QP, KB)
+#define PKV_ALIGN ".p2align 3\n"
+#define PKV_S_IN [m] "v"(pl.m), [r1] "v"(pl.r1), [r2] "v"(pl.r2), [r3] "v"(pl.r3)
+#define PKV_S_INOUT(X)                                                                            \
+    [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [q] "+v"(q), [a] "+v"(X[0]), [b] "+v"(X[1]), \
+        [c] "+v"(X[2]), [d] "+v"(X[3])
+#define PKV_S_FRESH(X)                                                                            \
+    [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [q] "+v"(q), [a] "=&v"(X[0]), [b] "=&v"(X[1]), \
+        [c] "=&v"(X[2]), [d] "=&v"(X[3])
+
+// After a block of n rounds in place the roles have turned n times: x0 moves to the register of
+// x3, and so on.
+__device__ __forceinline__ void roles_turn1(uint32_t x[4]) {
+    const uint32_t t = x[3];
+    x[3] = x[2]; x[2] = x[1]; x[1] = x[0]; x[0] = t;
 }
+__device__ __forceinline__ void roles_turn3(uint32_t x[4]) {
+    const uint32_t t = x[0];
+    x[0] = x[1]; x[1] = x[2]; x[2] = x[3]; x[3] = t;
+}
+
+// Q of round 0 (h0 + K_0 + W_0, into the e lanes of q) and K + W of rounds 1..3 from the partner's
+// key words v: four DPP adds.  v was written well before (a workgroup barrier lies between), and
+// s_nop 1 covers the two wait states a DPP read of a freshly written VGPR would need anyway.
+__device__ __forceinline__ void swap_q_add3(uint32_t& q, uint32_t out[4], const uint32_t v[4], const uint32_t k[4]) {
+    asm volatile("s_nop 1\n"
+                 "v_add_u32_dpp %[q], %[v0], %[k0] row_ror:8 row_mask:0xf bank_mask:0x3\n"
+                 "v_add_u32_dpp %[o1], %[v1], %[k1] row_ror:8 row_mask:0xf bank_mask:0xf\n"
+                 "v_add_u32_dpp %[o2], %[v2], %[k2] row_ror:8 row_mask:0xf bank_mask:0xf\n"
+                 "v_add_u32_dpp %[o3], %[v3], %[k3] row_ror:8 row_mask:0xf bank_mask:0xf"
+                 : [q] "+v"(q), [o1] "=&v"(out[1]), [o2] "=&v"(out[2]), [o3] "=&v"(out[3])
+                 : [v0] "v"(v[0]), [v1] "v"(v[1]), [v2] "v"(v[2]), [v3] "v"(v[3]), [k0] "v"(k[0]), [k1] "v"(k[1]),
+                   [k2] "v"(k[2]), [k3] "v"(k[3]));
+}
+
+// Compression 1, rounds 0..6 from the initial value iv (K + W of rounds 1..3: kw[1..3], 4..7: dg).
+__device__ __forceinline__ void pair_c1_r0_6(uint32_t x[4], uint32_t& q, const PairLane& pl, const uint32_t iv[4],
+                                            const uint32_t kw[4], const uint32_t dg[4]) {
+    uint32_t t0, t1, t2;
+    asm volatile(PKV_ALIGN PKV_F0(PKV_QO, k1) PKV_F1(PKV_QO, k2) PKV_F2(PKV_QO, k3) PKV_F3(PKV_QO, k4)
+                     PKV_R0(PKV_QO, k5) PKV_R1(PKV_QO, k6) PKV_R2(PKV_QO, k7)
+                 : PKV_S_FRESH(x)
+                 : PKV_S_IN, [i0] "v"(iv[0]), [i1] "v"(iv[1]), [i2] "v"(iv[2]), [i3] "v"(iv[3]), [k1] "v"(kw[1]),
+                   [k2] "v"(kw[2]), [k3] "v"(kw[3]), [k4] "v"(dg[0]), [k5] "v"(dg[1]), [k6] "v"(dg[2]),
+                   [k7] "v"(dg[3]));
+    roles_turn3(x);
+}
+
+// Compression 1, rounds 7..11 (K + W of rounds 8..12 from the token words r: t = 8 + odd + 2j).
+__device__ __forceinline__ void pair_c1_r7_11(uint32_t x[4], uint32_t& q, const PairLane& pl, const uint32_t r[4]) {
+    uint32_t t0, t1, t2;
+    asm volatile(PKV_ALIGN PKV_R0(PKV_QO, w0) PKV_R1(PKV_QP, w0) PKV_R2(PKV_QO, w1) PKV_R3(PKV_QP, w1)
+                     PKV_R0(PKV_QO, w2)
+                 : PKV_S_INOUT(x)
+                 : PKV_S_IN, [w0] "v"(r[0]), [w1] "v"(r[1]), [w2] "v"(r[2]));
+    roles_turn1(x);
+}
+
+// Three rounds whose next K + W words are the partner's ka, own kb, partner's kc: the rounds
+// right after a phase barrier, which leave the phase's new words time to arrive from LDS.
+__device__ __forceinline__ void pair_r3_pp(uint32_t x[4], uint32_t& q, const PairLane& pl, uint32_t ka, uint32_t kb,
+                                          uint32_t kc) {
+    uint32_t t0, t1, t2;
+    asm volatile(PKV_ALIGN PKV_R0(PKV_QP, w0) PKV_R1(PKV_QO, w1) PKV_R2(PKV_QP, w2)
+                 : PKV_S_INOUT(x)
+                 : PKV_S_IN, [w0] "v"(ka), [w1] "v"(kb), [w2] "v"(kc));
+    roles_turn3(x);
+}
+
+// 13 rounds t0 - 1 .. t0 + 11 of a phase whose own words are w (t = t0 + odd + 2j, j = 0..7).
+__device__ __forceinline__ void pair_r13_phase(uint32_t x[4], uint32_t& q, const PairLane& pl, const uint32_t w[8]) {
+    uint32_t t0, t1, t2;
+    asm volatile(PKV_ALIGN PKV_PH4(w0, w1) PKV_PH4(w2, w3) PKV_PH4(w4, w5) PKV_R0(PKV_QO, w6)
+                 : PKV_S_INOUT(x)
+                 : PKV_S_IN, [w0] "v"(w[0]), [w1] "v"(w[1]), [w2] "v"(w[2]), [w3] "v"(w[3]), [w4] "v"(w[4]),
+                   [w5] "v"(w[5]), [w6] "v"(w[6]));
+    roles_turn1(x);
+}
+
+// Rounds 47..63 of compression 1; the last one forms compression 2's first Q from k2w0 (its
+// K_0 + W_0 + h0 on the e lane).
+__device__ __forceinline__ void pair_r17_last(uint32_t x[4], uint32_t& q, const PairLane& pl, const uint32_t w[8],
+                                             uint32_t k2w0) {
+    uint32_t t0, t1, t2;
+    asm volatile(PKV_ALIGN PKV_PH4(w0, w1) PKV_PH4(w2, w3) PKV_PH4(w4, w5) PKV_PH4(w6, w7) PKV_R0(PKV_QO, w8)
+                 : PKV_S_INOUT(x)
+                 : PKV_S_IN, [w0] "v"(w[0]), [w1] "v"(w[1]), [w2] "v"(w[2]), [w3] "v"(w[3]), [w4] "v"(w[4]),
+                   [w5] "v"(w[5]), [w6] "v"(w[6]), [w7] "v"(w[7]), [w8] "v"(k2w0));
+    roles_turn1(x);
+}
+
+// Compression 2 from the chaining value h (read only): 64 rounds whose own K + W words are k
+// (t = odd + 2j, j = 0..31), the first four rounds writing fresh registers.
+#define PKV_C2_4(KA, KB, KC) PKV_R0(PKV_QP, KA) PKV_R1(PKV_QO, KB) PKV_R2(PKV_QP, KB) PKV_R3(PKV_QO, KC)
+__device__ __forceinline__ void pair_c2(uint32_t x[4], uint32_t& q, const PairLane& pl, const uint32_t h[4],
+                                       const uint32_t k[32]) {
+    uint32_t t0, t1, t2;
+    asm volatile(PKV_ALIGN PKV_F0(PKV_QP, k0) PKV_F1(PKV_QO, k1) PKV_F2(PKV_QP, k1) PKV_F3(PKV_QO, k2)
+                     PKV_C2_4(k2, k3, k4) PKV_C2_4(k4, k5, k6) PKV_C2_4(k6, k7, k8) PKV_C2_4(k8, k9, k10)
+                     PKV_C2_4(k10, k11, k12) PKV_C2_4(k12, k13, k14) PKV_C2_4(k14, k15, k16)
+                     PKV_C2_4(k16, k17, k18) PKV_C2_4(k18, k19, k20) PKV_C2_4(k20, k21, k22)
+                     PKV_C2_4(k22, k23, k24) PKV_C2_4(k24, k25, k26) PKV_C2_4(k26, k27, k28)
+                     PKV_C2_4(k28, k29, k30) PKV_R0(PKV_QP, k30) PKV_R1(PKV_QO, k31) PKV_R2(PKV_QP, k31)
+                     PKV_R3(PKV_QN, k31)
+                 : PKV_S_FRESH(x)
+                 : PKV_S_IN, [i0] "v"(h[0]), [i1] "v"(h[1]), [i2] "v"(h[2]), [i3] "v"(h[3]), [k0] "v"(k[0]),
+                   [k1] "v"(k[1]), [k2] "v"(k[2]), [k3] "v"(k[3]), [k4] "v"(k[4]), [k5] "v"(k[5]), [k6] "v"(k[6]),
+                   [k7] "v"(k[7]), [k8] "v"(k[8]), [k9] "v"(k[9]), [k10] "v"(k[10]), [k11] "v"(k[11]),
+                   [k12] "v"(k[12]), [k13] "v"(k[13]), [k14] "v"(k[14]), [k15] "v"(k[15]), [k16] "v"(k[16]),
+                   [k17] "v"(k[17]), [k18] "v"(k[18]), [k19] "v"(k[19]), [k20] "v"(k[20]), [k21] "v"(k[21]),
+                   [k22] "v"(k[22]), [k23] "v"(k[23]), [k24] "v"(k[24]), [k25] "v"(k[25]), [k26] "v"(k[26]),
+                   [k27] "v"(k[27]), [k28] "v"(k[28]), [k29] "v"(k[29]), [k30] "v"(k[30]), [k31] "v"(k[31]));
+}
+#undef PKV_C2_4
+#undef PKV_S_FRESH
+#undef PKV_S_INOUT
+#undef PKV_S_IN
+#undef PKV_ALIGN
+#undef PKV_PH4
+#undef PKV_F3
+#undef PKV_F2
+#undef PKV_F1
+#undef PKV_F0
+#undef PKV_R3
+#undef PKV_R2
+#undef PKV_R1
+#undef PKV_R0
+#undef PKV_SR
+#undef PKV_QN
+#undef PKV_QP
+#undef PKV_QO
+#undef PKV_S_HEAD
 
 // Bitwise select m ? a : b in one instruction (v_bfi_b32), with the lane's parity mask m as an
 // ordinary register: no condition register to rebuild around each use.
@@ -434,6 +552,18 @@ __device__ __forceinline__ void pair_schedule8(uint32_t v[8], const PairK& pk, u
     }
 }
 
+// The same steps writing K + W in the parity-split layout of PpShared: word t = 2j + odd goes to
+// row (t - T0) / 8, component j % 4 of the lane's own parity block (col includes parity and chain).
+template <int J0, int T0>
+__device__ __forceinline__ void pair_schedule8s(uint32_t v[8], const PairK& pk, uint32_t* col) {
+#pragma unroll
+    for (int j = J0; j < J0 + 8; ++j) {
+        uint32_t wk;
+        pair_schedule_step(v, pk.m, pk.k[j], wk);
+        col[((2 * j - T0) >> 3) * (kPpChains * 4) + (j & 3)] = wk;
+    }
+}
+
 // This lane's parity of a key's 16 tokens (out[k] = token 2k + odd), zeros past the chain.
 __device__ __forceinline__ void load_tokens_pair(const int32_t* tp, int64_t key, int64_t n, bool odd, uint32_t out[8]) {
     if (key < n) {
@@ -453,13 +583,13 @@ __device__ __forceinline__ void produce_key_pair(PpShared& sh, uint32_t chain, b
                                                  const uint32_t tk[8]) {
     const uint32_t o = odd ? 1u : 0u;
     uint32_t* wcol = reinterpret_cast<uint32_t*>(&sh.w1tok[buf][0][chain]) + o;
-    uint32_t* kcol = reinterpret_cast<uint32_t*>(&sh.kw1tok[buf][0][chain]) + o;
+    uint32_t* kcol = reinterpret_cast<uint32_t*>(&sh.kw1tok[buf][o][chain]);
 #pragma unroll
     for (int k = 0; k < 4; ++k) {                      // compression 1, word 8 + 2k + odd = token 2k + odd
         const uint32_t x = bswap(tk[k]);
         const uint32_t kk = pk.k[4 + k];
         wcol[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = x;
-        kcol[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = x + kk;
+        kcol[k] = x + kk;
     }
     // compression 2: words 0..7 = tokens 8..15, then the padding of a 96-byte message
     uint32_t own[8];
@@ -469,15 +599,18 @@ __device__ __forceinline__ void produce_key_pair(PpShared& sh, uint32_t chain, b
     own[5] = 0u;
     own[6] = 0u;
     own[7] = pk.m & ((32u + 4u * 16u) * 8u);
-    uint32_t* col = reinterpret_cast<uint32_t*>(&sh.kw2[buf][0][chain]) + o;
+    uint32_t* col = reinterpret_cast<uint32_t*>(&sh.kw2[buf][o][0][chain]);
+    // word 0 carries h0 as well: the last round of compression 1 forms compression 2's first Q
+    // (h of the chaining value + K_0 + W_0) from it
 #pragma unroll
-    for (int k = 0; k < 8; ++k) col[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = own[k] + pk.k[k];
+    for (int k = 0; k < 8; ++k)
+        col[(k >> 2) * (kPpChains * 4) + (k & 3)] = own[k] + pk.k[k] + (k == 0 ? (~pk.m & kInitH[7]) : 0u);
     uint32_t v[8];                                     // own words, newest first
 #pragma unroll
     for (int k = 0; k < 8; ++k) v[k] = own[7 - k];
-    pair_schedule8<8, 0>(v, pk, col);
-    pair_schedule8<16, 0>(v, pk, col);
-    pair_schedule8<24, 0>(v, pk, col);
+    pair_schedule8s<8, 0>(v, pk, col);
+    pair_schedule8s<16, 0>(v, pk, col);
+    pair_schedule8s<24, 0>(v, pk, col);
 }
 
 // ---- fused derive and lookup: the helper probes the index while the consumer hashes ------------
@@ -583,6 +716,7 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
         __syncthreads();
         for (int k = 0; k < 2 * P; ++k) nmax = pair_n[k] > nmax ? pair_n[k] : nmax;
     }
+    nmax = uniform64(nmax);
     uint32_t dg[4] = {0u, 0u, 0u, 0u};
     if (valid) load_digest(a, r, dg);
 
@@ -600,43 +734,58 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             iv[q] = odd ? kInitH[q] : kInitH[4 + q];
             dgk[q] = dg[q] + kRoundK[4 + q];
         }
-        // K + W of rounds 0..3 of the next key (W0..W3 = previous key, held by the a lane and
-        // swapped over to the e lane, the only lane whose Q uses it)
-        uint32_t kwp[4], kk[4], key[4] = {0u, 0u, 0u, 0u};
+        // Q of round 0 of the next key (h0 + K_0 + W_0, e lanes) and K + W of its rounds 1..3
+        // (W0..W3 = previous key, held by the a lane and swapped over to the e lane, the only lane
+        // whose Q uses them).  The a lanes' Q is zero throughout: every write of Q is masked to the
+        // e lanes.
+        uint32_t kwp[4], kk[4], key[4] = {0u, 0u, 0u, 0u}, q = odd ? 0u : kRoundK[0] + kInitH[7];
 #pragma unroll
         for (int j = 0; j < 4; ++j) kwp[j] = kk[j] = kRoundK[j];
-        if (odd) sh.prev[c] = make_uint4(0u, 0u, 0u, 0u);
+        kk[0] = kRoundK[0] + kInitH[7];
+        uint4* const prev_out = &sh.prev[odd ? 1 : 0][c];
+        const uint32_t par = odd ? 1u : 0u;
+        if (odd) sh.prev[1][c] = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();                                       // prologue
         for (int64_t i = 0; i < nmax; ++i) {
             const int buf = static_cast<int>(i & 1);
-            uint32_t x[4], kw[16], kw2[64], hmid[4], q;
+            uint32_t x[4], r1[4], k2[32], wa[8], wb[8], hmid[4];
             if (i > 0) {
                 // the previous key, after the barrier that handed it to the helper (its critical
-                // path runs from that barrier, this wavefront waits for it at the next one): the e
-                // lane's K + W of rounds 0..3, and the key into the key array
-                swap_add4(kwp, key, kk);
+                // path runs from that barrier, this wavefront waits for it at the next one): Q of
+                // round 0 and the e lane's K + W of rounds 1..3, and the key into the key array
+                swap_q_add3(q, kwp, key, kk);
                 if (odd && i - 1 < n)
                     reinterpret_cast<uint4*>(a.keys)[k0 + i - 1] =
                         make_uint4(bswap(key[0]), bswap(key[1]), bswap(key[2]), bswap(key[3]));
             }
+            get4(&sh.kw1tok[buf][par][c], r1);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) { kw[j] = kwp[j]; kw[4 + j] = dgk[j]; }
-            get4(&sh.kw1tok[buf][0][c], kw + 8);
-            get4(&sh.kw1tok[buf][1][c], kw + 12);
+            for (int r = 0; r < 8; ++r) get4(&sh.kw2[buf][par][r][c], k2 + 4 * r);
+            pair_c1_r0_6(x, q, pl, iv, kwp, dgk);                      // rounds 0..6
+            pair_c1_r7_11(x, q, pl, r1);                               // rounds 7..11
+            // each phase barrier publishes the helper's next 16 words; the three rounds after it
+            // still use the previous words and cover the new ones' LDS latency
+            __syncthreads();
+            get4(&sh.kw1hi[par][0][c], wa);
+            get4(&sh.kw1hi[par][1][c], wa + 4);
+            pair_r3_pp(x, q, pl, r1[2], r1[3], r1[3]);                 // rounds 12..14
+            pair_r13_phase(x, q, pl, wa);                              // rounds 15..27
+            __syncthreads();
+            get4(&sh.kw1hi[par][2][c], wb);
+            get4(&sh.kw1hi[par][3][c], wb + 4);
+            pair_r3_pp(x, q, pl, wa[6], wa[7], wa[7]);                 // rounds 28..30
+            pair_r13_phase(x, q, pl, wb);                              // rounds 31..43
+            __syncthreads();
+            get4(&sh.kw1hi[par][4][c], wa);
+            get4(&sh.kw1hi[par][5][c], wa + 4);
+            pair_r3_pp(x, q, pl, wb[6], wb[7], wb[7]);                 // rounds 44..46
+            pair_r17_last(x, q, pl, wa, k2[0]);                        // rounds 47..63
 #pragma unroll
-            for (int ph = 0; ph < 16; ++ph) get4(&sh.kw2[buf][ph][c], kw2 + 4 * ph);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) x[j] = iv[j];
-            pair_comp1(x, pl, kw, sh.kw1hi, c);            // three barriers inside
-#pragma unroll
-            for (int j = 0; j < 4; ++j) { hmid[j] = x[j] + iv[j]; x[j] = hmid[j]; }
-            q = (x[3] + kw2[0]) & pl.nm;
-#pragma unroll
-            for (int ph = 0; ph < 4; ++ph)                     // compression 2
-                pair_rounds16_regs(x, q, pl, kw2 + 16 * ph, ph < 3 ? kw2[16 * ph + 16] : 0u);
+            for (int j = 0; j < 4; ++j) hmid[j] = x[j] + iv[j];
+            pair_c2(x, q, pl, hmid, k2);                               // compression 2
 #pragma unroll
             for (int j = 0; j < 4; ++j) key[j] = x[j] + hmid[j];   // the key on the a lane
-            if (odd) put4(&sh.prev[c], key);
+            put4(prev_out, key);
             __syncthreads();                                   // end of key
         }
         if (odd && nmax > 0 && nmax - 1 < n)                   // the last key of a chain of nmax keys
@@ -645,11 +794,15 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
         __syncthreads();                                       // every key is in the key array
     } else {
         // ---------------- helper: lane pair per chain ----------------
+        // The consumer waits at each phase barrier for this wavefront's schedule words, so the
+        // helper outranks whatever else shares its SIMD (the index kernels of the previous batch
+        // run beside this kernel); it issues little, so the others lose little.
+        __builtin_amdgcn_s_setprio(3);
         const int32_t* tp = a.tokens + t0;
         uint32_t dsel[2];
         dsel[0] = odd ? dg[1] : dg[0];     // W4 / W5
         dsel[1] = odd ? dg[3] : dg[2];     // W6 / W7
-        uint32_t* kw1hi_col = reinterpret_cast<uint32_t*>(&sh.kw1hi[0][c]) + (odd ? 1 : 0);
+        uint32_t* kw1hi_col = reinterpret_cast<uint32_t*>(&sh.kw1hi[odd ? 1 : 0][0][c]);
         const PairK pk = make_pair_k(odd);
         uint32_t tk[8], pre[8];
         PairProbe pr;
@@ -665,7 +818,7 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
         for (int64_t i = 0; i < nmax; ++i) {
             const int buf = static_cast<int>(i & 1);
             uint32_t pv[4], tw[8], v[8];
-            get4(&sh.prev[c], pv);
+            get4(&sh.prev[1][c], pv);
             get4(&sh.w1tok[buf][0][c], tw);
             get4(&sh.w1tok[buf][1][c], tw + 4);
             // own words, newest first: W14 W12 .. W0 (e lane) or W15 W13 .. W1 (a lane)
@@ -675,11 +828,11 @@ __global__ __launch_bounds__(kPcThreads * P) void k_derive_b16_pp(ChainArgs a) {
             v[5] = dsel[0];
             v[6] = bsel(pk.m, pv[3], pv[2]);
             v[7] = bsel(pk.m, pv[1], pv[0]);
-            pair_schedule8<8>(v, pk, kw1hi_col);
+            pair_schedule8s<8, 16>(v, pk, kw1hi_col);
             __syncthreads();
-            pair_schedule8<16>(v, pk, kw1hi_col);
+            pair_schedule8s<16, 16>(v, pk, kw1hi_col);
             __syncthreads();
-            pair_schedule8<24>(v, pk, kw1hi_col);
+            pair_schedule8s<24, 16>(v, pk, kw1hi_col);
             __syncthreads();
             if (FUSED) {                                       // keys 0 .. i - 1 exist; pv is key i - 1
                 const uint4 newest = make_uint4(bswap(pv[0]), bswap(pv[1]), bswap(pv[2]), bswap(pv[3]));

@@ -287,6 +287,10 @@ __device__ __forceinline__ void publish_slot(const Tab& t, uint64_t s, const Key
 }
 
 __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
+    // Beside the next batch's key derivation, a store wavefront that shares a SIMD with one of its
+    // round-issuing wavefronts would only get the issue slots that wavefront leaves idle; one level
+    // of priority lets the store's short bursts go first.
+    __builtin_amdgcn_s_setprio(1);
     __shared__ uint64_t log_slots[kStoreThreads];       // the workgroup's new slots
     __shared__ uint32_t log_n, waves_done;
     const uint32_t lane = lane_id();
