@@ -260,7 +260,6 @@ struct StoreProbe {
     uint64_t want;             // its location
     uint64_t rot;              // path rotation inside each bucket
     uint64_t p;                // path position
-    uint64_t steps;            // slots passed in the current phase
     uint64_t first_free;       // position of the first removed slot met while scanning, or ~0
     uint32_t waits;
     bool scanning;             // phase 1: the key may still sit further along its path
@@ -332,30 +331,57 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
         live = false;
     }
     StoreProbe st;
+    uint64_t p_begin = 0;                                   // where the current phase of the path began
     if (live) {
         st.kw = key_words(key);
         st.want = want;
         st.rot = path_rotation(st.kw);
         st.p = home_bucket(key, (t.capacity / kSlotsPerBucket) - 1) * kSlotsPerBucket;
-        st.steps = 0;
         st.first_free = ~0ull;
         st.waits = 0;
         st.scanning = true;
+        p_begin = st.p;
     }
+    // Each pass first runs a tight scan past the slots that need nothing from the lane: slots of
+    // other keys, and removed slots while the key may still sit further along its path (the first
+    // of those is remembered).  It stops at a never-used slot, at a slot with the lane's own claim
+    // word, or, once the lane claims, at a removed slot; the rest of the pass handles that slot.
+    // A whole cycle of the path is detected by returning to the position the current phase began at.
     while (live) {
-        const uint64_t s = path_slot(st.p, st.rot);
-        const uint64_t c = load_relaxed(t.lo(s));
+        uint64_t s = 0, c = 0;
+        bool stop = false, more = true;
+        do {                                                // straight-line body, one exit test
+            s = path_slot(st.p, st.rot);
+            c = load_relaxed(t.lo(s));
+            const bool removed = c == kLoRemoved;
+            stop = (c == kLoEmpty) | (c == st.kw.claim) | (removed & !st.scanning);
+            const uint64_t next = (st.p + 1) & slot_mask;
+            if (!stop & removed & (st.first_free == ~0ull)) st.first_free = st.p;   // scanning
+            if (!stop) st.p = next;
+            more = !stop & (next != p_begin);               // else a whole cycle of this phase
+        } while (more);
+        // the slot's word is examined again below: an empty asm keeps the compiler from carrying
+        // the loop's comparison results out of it as lane masks merged on every pass
+        asm volatile("" : "+v"(c));
+        stop = (c == kLoEmpty) | (c == st.kw.claim) | ((c == kLoRemoved) & !st.scanning);
         bool advance = false, done = false, fail = false;
-        if (c == kLoEmpty || c == kLoRemoved) {
-            bool try_claim = !st.scanning;
-            if (st.scanning && c == kLoEmpty) {            // a never-used slot ends the path: the key is absent
+        if (!stop) {                                        // the cycle ended without a slot to act on
+            if (st.scanning && st.first_free != ~0ull) {    // claim the first removed slot of the path
                 st.scanning = false;
-                st.steps = 0;
-                if (st.first_free != ~0ull) st.p = st.first_free;   // claim the first removed slot on the path instead
-                else try_claim = true;
-            } else if (st.scanning) {                       // a removed slot met while scanning
-                if (st.first_free == ~0ull) st.first_free = st.p;
-                advance = true;
+                st.p = p_begin = st.first_free;
+            } else {
+                report(a.status, PKV_EFULL);
+                fail = true;
+            }
+        } else if (c != st.kw.claim) {                      // never used, or removed while claiming
+            bool try_claim = !st.scanning;
+            if (st.scanning) {                              // never used: the key is absent
+                st.scanning = false;
+                if (st.first_free != ~0ull) st.p = p_begin = st.first_free;   // claim the first removed slot on the path instead
+                else {
+                    p_begin = st.p;
+                    try_claim = true;
+                }
             }
             if (try_claim && cas_relaxed(t.lo(s), c, st.kw.claim)) {
                 publish_slot(t, s, st.kw, a.generation, st.want);
@@ -363,7 +389,7 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
                 log_slots[atomicAdd(&log_n, 1u)] = s | (c == kLoRemoved ? kFromRemoved : 0);
                 done = true;
             }                                               // a lost race reads the slot again
-        } else if (c == st.kw.claim) {
+        } else {                                            // the lane's own claim word
             uint64_t hi, loc;
             read_published_pair(t.pair(s), hi, loc);
             if (loc == kEmpty) {                            // claimed, not yet published: read it again
@@ -385,16 +411,13 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
             } else {
                 advance = true;
             }
-        } else {
-            advance = true;                                 // another key
         }
-        if (advance) {
+        if (advance) {                                      // another key under the same claim word
             st.p = (st.p + 1) & slot_mask;
-            if (++st.steps >= t.capacity) {                 // a whole cycle
+            if (st.p == p_begin) {
                 if (st.scanning && st.first_free != ~0ull) {
                     st.scanning = false;
-                    st.steps = 0;
-                    st.p = st.first_free;
+                    st.p = p_begin = st.first_free;
                 } else {
                     report(a.status, PKV_EFULL);
                     fail = true;

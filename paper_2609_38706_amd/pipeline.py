@@ -167,8 +167,11 @@ class TwoStreamRunner:
     Key derivation touches no index state, so the derive of batch k+1 can run while batch k is looked
     up and stored.  Every index operation (lookup, store, rollback) stays on one stream in batch
     order, so the hit lengths and the index contents equal those of running the batches one after
-    another.  The preparation of a batch (key offsets, descriptor digests) also runs on the index
-    stream, after the previous use of that batch's buffers, which keeps it off the derive stream.
+    another.  The preparation of a batch (descriptor digests, key offsets) also runs on the index
+    stream, two passes ahead: the digests of batch k+2 right after the derive of batch k (whose
+    digest buffers they may reuse) and its key offsets after batch k's index work (whose key
+    offsets they may overwrite), so that the derive of batch k+2 is ready to start once the derive
+    of batch k+1 ends and is launched onto a GPU whose index stream has gone quiet.
 
     Both streams have the default priority.  A ``DeviceBatch`` may be reused (its buffers are
     recycled once its previous pass has finished) but not twice in a row.
@@ -196,34 +199,40 @@ class TwoStreamRunner:
         self.s_index.wait_stream(cur)
         if not batches:
             return
+        ready = {}
 
-        def prepare(db):
-            db.key_offsets(self.s_index)
-            db.digest(self.s_index)
+        def mark(j):
             ev = torch.cuda.Event()
             ev.record(self.s_index)
-            return ev
+            ready[j] = ev
 
-        ready = prepare(batches[0])
+        for j in range(min(2, len(batches))):
+            batches[j].digest(self.s_index)
+            batches[j].key_offsets(self.s_index)
+            mark(j)
         for k, db in enumerate(batches):
-            self.s_derive.wait_event(ready)
+            self.s_derive.wait_event(ready.pop(k))
             ev = derive_events[k] if derive_events is not None else None
             if ev is not None:
                 ev[0].record(self.s_derive)
             db.derive(self.s_derive)
             done = ev[1] if ev is not None else torch.cuda.Event()
             done.record(self.s_derive)
-            if k + 1 < len(batches):
-                ready = prepare(batches[k + 1])     # after the index work of its previous pass
             self.s_index.wait_event(done)
+            ahead = batches[k + 2] if k + 2 < len(batches) else None
+            if ahead is not None:
+                ahead.digest(self.s_index)
             if index_work is not None:
                 index_work(k, db, self.s_index)
-                continue
-            with torch.cuda.stream(self.s_index):
-                db.n_new.zero_()
-            db.lookup(self.table, self.s_index)
-            db.store(self.table, self.s_index)
-            if rollback:
-                db.rollback(self.table, self.s_index)
+            else:
+                with torch.cuda.stream(self.s_index):
+                    db.n_new.zero_()
+                db.lookup(self.table, self.s_index)
+                db.store(self.table, self.s_index)
+                if rollback:
+                    db.rollback(self.table, self.s_index)
+            if ahead is not None:
+                ahead.key_offsets(self.s_index)
+                mark(k + 2)
         cur.wait_stream(self.s_derive)
         cur.wait_stream(self.s_index)

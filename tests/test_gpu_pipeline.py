@@ -100,15 +100,19 @@ def test_recycled_buffers_with_rollback_repeat_the_first_pass(pkv):
     idx.store(k0, ko0, np.zeros(pre.n_req, np.int32), locations(ko0, pre.tag))
     k1, ko1 = oracle_keys(run)
     want = idx.lookup(k1, ko1)
-    a, b = gpu_batch(run), gpu_batch(run)
-    order = [a, b] * 5
+    a, b, c = gpu_batch(run), gpu_batch(run), gpu_batch(run)
     runner = TwoStreamRunner(table)
-    runner.run(order, rollback=True)
-    torch.cuda.synchronize()
-    for x in (a, b):
-        assert x.host_status() == 0
-        assert (x.host_hits() == want).all()
-    after = export_sorted(table)
-    assert (before[0] == after[0]).all() and (before[1] == after[1]).all()
+    # two buffer sets alternating (a pass's preparation reuses the buffers of the pass two before),
+    # then three in a cycle, then a single pass
+    for order in ([a, b] * 5, [a, b, c] * 4, [c]):
+        for x in (a, b, c):
+            x.hits.fill_(-7)
+        runner.run(order, rollback=True)
+        torch.cuda.synchronize()
+        for x in set(order):
+            assert x.host_status() == 0
+            assert (x.host_hits() == want).all()
+        after = export_sorted(table)
+        assert (before[0] == after[0]).all() and (before[1] == after[1]).all()
     with pytest.raises(ValueError):
         runner.run([a, a])
