@@ -232,9 +232,10 @@ __device__ __forceinline__ uint32_t first_request(const StoreArgs& a, uint64_t w
     const uint64_t n = a.n_req;
     uint64_t lo = 0, hi = n;
     if (total > 0 && n > 2) {
-        // single precision is close enough for a guess: the doubling steps correct it
+        // single precision and the hardware reciprocal are close enough for a guess: the doubling
+        // steps correct it
         uint64_t g = static_cast<uint64_t>(static_cast<float>(wave_base) *
-                                           (static_cast<float>(n) / static_cast<float>(total)));
+                                           (static_cast<float>(n) * __builtin_amdgcn_rcpf(static_cast<float>(total))));
         if (g >= n) g = n - 1;
         uint64_t step = 1;
         if (a.key_off[g] <= wb) {
@@ -348,22 +349,24 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
     // word, or, once the lane claims, at a removed slot; the rest of the pass handles that slot.
     // A whole cycle of the path is detected by returning to the position the current phase began at.
     while (live) {
-        uint64_t s = 0, c = 0;
-        bool stop = false, more = true;
+        // a removed slot stops the scan only once the lane claims: compared against this word
+        // (while scanning it repeats the never-used marker, which stops the scan anyway)
+        const uint64_t stop_word = st.scanning ? kLoEmpty : kLoRemoved;
+        uint64_t s = 0, c = 0, at = st.p;
+        bool stop = false;
         do {                                                // straight-line body, one exit test
-            s = path_slot(st.p, st.rot);
+            at = st.p;
+            s = path_slot(at, st.rot);
             c = load_relaxed(t.lo(s));
-            const bool removed = c == kLoRemoved;
-            stop = (c == kLoEmpty) | (c == st.kw.claim) | (removed & !st.scanning);
-            const uint64_t next = (st.p + 1) & slot_mask;
-            if (!stop & removed & (st.first_free == ~0ull)) st.first_free = st.p;   // scanning
-            if (!stop) st.p = next;
-            more = !stop & (next != p_begin);               // else a whole cycle of this phase
-        } while (more);
+            stop = (c == kLoEmpty) | (c == st.kw.claim) | (c == stop_word);
+            if ((c == kLoRemoved) & (st.first_free == ~0ull)) st.first_free = at;   // only while scanning
+            st.p = (at + 1) & slot_mask;
+        } while (!stop & (st.p != p_begin));                // else a whole cycle of this phase
+        if (stop) st.p = at;                                // the slot to act on
         // the slot's word is examined again below: an empty asm keeps the compiler from carrying
         // the loop's comparison results out of it as lane masks merged on every pass
         asm volatile("" : "+v"(c));
-        stop = (c == kLoEmpty) | (c == st.kw.claim) | ((c == kLoRemoved) & !st.scanning);
+        stop = (c == kLoEmpty) | (c == st.kw.claim) | (c == stop_word);
         bool advance = false, done = false, fail = false;
         if (!stop) {                                        // the cycle ended without a slot to act on
             if (st.scanning && st.first_free != ~0ull) {    // claim the first removed slot of the path
