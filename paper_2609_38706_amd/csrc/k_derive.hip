@@ -1436,6 +1436,10 @@ __device__ __forceinline__ uint32_t pad_word(uint32_t le, int32_t r) {
 
 __global__ __launch_bounds__(64) void k_digest_pp(const uint8_t* bytes, uint64_t n_bytes, const int64_t* off,
                                                   const uint32_t* len, uint32_t n, uint8_t* out, int32_t* status) {
+    // A batch's digests run beside the previous batch's key derivation and are few wavefronts of
+    // serial rounds: without priority, one that shares a SIMD with a round-issuing wavefront only
+    // gets the slots that wavefront leaves idle and takes several times as long.
+    __builtin_amdgcn_s_setprio(3);
     __shared__ uint32_t stage[kDigestStageWords + 17];   // 17 words of slack: a block's reads are never clamped
     const uint32_t lane = threadIdx.x;
     const uint32_t c = pair_chain(lane);
