@@ -146,3 +146,59 @@ def test_marker_keys_and_wide_epochs(pkv):
         assert (gk == ok).all() and (gl == ol).all() and (ge == idx.dump_epochs()).all(), budget
         assert check_structure(table) == len(idx)
     assert len(idx) == 0
+
+
+def test_store_without_never_used_slots_reuses_removed_ones(pkv):
+    """A table whose slots are all live or removed (none never used): a new key's scan runs a whole
+    cycle of its path without meeting a free slot and then claims the first removed slot on it; a
+    lookup of an absent key ends after one cycle; a batch beyond the capacity reports EFULL."""
+    import torch
+    announce("budget tier: store into a table with no never-used slot")
+    cap = 64
+    table = pkv.Table(cap, epochs=True)
+    idx = oracle.Index(cap)
+    rng = np.random.default_rng(54)
+    keys = rng.integers(0, 256, size=(cap + 20, 16), dtype=np.uint8)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    n_new = torch.zeros(1, dtype=torch.int64, device="cuda")
+    n_ev = torch.zeros(1, dtype=torch.int64, device="cuda")
+
+    def store(lo, hi, epoch):
+        kk = keys[lo:hi]
+        ko = np.array([0, hi - lo], np.int64)
+        locs = np.arange(lo, hi, dtype=np.uint64)
+        pkv.pkv_store_touch(table, torch.from_numpy(kk.copy()).cuda(), torch.from_numpy(ko).cuda(),
+                            torch.zeros(1, dtype=torch.int32, device="cuda"),
+                            torch.from_numpy(locs.view(np.int64)).cuda(), n_new, status, epoch)
+        return idx.store_touch(kk, ko, np.zeros(1, np.int32), locs, epoch)
+
+    def same():
+        gk, gl, ge = raw_entries(table)
+        ok, ol = idx.dump()
+        assert (gk == ok).all() and (gl == ol).all() and (ge == idx.dump_epochs()).all()
+        assert check_structure(table) == len(idx)
+
+    assert store(0, 16, 1) == 0 and store(16, cap, 2) == 0       # every slot taken
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    same()
+    pkv.pkv_table_evict(table, cap - 16, n_ev)                    # the 16 entries of epoch 1 removed
+    assert int(n_ev.item()) == idx.evict(cap - 16) == 16
+    keys_now, locs_now = raw_table(table)
+    assert (locs_now[:cap] == EMPTY).sum() == 0 and (locs_now[:cap] == TOMB).sum() == 16
+    same()
+    assert store(cap, cap + 10, 3) == 0                           # 10 new keys into removed slots
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    same()
+    # a lookup of stored keys followed by an absent one (its path has no never-used slot)
+    both = np.concatenate([keys[16:20], keys[cap + 19:cap + 20]])
+    hits = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pkv.pkv_lookup_prefix(table, torch.from_numpy(both.copy()).cuda(),
+                          torch.tensor([0, 5], dtype=torch.int64, device="cuda"), hits, status)
+    torch.cuda.synchronize()
+    assert int(hits.item()) == 4 and int(status.item()) == 0
+    # 7 more new keys with 6 removed slots left: beyond the capacity
+    assert store(cap + 10, cap + 17, 4) == pkv.PKV_EFULL
+    torch.cuda.synchronize()
+    assert int(status.item()) == pkv.PKV_EFULL
