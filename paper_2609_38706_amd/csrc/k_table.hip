@@ -223,8 +223,9 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
 // ---- store ------------------------------------------------------------------------------------
 // One lane per key of the batch; candidate = key j of request r with j >= hits[r].  A wavefront
 // covers 64 consecutive keys: one (wave-uniform) search finds the request of its first key, and
-// each lane walks forward over the few request boundaries inside the wavefront.  The key and its
-// location are loaded before that search, so their round trip overlaps it.
+// each lane walks forward over the few request boundaries inside the wavefront.  Only candidates
+// load their key and location, after that search: a third of the keys of a typical batch lie in hit
+// prefixes, and whole wavefronts of them then read nothing but the offsets and hit lengths.
 struct StoreArgs {
     Tab t;
     const uint4* keys;
@@ -329,12 +330,6 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
     const uint64_t slot_mask = t.capacity - 1;
     const uint64_t k = wave_base + lane;
     const bool in_batch = static_cast<int64_t>(k) < total;
-    uint4 key = make_uint4(0u, 0u, 0u, 0u);
-    uint64_t want = 0;
-    if (in_batch) {                                         // issued before the request search
-        key = a.keys[k];
-        want = a.locs[k];
-    }
     bool live = false;
     if (static_cast<int64_t>(wave_base) < total) {
         uint32_t r = first_request(a, wave_base, total);
@@ -345,6 +340,13 @@ __global__ __launch_bounds__(kStoreThreads) void k_store(StoreArgs a) {
             if (h < 0) h = 0;
             live = j >= h;
         }
+    }
+    // only candidates read their key and location (keys inside a hit prefix are never stored)
+    uint4 key = make_uint4(0u, 0u, 0u, 0u);
+    uint64_t want = 0;
+    if (live) {
+        key = a.keys[k];
+        want = a.locs[k];
     }
     if (live && want >= PKV_LOC_LIMIT) {
         report(a.status, PKV_ERESERVED);
