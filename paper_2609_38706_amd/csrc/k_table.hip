@@ -95,21 +95,16 @@ __global__ __launch_bounds__(256) void k_init(uint4* t, uint64_t capacity) {
         t[i] = (i & 1) ? make_uint4(~0u, ~0u, ~0u, ~0u) : make_uint4(~0u, ~0u, 0u, 0u);
 }
 
-// ---- lookup: a group of kLookupLanes lanes per request ---------------------------------------
+// ---- lookup: one wavefront per request --------------------------------------------------------
 // A request's keys are probed in windows, one lane per key; a lane loads its key's bucket (eight
 // 16-byte loads issued together: each slot's {claim word, tag} and {key bytes 8..15, location}),
 // and the next window's keys are fetched while the current window's buckets are in flight.  A
 // ballot finds the first absent key, which ends the request.  The first window holds
-// kFirstWindow keys and each later window twice as many, up to the group's lanes: probes past a
-// request's first miss are wasted bandwidth (at most a window less one per request), so short
-// prefixes (and misses on the first key) probe few keys, while long prefixes soon reach full
-// windows.  A wavefront holds 64 / kLookupLanes requests and runs until the last of them ends.
+// kFirstWindow keys and each later window twice as many, up to 64: probes past a request's first
+// miss are wasted bandwidth, so short prefixes (and misses on the first key) probe few keys,
+// while long prefixes soon reach full 64-key windows.
 constexpr int kLookupWaves = 4;
-constexpr uint32_t kLookupLanes = 64;
 constexpr uint32_t kFirstWindow = 16;
-static_assert(kLookupLanes == 16 || kLookupLanes == 32 || kLookupLanes == 64, "lanes per request");
-static_assert(kFirstWindow <= kLookupLanes, "first window");
-constexpr uint32_t kLookupGroups = 64 / kLookupLanes;     // requests per wavefront
 
 struct Bucket {
     uint4 c[4];      // slot j: {claim word, tag}
@@ -152,72 +147,57 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
                                                             uint64_t n_keys, int32_t* __restrict__ hits,
                                                             uint32_t* epochs, uint32_t epoch, int32_t* status) {
     const uint32_t lane = lane_id();
-    const uint32_t g = lane / kLookupLanes;                     // the lane's group in the wavefront
-    const uint32_t gl = lane % kLookupLanes;                    // the lane's place in its group
-    const uint32_t wave = blockIdx.x * kLookupWaves + (threadIdx.x >> 6);
-    if (static_cast<uint64_t>(wave) * kLookupGroups >= n_req) return;   // wave-uniform
-    const uint32_t r = wave * kLookupGroups + g;
-    const bool leader = gl == 0;
-    int64_t k0 = 0, n = 0;
-    bool active = r < n_req;
-    if (active) {
-        const int64_t a0 = key_off[r], a1 = key_off[r + 1];
-        if (a0 < 0 || a1 < a0 || static_cast<uint64_t>(a1) > n_keys) {
-            if (leader) {
-                report(status, PKV_ELAYOUT);
-                hits[r] = 0;
-            }
-            active = false;
-        } else {
-            k0 = a0;
-            n = a1 - a0;
-            if (n == 0) {
-                if (leader) hits[r] = 0;
-                active = false;
-            }
+    const uint32_t r = blockIdx.x * kLookupWaves + (threadIdx.x >> 6);
+    if (r >= n_req) return;
+    const int64_t k0 = key_off[r], k1 = key_off[r + 1];
+    if (k0 < 0 || k1 < k0 || static_cast<uint64_t>(k1) > n_keys) {
+        if (lane == 0) {
+            report(status, PKV_ELAYOUT);
+            hits[r] = 0;
         }
+        return;
+    }
+    const int64_t n = k1 - k0;
+    if (n == 0) {
+        if (lane == 0) hits[r] = 0;
+        return;
     }
     const uint64_t bmask = capacity / kSlotsPerBucket - 1;
     const uint4 marker = make_uint4(~0u, ~0u, ~0u, ~0u);
 
-    // Key idx of the lane's request, or the marker past its end (the load index stays inside the
-    // request, so the load is in bounds whenever it is made: only for an active group, n > 0).
+    // Key idx of the request, or the marker for a lane outside the window or past the request's
+    // end (no load is made for those).
     auto key_at = [&](int64_t idx, bool want) {
         if (!want || idx >= n) return marker;
         return keys[k0 + idx];
     };
     int64_t base = 0;
     uint32_t width = kFirstWindow;
-    uint4 nk = key_at(gl, active && gl < width);
+    uint4 nk = key_at(lane, lane < width);
     int64_t h = n;
-    const uint64_t gmask = kLookupLanes == 64 ? ~0ull : ((1ull << kLookupLanes) - 1);
-    while (__ballot(active)) {
+    while (base < n) {
         const uint4 ck = nk;
-        const bool v = active && gl < width && base + gl < n;
+        const bool v = lane < width && base + lane < n;
         const uint64_t bk = home_bucket(ck, bmask);
         Bucket bucket;
         if (v) load_bucket(t, bk, bucket);
-        // next window: twice as wide, up to the group
-        const uint32_t next_width = width * 2 < kLookupLanes ? width * 2 : kLookupLanes;
+        // next window: twice as wide, up to the wavefront
+        const uint32_t next_width = width * 2 < 64 ? width * 2 : 64;
         const int64_t next_base = base + width;
-        nk = key_at(next_base + gl, active && next_base < n && gl < next_width);
+        nk = key_at(next_base + lane, next_base < n && lane < next_width);
         const int64_t fslot = v ? probe_key(t, capacity, bmask, ck, bk, bucket) : -1;
-        const uint64_t miss = (__ballot(v && fslot < 0) >> (g * kLookupLanes)) & gmask;
+        const uint64_t miss = __ballot(v && fslot < 0);
         const int64_t stop = miss ? base + __builtin_ctzll(miss) : -1;
-        if (epochs && fslot >= 0 && (stop < 0 || base + gl < stop))   // a touching lookup refreshes hits
+        if (epochs && fslot >= 0 && (stop < 0 || base + lane < stop))   // a touching lookup refreshes hits
             epochs[fslot] = epoch;
-        if (active) {
-            if (stop >= 0) {
-                h = stop;
-                active = false;
-            } else if (next_base >= n) {
-                active = false;
-            }
+        if (stop >= 0) {
+            h = stop;
+            break;
         }
         base = next_base;
         width = next_width;
     }
-    if (r < n_req && leader && n > 0) hits[r] = static_cast<int32_t>(h < n ? h : n);
+    if (lane == 0) hits[r] = static_cast<int32_t>(h < n ? h : n);
 }
 
 // ---- store ------------------------------------------------------------------------------------
@@ -759,9 +739,7 @@ int launch_lookup(const uint64_t* table, uint64_t capacity, const uint8_t* keys,
                   uint32_t n_req, uint64_t n_keys, int32_t* hits, uint32_t* epochs, uint32_t epoch, int32_t* status,
                   hipStream_t s) {
     if (n_req == 0) return PKV_OK;
-    const uint64_t waves = (n_req + kLookupGroups - 1) / kLookupGroups;
-    hipLaunchKernelGGL(k_lookup, dim3(static_cast<unsigned>((waves + kLookupWaves - 1) / kLookupWaves)),
-                       dim3(64 * kLookupWaves), 0, s,
+    hipLaunchKernelGGL(k_lookup, dim3((n_req + kLookupWaves - 1) / kLookupWaves), dim3(64 * kLookupWaves), 0, s,
                        reinterpret_cast<const uint4*>(table), capacity, reinterpret_cast<const uint4*>(keys),
                        key_off, n_req, n_keys, hits, epochs, epoch, status);
     return check_launch("pkv_lookup_prefix");
