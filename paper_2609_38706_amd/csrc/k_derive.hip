@@ -1064,10 +1064,37 @@ struct PairProduction {
     uint32_t w[8];
 };
 
-__device__ __forceinline__ void load_production_pair(const int32_t* tp, uint32_t B, uint32_t m, int64_t n, int64_t g,
-                                                     bool odd, PairProduction& pr) {
-    const int64_t key = g / m;
-    const uint32_t c = static_cast<uint32_t>(g - key * m) + 1;
+// Where production g sits: key g / m, token compression c = g % m + 1 of that key, ring slot g % 3.
+// The loops step it one production at a time (wave-uniform scalars: no division per compression).
+struct ProdPos {
+    int64_t key;
+    uint32_t c;
+    uint32_t slot;
+};
+
+__device__ __forceinline__ ProdPos prod_pos(int64_t g, uint32_t m) {
+    ProdPos p;
+    p.key = g / m;
+    p.c = static_cast<uint32_t>(g - p.key * m) + 1;
+    p.slot = static_cast<uint32_t>(g % 3);
+    return p;
+}
+
+__device__ __forceinline__ ProdPos prod_next(ProdPos p, uint32_t m) {
+    if (p.c == m) {
+        p.c = 1;
+        ++p.key;
+    } else {
+        ++p.c;
+    }
+    p.slot = p.slot == 2 ? 0 : p.slot + 1;
+    return p;
+}
+
+__device__ __forceinline__ void load_production_pair(const int32_t* tp, uint32_t B, uint32_t m, int64_t n,
+                                                     const ProdPos& at, bool odd, PairProduction& pr) {
+    const int64_t key = at.key;
+    const uint32_t c = at.c;
     const uint32_t o = odd ? 1u : 0u;
 #pragma unroll
     for (int k = 0; k < 4; ++k) pr.head[k] = 0u;
@@ -1095,9 +1122,9 @@ __device__ __forceinline__ void load_production_pair(const int32_t* tp, uint32_t
 // also its parity of compression 1's token words.
 template <typename Shared>
 __device__ __forceinline__ void produce_comp_pair(Shared& sh, uint32_t chain, bool odd, const PairK& pk, uint32_t m,
-                                                  uint32_t bitlen, int64_t g, const PairProduction& pr) {
-    const int64_t key = g / m;
-    const uint32_t c = static_cast<uint32_t>(g - key * m) + 1;
+                                                  uint32_t bitlen, const ProdPos& at, const PairProduction& pr) {
+    const int64_t key = at.key;
+    const uint32_t c = at.c;
     const uint32_t o = odd ? 1u : 0u;
     if (c == 1) {
         const int kb = static_cast<int>(key & 1);
@@ -1123,7 +1150,7 @@ __device__ __forceinline__ void produce_comp_pair(Shared& sh, uint32_t chain, bo
         own[6] = 0u;
         own[7] = pk.m & bitlen;
     }
-    uint32_t* col = reinterpret_cast<uint32_t*>(&sh.kwt[static_cast<int>(g % 3)][0][chain]) + o;
+    uint32_t* col = reinterpret_cast<uint32_t*>(&sh.kwt[at.slot][0][chain]) + o;
 #pragma unroll
     for (int k = 0; k < 8; ++k) col[((2 * k) >> 2) * (kPpChains * 4) + ((2 * k) & 3)] = own[k] + pk.k[k];
     uint32_t v[8];                                     // own words, newest first
@@ -1182,6 +1209,7 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
         uint32_t kwa[16], kwb[16];
 #pragma unroll
         for (int j = 0; j < 4; ++j) get4(&sh.kwt[0][j][c], kwa + 4 * j);
+        uint32_t slot = 0;                                     // ring slot of the next token compression
         for (int64_t i = 0; i < nmax; ++i) {
             const int kb = static_cast<int>(i & 1);
             uint32_t x[4], h[4], kw[16], q;
@@ -1206,8 +1234,8 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
             for (int j = 0; j < 4; ++j) h[j] = x[j] + iv[j];
             __syncthreads();                                   // end of compression 1
             for (uint32_t cc = 1; cc <= m; ++cc) {
-                const int64_t g = i * m + (cc - 1);            // produced two compressions ago
-                const int slot = static_cast<int>(g % 3), nslot = static_cast<int>((g + 1) % 3);
+                // token compression i * m + cc - 1, produced two compressions ago
+                const uint32_t nslot = slot == 2 ? 0u : slot + 1;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) x[j] = h[j];
                 q = (x[3] + kwa[0]) & pl.nm;
@@ -1236,6 +1264,7 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
                     }
                 }
                 __syncthreads();                               // end of token compression cc
+                slot = nslot;
             }
         }
     } else {
@@ -1246,14 +1275,17 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
         dsel[1] = odd ? dg[3] : dg[2];
         uint32_t* kw1hi_col = reinterpret_cast<uint32_t*>(&sh.kw1hi[0][c]) + (odd ? 1 : 0);
         const PairK pk = make_pair_k(odd);
-        const int64_t total = nmax * m;                        // token compressions of the workgroup
         PairProduction p0, p1, p2;
-        load_production_pair(tp, B, m, n, 0, odd, p0);
-        load_production_pair(tp, B, m, n, 1, odd, p1);
-        produce_comp_pair(sh, c, odd, pk, m, bitlen, 0, p0);
-        produce_comp_pair(sh, c, odd, pk, m, bitlen, 1, p1);
-        load_production_pair(tp, B, m, n, 2, odd, p0);         // p0, p1 = productions g + 2, g + 3
-        load_production_pair(tp, B, m, n, 3, odd, p1);
+        const ProdPos g0 = prod_pos(0, m), g1 = prod_next(g0, m);
+        load_production_pair(tp, B, m, n, g0, odd, p0);
+        load_production_pair(tp, B, m, n, g1, odd, p1);
+        produce_comp_pair(sh, c, odd, pk, m, bitlen, g0, p0);
+        produce_comp_pair(sh, c, odd, pk, m, bitlen, g1, p1);
+        ProdPos make = prod_next(g1, m);                       // production g, made during compression (i, cc)
+        ProdPos fetch = prod_next(make, m);
+        load_production_pair(tp, B, m, n, make, odd, p0);      // p0, p1 = productions g, g + 1
+        load_production_pair(tp, B, m, n, fetch, odd, p1);
+        fetch = prod_next(fetch, m);                           // production g + 2
         __syncthreads();                                       // prologue
         for (int64_t i = 0; i < nmax; ++i) {
             const int kb = static_cast<int>(i & 1);
@@ -1275,11 +1307,12 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
             __syncthreads();
             __syncthreads();                                   // end of compression 1
             for (uint32_t cc = 1; cc <= m; ++cc) {
-                const int64_t g = i * m + (cc - 1) + 2;        // production made during compression (i, cc)
                 p2 = p0;
                 p0 = p1;
-                load_production_pair(tp, B, m, n, g + 2, odd, p1);
-                if (g < total) produce_comp_pair(sh, c, odd, pk, m, bitlen, g, p2);
+                load_production_pair(tp, B, m, n, fetch, odd, p1);
+                if (make.key < nmax) produce_comp_pair(sh, c, odd, pk, m, bitlen, make, p2);
+                make = prod_next(make, m);
+                fetch = prod_next(fetch, m);
                 __syncthreads();                               // end of token compression cc
             }
         }
