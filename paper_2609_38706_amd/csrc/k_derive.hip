@@ -258,20 +258,6 @@ __device__ __forceinline__ bool pair_is_a(uint32_t lane) { return (lane & 8u) !=
 // The compiler puts 4-byte instructions (s_nop, VOP2) between asm statements, so each block of
 // rounds starts by padding itself back to an 8-byte boundary (the assembler pads with s_nop).
 #define PKV_ALIGN8 ".p2align 3\n"
-#define PKV_ROUNDS4_OPERANDS                                                                      \
-    : [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [q] "+v"(q), [a] "+v"(x0), [b] "+v"(x1),  \
-      [c] "+v"(x2), [d] "+v"(x3)                                                                  \
-    : [m] "v"(pl.m), [r1] "v"(pl.r1), [r2] "v"(pl.r2), [r3] "v"(pl.r3), [k1] "v"(k1), [k2] "v"(k2),     \
-      [k3] "v"(k3)
-
-// Four paired rounds; k1..k4 are K + W of the four rounds that follow each of them.
-__device__ __forceinline__ void pair_rounds4(uint32_t& x0, uint32_t& x1, uint32_t& x2, uint32_t& x3, uint32_t& q,
-                                             const PairLane& pl, uint32_t k1, uint32_t k2, uint32_t k3,
-                                             uint32_t k4) {
-    uint32_t t0, t1, t2;
-    asm volatile(PKV_ALIGN8 PKV_PAIR_ROUND(a, b, c, d, k1) PKV_PAIR_ROUND(d, a, b, c, k2) PKV_PAIR_ROUND(c, d, a, b, k3)
-                     PKV_PAIR_ROUND(b, c, d, a, k4) PKV_ROUNDS4_OPERANDS, [k4] "v"(k4));
-}
 
 // 16 paired rounds as one asm statement, for K + W words that are all in registers already (the
 // compiler's separator and the alignment padding then come once per 16 rounds instead of once
@@ -292,20 +278,9 @@ __device__ __forceinline__ void pair_rounds16_regs(uint32_t x[4], uint32_t& q, c
                    [k12] "v"(kw[12]), [k13] "v"(kw[13]), [k14] "v"(kw[14]), [k15] "v"(kw[15]), [k16] "v"(after));
 }
 #undef PKV_PAIR_ROUNDS4
-#undef PKV_ROUNDS4_OPERANDS
 #undef PKV_ALIGN8
 #undef PKV_PAIR_ROUND
 #undef PKV_ROUND_HEAD
-
-// 16 paired rounds; kw[j] = K + W of round t0 + j, `after` = K + W of round t0 + 16 (any value
-// when the caller recomputes q before the next round).
-__device__ __forceinline__ void pair_rounds16(uint32_t x[4], uint32_t& q, const PairLane& pl, const uint32_t* kw,
-                                              uint32_t after) {
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[1], kw[2], kw[3], kw[4]);
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[5], kw[6], kw[7], kw[8]);
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[9], kw[10], kw[11], kw[12]);
-    pair_rounds4(x[0], x[1], x[2], x[3], q, pl, kw[13], kw[14], kw[15], after);
-}
 
 // v of the pair's other lane (DPP row_ror:8).
 __device__ __forceinline__ uint32_t lane_swap(uint32_t v) {
@@ -1220,14 +1195,14 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) x[j] = iv[j];
             q = (x[3] + kw[0]) & pl.nm;
-            pair_rounds16(x, q, pl, kw, 0u);               // rounds 0..15
+            pair_rounds16_regs(x, q, pl, kw, 0u);               // rounds 0..15
             __syncthreads();
 #pragma unroll
             for (int ph = 0; ph < 3; ++ph) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) get4(&sh.kw1hi[4 * ph + j][c], kw + 4 * j);
                 q = (x[3] + kw[0]) & pl.nm;
-                pair_rounds16(x, q, pl, kw, 0u);
+                pair_rounds16_regs(x, q, pl, kw, 0u);
                 if (ph < 2) __syncthreads();
             }
 #pragma unroll
@@ -1241,16 +1216,16 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pp(ChainArgs a) {
                 q = (x[3] + kwa[0]) & pl.nm;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) get4(&sh.kwt[slot][4 + j][c], kwb + 4 * j);
-                pair_rounds16(x, q, pl, kwa, kwb[0]);      // rounds 0..15
+                pair_rounds16_regs(x, q, pl, kwa, kwb[0]);      // rounds 0..15
 #pragma unroll
                 for (int j = 0; j < 4; ++j) get4(&sh.kwt[slot][8 + j][c], kwa + 4 * j);
-                pair_rounds16(x, q, pl, kwb, kwa[0]);      // rounds 16..31
+                pair_rounds16_regs(x, q, pl, kwb, kwa[0]);      // rounds 16..31
 #pragma unroll
                 for (int j = 0; j < 4; ++j) get4(&sh.kwt[slot][12 + j][c], kwb + 4 * j);
-                pair_rounds16(x, q, pl, kwa, kwb[0]);      // rounds 32..47
+                pair_rounds16_regs(x, q, pl, kwa, kwb[0]);      // rounds 32..47
 #pragma unroll
                 for (int j = 0; j < 4; ++j) get4(&sh.kwt[nslot][j][c], kwa + 4 * j);
-                pair_rounds16(x, q, pl, kwb, 0u);          // rounds 48..63
+                pair_rounds16_regs(x, q, pl, kwb, 0u);          // rounds 48..63
 #pragma unroll
                 for (int j = 0; j < 4; ++j) h[j] += x[j];
                 if (cc == m) {                                 // h on the a lane is the key
