@@ -852,12 +852,39 @@ struct Production {
     uint32_t w[16];
 };
 
+// Where production g sits: key g / m, token compression c = g % m + 1 of that key, ring slot g % 3.
+// The loops step it one production at a time (wave-uniform scalars: no division per compression).
+struct ProdPos {
+    int64_t key;
+    uint32_t c;
+    uint32_t slot;
+};
+
+__device__ __forceinline__ ProdPos prod_pos(int64_t g, uint32_t m) {
+    ProdPos p;
+    p.key = g / m;
+    p.c = static_cast<uint32_t>(g - p.key * m) + 1;
+    p.slot = static_cast<uint32_t>(g % 3);
+    return p;
+}
+
+__device__ __forceinline__ ProdPos prod_next(ProdPos p, uint32_t m) {
+    if (p.c == m) {
+        p.c = 1;
+        ++p.key;
+    } else {
+        ++p.c;
+    }
+    p.slot = p.slot == 2 ? 0 : p.slot + 1;
+    return p;
+}
+
 // Production g (global, g = key * m + (c - 1)) of one lane: compression c (1..m) of `key`.
 // Every word is written on every path (zeros past the lane's last key or past the block).
-__device__ __forceinline__ void load_production(const int32_t* tp, uint32_t B, uint32_t m, int64_t n, int64_t g,
-                                                Production& pr) {
-    const int64_t key = g / m;
-    const uint32_t c = static_cast<uint32_t>(g - key * m) + 1;
+__device__ __forceinline__ void load_production(const int32_t* tp, uint32_t B, uint32_t m, int64_t n,
+                                                const ProdPos& at, Production& pr) {
+    const int64_t key = at.key;
+    const uint32_t c = at.c;
 #pragma unroll
     for (int q = 0; q < 8; ++q) pr.head[q] = 0u;
 #pragma unroll
@@ -880,10 +907,10 @@ __device__ __forceinline__ void load_production(const int32_t* tp, uint32_t B, u
 }
 
 template <typename Shared>
-__device__ __forceinline__ void produce_comp(Shared& sh, uint32_t lane, uint32_t m, uint32_t bitlen, int64_t g,
+__device__ __forceinline__ void produce_comp(Shared& sh, uint32_t lane, uint32_t m, uint32_t bitlen, const ProdPos& at,
                                              const Production& pr) {
-    const int64_t key = g / m;
-    const uint32_t c = static_cast<uint32_t>(g - key * m) + 1;
+    const int64_t key = at.key;
+    const uint32_t c = at.c;
     if (c == 1) {
         const int kb = static_cast<int>(key & 1);
         uint32_t v[8], kv[8];
@@ -906,7 +933,7 @@ __device__ __forceinline__ void produce_comp(Shared& sh, uint32_t lane, uint32_t
         for (int q = 9; q < 15; ++q) w[q] = 0u;
         w[15] = bitlen;
     }
-    const int slot = static_cast<int>(g % 3);
+    const uint32_t slot = at.slot;
 #pragma unroll
     for (int q = 0; q < 16; ++q) kw[q] = w[q] + kRoundK[q];
     lds_put16(&sh.kwt[slot][0], lane, kw);
@@ -942,6 +969,7 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pc(ChainArgs a) {
         for (int q = 0; q < 4; ++q) dgk[q] = dg[q] + kRoundK[4 + q];
         put4(&sh.prev[lane], prev);
         __syncthreads();                                       // prologue
+        uint32_t slot = 0;                                     // ring slot of the next token compression
         for (int64_t i = 0; i < nmax; ++i) {
             const int kb = static_cast<int>(i & 1);
             uint32_t s[8], h[8], kw[16];
@@ -964,10 +992,10 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pc(ChainArgs a) {
             for (int q = 0; q < 8; ++q) h[q] = s[q] + kInitH[q];
             __syncthreads();                                   // end of compression 1
             for (uint32_t c = 1; c <= m; ++c) {
-                const int64_t g = i * m + (c - 1);             // produced two compressions ago
+                // token compression i * m + c - 1, produced two compressions ago, in ring slot `slot`
                 uint32_t kwc[64];
 #pragma unroll
-                for (int ph = 0; ph < 4; ++ph) lds_get16(&sh.kwt[g % 3][4 * ph], lane, kwc + 16 * ph);
+                for (int ph = 0; ph < 4; ++ph) lds_get16(&sh.kwt[slot][4 * ph], lane, kwc + 16 * ph);
 #pragma unroll
                 for (int q = 0; q < 8; ++q) s[q] = h[q];
 #pragma unroll
@@ -981,18 +1009,22 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pc(ChainArgs a) {
                     put4(&sh.prev[lane], prev);
                 }
                 __syncthreads();                               // end of token compression c
+                slot = slot == 2 ? 0u : slot + 1;
             }
         }
     } else {
         // ---------------- helper ----------------
-        const int64_t total = nmax * m;                        // token compressions of the wavefront
         Production p0, p1, p2;
-        load_production(tp, B, m, n, 0, p0);
-        load_production(tp, B, m, n, 1, p1);
-        produce_comp(sh, lane, m, bitlen, 0, p0);
-        produce_comp(sh, lane, m, bitlen, 1, p1);
-        load_production(tp, B, m, n, 2, p0);                   // p0, p1 = productions g + 2, g + 3
-        load_production(tp, B, m, n, 3, p1);
+        const ProdPos g0 = prod_pos(0, m), g1 = prod_next(g0, m);
+        load_production(tp, B, m, n, g0, p0);
+        load_production(tp, B, m, n, g1, p1);
+        produce_comp(sh, lane, m, bitlen, g0, p0);
+        produce_comp(sh, lane, m, bitlen, g1, p1);
+        ProdPos make = prod_next(g1, m);                       // production g, made during compression (i, c)
+        ProdPos fetch = prod_next(make, m);
+        load_production(tp, B, m, n, make, p0);                // p0, p1 = productions g, g + 1
+        load_production(tp, B, m, n, fetch, p1);
+        fetch = prod_next(fetch, m);                           // production g + 2
         __syncthreads();                                       // prologue
         for (int64_t i = 0; i < nmax; ++i) {
             const int kb = static_cast<int>(i & 1);
@@ -1013,11 +1045,12 @@ __global__ __launch_bounds__(kPcThreads) void k_derive_m16_pc(ChainArgs a) {
             __syncthreads();
             __syncthreads();                                   // end of compression 1
             for (uint32_t c = 1; c <= m; ++c) {
-                const int64_t g = i * m + (c - 1) + 2;         // production made during compression (i, c)
                 p2 = p0;
                 p0 = p1;
-                load_production(tp, B, m, n, g + 2, p1);
-                if (g < total) produce_comp(sh, lane, m, bitlen, g, p2);
+                load_production(tp, B, m, n, fetch, p1);
+                if (make.key < nmax) produce_comp(sh, lane, m, bitlen, make, p2);
+                make = prod_next(make, m);
+                fetch = prod_next(fetch, m);
                 __syncthreads();                               // end of token compression c
             }
         }
@@ -1038,33 +1071,6 @@ struct PairProduction {
     uint32_t head[4];
     uint32_t w[8];
 };
-
-// Where production g sits: key g / m, token compression c = g % m + 1 of that key, ring slot g % 3.
-// The loops step it one production at a time (wave-uniform scalars: no division per compression).
-struct ProdPos {
-    int64_t key;
-    uint32_t c;
-    uint32_t slot;
-};
-
-__device__ __forceinline__ ProdPos prod_pos(int64_t g, uint32_t m) {
-    ProdPos p;
-    p.key = g / m;
-    p.c = static_cast<uint32_t>(g - p.key * m) + 1;
-    p.slot = static_cast<uint32_t>(g % 3);
-    return p;
-}
-
-__device__ __forceinline__ ProdPos prod_next(ProdPos p, uint32_t m) {
-    if (p.c == m) {
-        p.c = 1;
-        ++p.key;
-    } else {
-        ++p.c;
-    }
-    p.slot = p.slot == 2 ? 0 : p.slot + 1;
-    return p;
-}
 
 __device__ __forceinline__ void load_production_pair(const int32_t* tp, uint32_t B, uint32_t m, int64_t n,
                                                      const ProdPos& at, bool odd, PairProduction& pr) {
@@ -1765,7 +1771,7 @@ int launch_derive(const int32_t* tokens, uint64_t n_tokens, const int64_t* tok_o
                   const uint8_t* digests, uint32_t block, const int64_t* key_off, uint64_t n_keys, uint8_t* keys,
                   int32_t* status, hipStream_t s) {
     if (n_req == 0) return PKV_OK;
-    ChainArgs a{tokens, n_tokens, tok_off, n_req, digests, block, key_off, n_keys, keys, status};
+    ChainArgs a{tokens, n_tokens, tok_off, n_req, digests, block, key_off, n_keys, keys, status, nullptr, 0, nullptr};
     const dim3 grid((n_req + kDeriveThreads - 1) / kDeriveThreads);
     const unsigned pp_grid = (n_req + kPpChains - 1) / kPpChains;
     const unsigned pp2_grid = (n_req + 2 * kPpChains - 1) / (2 * kPpChains);

@@ -123,8 +123,8 @@ __device__ __forceinline__ void load_bucket(const uint4* __restrict__ t, uint64_
 // Probe of one key (lane-private) whose home bucket is already loaded in bk.  Returns the slot
 // holding the key, or -1 when it is absent; continues to later buckets while a bucket neither
 // matches nor holds a never-used slot.
-__device__ __forceinline__ int64_t probe_key(const uint4* __restrict__ t, uint64_t capacity, uint64_t bmask,
-                                             const uint4& key, uint64_t b, Bucket& bk) {
+__device__ __forceinline__ int64_t probe_key(const uint4* __restrict__ t, uint64_t bmask, const uint4& key,
+                                             uint64_t b, Bucket& bk) {
     const KeyWords kw = key_words(key);
     const uint64_t n_buckets = bmask + 1;
     for (uint64_t it = 0; it < n_buckets; ++it) {
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(64 * kLookupWaves) void k_lookup(const uint4* __res
         const uint32_t next_width = width * 2 < 64 ? width * 2 : 64;
         const int64_t next_base = base + width;
         nk = key_at(next_base + lane, next_base < n && lane < next_width);
-        const int64_t fslot = v ? probe_key(t, capacity, bmask, ck, bk, bucket) : -1;
+        const int64_t fslot = v ? probe_key(t, bmask, ck, bk, bucket) : -1;
         const uint64_t miss = __ballot(v && fslot < 0);
         const int64_t stop = miss ? base + __builtin_ctzll(miss) : -1;
         if (epochs && fslot >= 0 && (stop < 0 || base + lane < stop))   // a touching lookup refreshes hits

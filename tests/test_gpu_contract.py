@@ -79,7 +79,7 @@ def test_ragged_with_empty_requests_in_between(pkv):
 
 
 @pytest.mark.parametrize("n_req,block", [(8192, 16), (8193, 16), (16384, 16), (16385, 16), (8192, 32), (8193, 32),
-                                         (16385, 48)])
+                                         (8193, 48), (9000, 256), (16385, 48)])
 def test_derive_kernels_agree_at_the_switches(pkv, n_req, block):
     """The kernel switches at 256 compute units.  B = 16: up to 8192 requests run one lane-pair
     consumer/helper pair per workgroup (32 chains each), 8193..16384 two pairs per workgroup, from
